@@ -1,0 +1,339 @@
+"""Benchmark of the multiplexed decoder-layer iteration on one MI355X.
+
+A step is one mx_layer_step over one mixed batch (prefill chunks co-batched
+with decodes): token map, RMSNorm, QKV GEMM, RoPE + KV append, paged attention
+(one launch for prefill and decode rows), O GEMM + residual, RMSNorm, gate/up
+GEMM + SwiGLU, down GEMM + residual.  Inputs are synthetic, seeded, and
+resident in HBM before the timed region.
+
+Default workload: the Llama-7B-shaped layer (hidden 4096, 32 x 128 MHA, FFN
+11008) with 64 decodes (contexts uniform in [512, 2048]) plus one 512-token
+prefill chunk; the decode-only point (P = 0) is timed beside it to give the
+latency-vs-mixed-prefill curve.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "mixed-batch layer iteration latency (µs) & tokens/s vs prefill tokens mixed"
+HBM_PEAK = 8.0e12        # bytes/s, MI355X
+MFMA_BF16_PEAK = 2.5e15  # flop/s, dense bf16
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=int(os.environ.get("WORLD_SIZE", "1")))
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="c2", help="layer shape c1..c5")
+    ap.add_argument("--prefill", type=int, nargs="*", default=None,
+                    help="mixed prefill tokens per point (default: the shape's sweep)")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--kernels", action="store_true", default=True)
+    ap.add_argument("--copy-calib-mib", type=int, default=0,
+                    help="run one plain device copy of this many MiB before timing (the "
+                         "known-size reference that scales rocprofv3 byte counters)")
+    return ap.parse_args()
+
+
+def source_sha(rel):
+    import hashlib
+    with open(os.path.join(ROOT, rel), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(kernel, workload, source):
+    """HBM bytes per launch of `kernel` on `workload` from the committed
+    rocprofv3 counter summary (profiles/traffic_<kernel>_<workload>.json), or
+    None when there is none or the kernel source changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_sha256") != source_sha(source):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def algorithmic(cfg, b):
+    """Algorithmic bytes / flops of the iteration's parts (what the method must
+    move or compute: no padding, K/V read once per KV head)."""
+    import numpy as np
+    import workload as wl
+    H, F, nq, nkv, d = cfg.hidden, cfg.ffn, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    T = b.T
+    KVB = cfg.kv_bytes_per_token
+    gemms = {
+        "qkv": (T, cfg.qkv_rows, H),
+        "o": (T, H, nq * d),
+        "gate_up": (T, 2 * F, H),
+        "down": (T, H, F),
+    }
+    out = {}
+    for name, (M, N, K) in gemms.items():
+        n_out = N // 2 if name == "gate_up" else N
+        res = M * N * 2 if name in ("o", "down") else 0
+        out[name] = dict(flops=2.0 * M * N * K, bytes=2.0 * (N * K + M * K + M * n_out) + res)
+    dec = b.phase == wl.DECODE
+    ctx1 = (b.ctx_len[dec].astype(np.int64) + 1)
+    dec_bytes = float((ctx1 * KVB).sum() + dec.sum() * 4 * nq * d
+                      + (4 * np.ceil(ctx1 / 16)).sum())
+    dec_flops = float((4 * nq * d * ctx1).sum())
+    pre = ~dec
+    p = b.ctx_len[pre].astype(np.int64)
+    t = b.n_new[pre].astype(np.int64)
+    pre_flops = float((4 * nq * d * (p * t + t * (t + 1) / 2)).sum())
+    pre_bytes = float(((p + t) * KVB + 4 * t * nq * d).sum())
+    out["attention"] = dict(flops=dec_flops + pre_flops, bytes=dec_bytes + pre_bytes,
+                            decode_bytes=dec_bytes, prefill_flops=pre_flops)
+    out["kv_append"] = dict(flops=0.0, bytes=2.0 * T * KVB)
+    out["rmsnorm"] = dict(flops=0.0, bytes=8.0 * T * H)
+    return out
+
+
+def t_roof(parts):
+    return sum(max(p["flops"] / MFMA_BF16_PEAK, p["bytes"] / HBM_PEAK) for p in parts.values())
+
+
+class Point:
+    """Device state of one sweep point."""
+
+    def __init__(self, key, P, w_dev, packed, cfg):
+        import torch
+        import paper_2606_16264_amd as mx
+        import workload as wl
+        import workload.device as wdev
+        self.key, self.P, self.cfg = key, P, cfg
+        self.b = wl.make_batch(key, P)
+        b = self.b
+        self.c = mx.layer_cfg(cfg.hidden, cfg.ffn, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim,
+                              b.pool_pages, cfg.rms_eps, cfg.rope_theta)
+        self.shape = self.c.attn
+        self.packed = packed
+        self.k, self.v = wdev.alloc_pools(cfg, b.pool_pages)
+        wdev.fill_pools(self.k, self.v, cfg, b, wl.kv_seed(key), poison=True)
+        self.mb = mx.Batch(b.phase, b.n_new, b.ctx_len, b.page_tables)
+        self.ws = torch.empty(mx.mx_workspace_bytes_for(self.mb, cfg=self.c), dtype=torch.uint8,
+                              device="cuda")
+        self.x = torch.from_numpy(wl.make_x(cfg, b.T, key)).cuda()
+        self.y = torch.empty_like(self.x)
+        self.parts = algorithmic(cfg, b)
+
+    def step(self):
+        import paper_2606_16264_amd as mx
+        mx.mx_layer_step(self.mb, self.c, self.packed, self.x, self.y, self.k, self.v, self.ws)
+
+    def release(self):
+        del self.k, self.v, self.ws
+
+
+def time_fn(fn, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(steps):
+        fn()
+    e.record()
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / steps  # ms
+
+
+def kernel_breakdown(pt, steps, warmup):
+    """Per-kernel durations of the step's own launches, measured live with the
+    library's launch timing (hipEvents recorded on the launch stream around
+    each kernel), with each part's algorithmic roofline fraction."""
+    import paper_2606_16264_amd as mx
+    for _ in range(warmup):
+        pt.step()
+    mx.mx_profile_read()
+    mx.mx_profile_enable(True)
+    for _ in range(steps):
+        pt.step()
+    mx.mx_profile_enable(False)
+    times = mx.mx_profile_read()
+    parts = pt.parts
+    algo = {"gemm_qkv": parts["qkv"], "gemm_o": parts["o"], "gemm_gate_up": parts["gate_up"],
+            "gemm_down": parts["down"], "paged_attn": parts["attention"],
+            "rmsnorm_1": {"flops": 0.0, "bytes": parts["rmsnorm"]["bytes"] / 2},
+            "rmsnorm_2": {"flops": 0.0, "bytes": parts["rmsnorm"]["bytes"] / 2},
+            "token_map": {"flops": 0.0, "bytes": 0.0}}
+    res = {}
+    for tag, (ms, n) in times.items():
+        us = ms / max(n, 1) * 1e3
+        a = algo.get(tag, {"flops": 0.0, "bytes": 0.0})
+        sec = us * 1e-6
+        res[tag] = dict(us=us, launches=n, flops=a["flops"], bytes=a["bytes"],
+                        hbm_frac=a["bytes"] / sec / HBM_PEAK if sec > 0 else 0.0,
+                        mfma_frac=a["flops"] / sec / MFMA_BF16_PEAK if sec > 0 else 0.0,
+                        achieved_GBps=a["bytes"] / sec / 1e9 if sec > 0 else 0.0,
+                        TFLOPs=a["flops"] / sec / 1e12 if sec > 0 else 0.0)
+    return res
+
+
+def cpu_baseline(key, cfg, w_host, budget_s):
+    """The fp64 oracle (as it stands) on a bounded sample of the same workload:
+    a sub-batch of decode requests plus the first tokens of the prefill chunk,
+    every row evaluated.  Reported as tokens/s on the host cores."""
+    import numpy as np
+    import oracle
+    import workload as wl
+    b = wl.make_batch(key, max(wl.SWEEPS[key]))
+    x = wl.make_x(cfg, b.T, key)
+    seed = wl.kv_seed(key)
+    dec = [r for r in range(b.R) if b.phase[r] == wl.DECODE]
+    pre = [r for r in range(b.R) if b.phase[r] == wl.PREFILL]
+    start = np.concatenate([[0], np.cumsum(b.n_new)])
+
+    def run(n_dec, n_pre_tok):
+        reqs = dec[:n_dec] + pre[:1]
+        sub = b.subset(reqs)
+        if pre:
+            sub.n_new[-1] = min(n_pre_tok, int(sub.n_new[-1]))
+        tok = []
+        for i, r in enumerate(reqs):
+            tok += list(range(int(start[r]), int(start[r]) + int(sub.n_new[i])))
+        kp, vp = wl.prior_kv_concat(cfg, sub, seed)
+        t0 = time.perf_counter()
+        oracle.layer_step(cfg.as_dict(), sub.n_new, sub.ctx_len, x[tok], w_host, kp, vp)
+        return time.perf_counter() - t0, sub.T
+
+    # grow the sample until one evaluation takes about the requested budget
+    n_dec, n_pre = 2, 2
+    dt, n = run(n_dec, n_pre)
+    while dt < budget_s / 2 and (n_dec < len(dec) or (pre and n_pre < int(b.n_new[pre[0]]))):
+        grow = min(4.0, max(1.5, budget_s / max(dt, 1e-3) / 1.5))
+        n_dec = int(min(len(dec), max(n_dec + 1, round(n_dec * grow))))
+        n_pre = int(max(n_pre + 1, round(n_pre * grow)))
+        dt, n = run(n_dec, n_pre)
+    return {"value": n / dt, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"{n_dec} decode requests + first {n_pre} tokens of the prefill chunk "
+                      f"({n} rows, full layer, fp64), {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1 "
+                                   "(multi-GPU sharding is described in DESIGN.md, not run)"}))
+        sys.exit(2)
+    import numpy as np
+    import torch
+    import paper_2606_16264_amd as mx
+    import workload as wl
+
+    torch.cuda.set_device(0)
+    key = args.config
+    cfg = wl.CONFIGS[key]
+    sweep = args.prefill if args.prefill is not None else wl.SWEEPS[key]
+    w_host = wl.make_weights(cfg, key)
+    w_dev = {k: torch.from_numpy(v).cuda() for k, v in w_host.items()}
+    b0 = wl.make_batch(key, sweep[0])
+    c0 = mx.layer_cfg(cfg.hidden, cfg.ffn, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim,
+                      b0.pool_pages, cfg.rms_eps, cfg.rope_theta)
+    packed = torch.empty(mx.mx_packed_weights_bytes(c0), dtype=torch.uint8, device="cuda")
+    mx.mx_pack_weights(c0, w_dev, packed)
+    del w_dev
+    torch.cuda.synchronize()
+    if args.copy_calib_mib:
+        n = args.copy_calib_mib << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"# copy calibration: {n} bytes device-to-device", file=sys.stderr, flush=True)
+        del src, dst
+    print(f"# bench: {key} ({cfg.name}) sweep P={sweep}, steps={args.steps}, warmup={args.warmup}",
+          file=sys.stderr, flush=True)
+
+    curve = []
+    headline = None
+    for P in sweep:
+        pt = Point(key, P, None, packed, cfg)
+        torch.cuda.synchronize()
+        ms = time_fn(pt.step, args.steps, args.warmup)
+        us = ms * 1e3
+        roof = t_roof(pt.parts) * 1e6
+        rec = dict(P=int(P), T=pt.b.T, R=pt.b.R, us=round(us, 2),
+                   tokens_per_s=pt.b.T / (us * 1e-6),
+                   decode_tokens_per_s=int((pt.b.phase == wl.DECODE).sum()) / (us * 1e-6),
+                   t_roof_us=round(roof, 2), roof_frac=roof / us)
+        print(f"# P={P}: {us:.1f} us/step, {rec['tokens_per_s']:.0f} tok/s, "
+              f"roofline {roof:.1f} us ({rec['roof_frac']:.2f})", file=sys.stderr, flush=True)
+        if P == sweep[-1]:
+            headline = (pt, rec)
+        else:
+            pt.release()
+        curve.append(rec)
+    pt, rec = headline
+    kernels = kernel_breakdown(pt, max(5, args.steps // 2), 2) if args.kernels else {}
+    for k, v in kernels.items():
+        print(f"# kernel {k}: {v['us']:.1f} us  hbm_frac={v['hbm_frac']:.3f}  "
+              f"mfma_frac={v['mfma_frac']:.3f}", file=sys.stderr, flush=True)
+    # dominant kernel and its roofline: the attention is HBM-bound (decode
+    # K/V streaming), the projections MFMA-bound at these token counts
+    dom = max(kernels, key=lambda k: kernels[k]["us"]) if kernels else None
+    roofline = None
+    wl_tag = f"{key}_P{pt.b.prefill_tokens}"
+    if dom == "paged_attn":
+        kv = kernels[dom]
+        roofline = {"kernel": "paged_attn_kernel", "bound": "hbm",
+                    "achieved": round(kv["achieved_GBps"], 1), "peak": HBM_PEAK / 1e9,
+                    "unit": "GB/s", "frac": round(kv["hbm_frac"], 4),
+                    "algorithmic_bytes": kv["bytes"], "avg_launch_us": round(kv["us"], 2),
+                    "traffic": measured_traffic("paged_attn_kernel", wl_tag,
+                                                "paper_2606_16264_amd/csrc/attention.hip")}
+    elif dom is not None:
+        kv = kernels[dom]
+        roofline = {"kernel": dom, "bound": "mfma", "achieved": round(kv["TFLOPs"], 1),
+                    "peak": MFMA_BF16_PEAK / 1e12, "unit": "TFLOP/s",
+                    "frac": round(kv["mfma_frac"], 4), "algorithmic_flops": kv["flops"],
+                    "avg_launch_us": round(kv["us"], 2),
+                    "traffic": measured_traffic(dom, wl_tag, "paper_2606_16264_amd/csrc/gemm.hip")}
+    cpu = None
+    if not args.no_cpu:
+        cpu = cpu_baseline(key, cfg, w_host, args.cpu_seconds)
+    out = {
+        "metric": METRIC,
+        "value": round(rec["tokens_per_s"], 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(rec["us"] / 1e3, 5),
+        "latency_us": rec["us"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded; chat-style mixed batch shapes, random-init weights)",
+        "config": {"workload": f"{cfg.name} layer ({key}): hidden {cfg.hidden}, "
+                               f"{cfg.n_q_heads}q/{cfg.n_kv_heads}kv x {cfg.head_dim}, ffn {cfg.ffn}; "
+                               f"{int((pt.b.phase == wl.DECODE).sum())} decodes + "
+                               f"{pt.b.prefill_tokens} mixed prefill tokens",
+                   "T": pt.b.T, "R": pt.b.R, "P": pt.b.prefill_tokens},
+        "curve": curve,
+        "t_roof_us": rec["t_roof_us"],
+        "roof_frac": round(rec["roof_frac"], 4),
+        "roofline": roofline,
+        "kernels": {k: {m: (round(v, 4) if isinstance(v, float) else v) for m, v in d.items()}
+                    for k, d in kernels.items()},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,247 @@
+/*
+ * mx.h -- C ABI of the MI355X (gfx950) multiplexed decoder-layer iteration.
+ *
+ * The problem statement this interface follows: a multiplexing worker runs
+ * iterations whose batch mixes requests in the prefill phase (a chunk of
+ * prompt tokens, possibly continuing an earlier chunk) with requests in the
+ * decode phase (one new token each); prefill chunks are piggybacked onto the
+ * running decode batch (paper Section 3.3, "Multiplexing Toggle"; Section 4.1,
+ * chunked prefill with one chunk per iteration).  The engine keeps keys and
+ * values in a paged cache (Section 4.1: the vLLM-based engine).  Every request
+ * is described by its phase, its new-token count, the number of tokens already
+ * cached and its page table.
+ *
+ * Conventions
+ *  - All tensor pointers are DEVICE pointers unless marked [host].
+ *  - bf16 tensors are passed as raw uint16 bit patterns.
+ *  - Tokens of the batch are concatenated in request order; request r owns the
+ *    n_new[r] consecutive rows starting at sum_{s<r} n_new[s].  Its i-th new
+ *    token sits at position ctx_len + i and attends causally to the request's
+ *    keys at positions 0 .. ctx_len + i.
+ *  - Page size is 16 tokens.  The KV slot of position p of a request is
+ *    pages[p / 16] * 16 + p % 16.
+ *  - Pools (one for keys, one for values), per layer, bf16:
+ *      k_pool[pool_pages][n_kv_heads][16][head_dim]   (token-major within a page)
+ *      v_pool[pool_pages][n_kv_heads][head_dim][16]   (each page stored transposed,
+ *                                                     so that the matrix-core
+ *                                                     operands load contiguously)
+ *    Byte offsets are 64-bit; pools larger than 4 GiB are supported.
+ *  - Ownership: the caller allocates and owns every device buffer (weights,
+ *    pools, activations, workspace) and the stream.  The library keeps no
+ *    pointer after a call returns except for work already enqueued.  Host
+ *    arrays (the batch) are read during the call only.  The library allocates
+ *    nothing per call; on its first call on a device it allocates a small ring
+ *    of pinned host staging buffers (grown, rarely, if a batch needs more) that
+ *    lives until the process ends.
+ *  - Errors: every input check runs on the host before anything is enqueued.
+ *    On error nothing is enqueued, a status is returned and mx_last_error()
+ *    (thread-local) gives a message.  No C++ exception crosses the ABI.  HIP
+ *    launch errors map to MX_ERR_HIP; asynchronous faults surface at the
+ *    caller's next synchronisation.
+ *  - Threading: calls may come from several threads; calls that share one
+ *    workspace must be ordered (same stream, or caller-side synchronisation).
+ */
+#ifndef MX_H
+#define MX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MX_OK = 0,
+  MX_ERR_INVALID = 1,     /* malformed batch or shape */
+  MX_ERR_NO_SPACE = 2,    /* a page table is too short for the request's positions */
+  MX_ERR_TOO_LARGE = 3,   /* the workspace is too small for this batch */
+  MX_ERR_UNSUPPORTED = 4, /* head_dim not in {64, 128}, page size not 16, ... */
+  MX_ERR_NULL = 5,        /* a required pointer is NULL */
+  MX_ERR_HIP = 6          /* a HIP runtime call failed */
+} mx_status;
+
+typedef enum { MX_PREFILL = 0, MX_DECODE = 1 } mx_phase;
+
+/* One request of the iteration (the fields a scheduler hands to a worker). */
+typedef struct {
+  int32_t phase;        /* mx_phase */
+  int32_t n_new;        /* new tokens this iteration: >= 1; exactly 1 for a decode */
+  int32_t ctx_len;      /* tokens already cached before this iteration (>= 1 for a decode) */
+  int32_t n_pages;      /* entries in pages[]: >= ceil((ctx_len + n_new) / 16) */
+  const int32_t* pages; /* [host] page ids in [0, pool_pages) */
+} mx_request;
+
+typedef struct {
+  int32_t num_reqs;       /* R >= 0; R == 0 is a no-op */
+  const mx_request* reqs; /* [host] R requests */
+} mx_batch;
+
+typedef struct {
+  int32_t n_q_heads, n_kv_heads; /* n_q_heads % n_kv_heads == 0; q head h reads kv head h / (n_q_heads / n_kv_heads) */
+  int32_t head_dim;              /* 64 or 128 */
+  int32_t page_size;             /* 16 */
+  int64_t pool_pages;            /* pages in each pool */
+  float scale;                   /* softmax scale; 0 means 1/sqrt(head_dim) */
+} mx_attn_shape;
+
+typedef struct {
+  int32_t hidden; /* H, a multiple of 64 */
+  int32_t ffn;    /* F, a multiple of 64 */
+  mx_attn_shape attn;
+  float rms_eps;    /* RMSNorm epsilon */
+  float rope_theta; /* RoPE base (rotate-half pairing) */
+} mx_layer_cfg;
+
+/* Canonical weights, bf16, row-major [out][in] (the layout of a linear layer):
+ *   ln1_g[H], w_qkv[(nq + 2 nkv) d][H] (rows: q heads, then k heads, then v heads),
+ *   w_o[H][nq d], ln2_g[H], w_gate_up[2F][H] (rows: gate, then up), w_down[H][F]. */
+typedef struct {
+  const uint16_t *ln1_g, *w_qkv, *w_o, *ln2_g, *w_gate_up, *w_down;
+} mx_layer_weights;
+
+const char* mx_status_str(mx_status s);
+/* Detail of the last error on the calling thread ("" if none). */
+const char* mx_last_error(void);
+/* ABI version: (major << 16) | minor. */
+uint32_t mx_version(void);
+
+/*
+ * Host-only check of a batch against a shape (the rules every entry point
+ * applies first): R >= 0; phase in {PREFILL, DECODE}; n_new >= 1; a decode has
+ * n_new == 1 and ctx_len >= 1; ctx_len >= 0; n_pages >= ceil((ctx_len + n_new)/16)
+ * (else MX_ERR_NO_SPACE); page ids in [0, pool_pages); the slots written by the
+ * new tokens are distinct across the batch (cached prefix pages may be shared
+ * read-only); n_q_heads % n_kv_heads == 0; head_dim in {64, 128} and
+ * page_size == 16 (else MX_ERR_UNSUPPORTED).  Touches no device.
+ */
+mx_status mx_batch_validate(const mx_batch* batch, const mx_attn_shape* shape);
+
+/*
+ * Workspace bytes that a call needs for this batch (mx_layer_step when cfg is
+ * given, mx_paged_attn / mx_kv_append when cfg is NULL and shape is given).
+ * Returns 0 and sets mx_last_error on an invalid batch.
+ */
+size_t mx_workspace_bytes_for(const mx_batch* batch, const mx_attn_shape* shape,
+                              const mx_layer_cfg* cfg);
+
+/*
+ * Upper bound of the workspace of mx_layer_step for any batch of at most
+ * max_tokens new tokens, max_reqs requests and max_pages page-table entries in
+ * total.  With cfg == NULL the bound for mx_paged_attn / mx_kv_append, using
+ * shape.
+ */
+size_t mx_workspace_bytes(const mx_layer_cfg* cfg, const mx_attn_shape* shape,
+                          int32_t max_tokens, int32_t max_reqs, int64_t max_pages);
+
+/* Bytes of the packed weight blob of one layer. */
+size_t mx_packed_weights_bytes(const mx_layer_cfg* cfg);
+
+/*
+ * Re-lays the canonical weights into the packed blob (device, packed_bytes
+ * from mx_packed_weights_bytes) that mx_layer_step reads: the gate and up
+ * rows of w_gate_up are interleaved in 32-row blocks so that one GEMM tile
+ * holds both operands of the SwiGLU product, and within every q and k head of
+ * w_qkv (head_dim 128) the rows of dims i and i + 64 are placed 32 rows apart
+ * so that one lane holds both halves of each rotary pair.  Enqueued on the
+ * stream.
+ */
+mx_status mx_pack_weights(const mx_layer_cfg* cfg, const mx_layer_weights* canonical,
+                          void* packed, size_t packed_bytes, hipStream_t stream);
+
+/*
+ * KV append (the cache write of the new tokens): k_new, v_new [T][n_kv_heads]
+ * [head_dim] are copied to the slots of the token map, k into k_pool's layout
+ * and v into v_pool's transposed page layout.  A pure byte copy.
+ */
+mx_status mx_kv_append(const mx_batch* batch, const mx_attn_shape* shape,
+                       const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_pool,
+                       uint16_t* v_pool, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Paged varlen attention over the mixed batch, one launch for prefill rows
+ * and decode rows (paper Section 3.3, chunked prefill piggybacked on decodes):
+ * q [T][n_q_heads][head_dim] -> out [T][n_q_heads][head_dim], bf16.  For token
+ * t (request r, position p) and q head h, with g = h / (nq / nkv):
+ *   out[t][h] = sum_{j <= p} softmax_j(scale * q[t][h] . K_r[j][g]) V_r[j][g],
+ * K_r[j] and V_r[j] read from the pools through the request's page table.
+ * Keys of positions 0 .. ctx_len + n_new - 1 must already be in the pools
+ * (mx_kv_append puts the new ones there).  Slots at or beyond that length are
+ * never read into a sum.  Long decode contexts are split across workgroups
+ * and merged deterministically: results are bit-identical from run to run.
+ */
+mx_status mx_paged_attn(const mx_batch* batch, const mx_attn_shape* shape, const uint16_t* q,
+                        const uint16_t* k_pool, const uint16_t* v_pool, uint16_t* out,
+                        void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * One multiplexed decoder-layer iteration (pre-norm Llama-style layer):
+ *   h  = RMSNorm(x) * ln1_g
+ *   q, k, v = h W_qkv^T;  RoPE (rotate-half, base rope_theta) on q and k at
+ *             each token's position
+ *   k, v -> pools (append), then attention as mx_paged_attn -> o
+ *   x1 = x + o W_o^T
+ *   h2 = RMSNorm(x1) * ln2_g
+ *   a  = silu(h2 W_gate^T) * (h2 W_up^T)
+ *   y  = x1 + a W_down^T
+ * x, y [T][H] bf16 (y must not alias x); packed_weights from mx_pack_weights.
+ * Repeating a call with the same inputs rewrites the same slots with the same
+ * values.
+ */
+mx_status mx_layer_step(const mx_batch* batch, const mx_layer_cfg* cfg, const void* packed_weights,
+                        const uint16_t* x, uint16_t* y, uint16_t* k_pool, uint16_t* v_pool,
+                        void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------- inspection */
+
+/* Byte offsets, inside the workspace of mx_layer_step for this batch, of the
+ * intermediate tensors the call leaves behind (bf16):
+ *   off[0] h / h2 [T][H] (h2 overwrites h), off[1] q [T][nq][d] (post-RoPE),
+ *   off[2] o [T][nq][d], off[3] x1 [T][H], off[4] a [T][F].
+ * (The new keys and values of the iteration are in the pools.) */
+mx_status mx_layer_workspace_offsets(const mx_batch* batch, const mx_layer_cfg* cfg,
+                                     size_t off[5]);
+
+/* Device token map of the batch as the iteration computes it (the kernel that
+ * every entry point runs first): tok_req[T], tok_pos[T] (int32) and
+ * tok_slot[T] (int64), device outputs. */
+mx_status mx_debug_token_map(const mx_batch* batch, const mx_attn_shape* shape, int32_t* tok_req,
+                             int32_t* tok_pos, int64_t* tok_slot, void* ws, size_t ws_bytes,
+                             hipStream_t stream);
+
+/* Gathers request req's keys and values, positions 0 .. ctx_len + n_new - 1, from
+ * the pools through its page table into k_out, v_out [len][n_kv_heads][head_dim]
+ * (device).  A byte copy through the same addressing the attention uses. */
+mx_status mx_debug_gather(const mx_batch* batch, const mx_attn_shape* shape, int32_t req,
+                          const uint16_t* k_pool, const uint16_t* v_pool, uint16_t* k_out,
+                          uint16_t* v_out, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Launch timing, for profiling.  When enabled, every kernel launch of
+ * mx_layer_step and mx_paged_attn is bracketed by two hipEvents recorded on the
+ * caller's stream (the launch's own stream), tagged with the step it performs
+ * ("token_map", "rmsnorm_1", "gemm_qkv", "paged_attn", "gemm_o", "rmsnorm_2",
+ * "gemm_gate_up", "gemm_down"; a tag covers a split-K GEMM's reduce and the
+ * attention's split merge).  Off by default. */
+mx_status mx_profile_enable(int32_t on);
+/* Waits for the recorded events, accumulates their durations per tag and
+ * returns the number of tags written (at most max_entries): names[i] is a
+ * static string, total_ms[i] the summed duration and counts[i] the number of
+ * launches.  Clears what it reports.  Any output array may be NULL. */
+int32_t mx_profile_read(const char** names, float* total_ms, int32_t* counts, int32_t max_entries);
+
+/* The projection GEMM of the layer on its own: C[M][N] = epi(A[M][K] B[N][K]^T),
+ * bf16 in, fp32 accumulate; epilogue 0 = store, 1 = + R[M][N] (residual),
+ * 2 = SwiGLU over B rows interleaved gate/up in 32-row blocks (C is [M][N/2]).
+ * K must be a multiple of 64.  ws holds the K-split scratch
+ * (mx_debug_gemm_ws_bytes).  For tests and microbenchmarks. */
+size_t mx_debug_gemm_ws_bytes(int32_t M, int32_t N, int32_t K);
+mx_status mx_debug_gemm(int32_t M, int32_t N, int32_t K, const uint16_t* A, const uint16_t* B,
+                        uint16_t* C, const uint16_t* R, int32_t epilogue, void* ws, size_t ws_bytes,
+                        hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,334 @@
+// attention.hip -- paged varlen attention for a mixed prefill/decode batch on
+// gfx950, one launch over a host-built work list, plus the split merge.
+//
+// Every wave computes, for up to 16 query rows that share one KV head, the
+// transposed score tile S^T = K Q^T (keys x rows) with the 16x16x32 bf16
+// matrix-core instruction, and then O^T += V^T P^T.  In that orientation the
+// probabilities come out of the first product already in the register layout
+// the second product wants as its B operand, and every softmax statistic of a
+// query row lives in the lane that also holds that row of O^T, so P never
+// leaves registers.  Keys are consumed two pages (32 keys) at a time; the key
+// order inside one 32-key step is permuted identically for both products so
+// that every key and value load is a 16-byte run.
+//
+//   decode item : the q heads of one KV-head group of a single decode token,
+//                 over one split of the request's pages; the four waves of the
+//                 workgroup stride over the split's 32-key chunks and combine
+//                 through LDS.  Requests with several splits leave fp32
+//                 partials (unnormalised O, running max, running sum) for the
+//                 merge kernel.
+//   prefill item: one q head, 64 query rows of a prefill chunk (16 per wave),
+//                 causal over the cached prefix plus the chunk.
+//
+// Masking is select-based: slots at or past the request's length are never
+// multiplied into a sum, so stale or NaN-filled slots cannot leak.
+#include "mx_device.h"
+#include "mx_kernels.h"
+
+namespace mx {
+
+namespace {
+
+constexpr float kNegBig = -1.0e30f;
+
+template <int HD>
+struct Chunk {
+  u32x4 k[2][HD / 32];  // keys: 16 B per lane per (score block, d-step)
+  u32x4 v[HD / 16];     // values (transposed pages): 16 B per lane per d-block
+};
+
+// Key order inside a 32-key step (two pages).  Score block b, row m holds key
+//   kappa_b(m) = 8 * (m / 4) + 4 * b + m % 4,
+// so that lane group g (rows 4g .. 4g+3 of both blocks) ends up with the eight
+// consecutive keys 8g .. 8g+7, all in page g / 2.  Those eight keys are then
+// one 16-byte run of a transposed value page, and they are exactly the k
+// indices the second product expects from this lane group.
+template <int HD>
+__device__ __forceinline__ void load_chunk(Chunk<HD>& c, const AttnParams& p, int kvh, int pid0,
+                                           int pid1, int col, int g4) {
+  // keys: lane row m = col; its key kappa_b(col) lives in page col / 8
+  {
+    const int page = (col < 8) ? pid0 : pid1;
+    const int slot0 = 8 * ((col >> 2) & 1) + (col & 3);
+    if (page >= 0) {
+      const uint16_t* kb_ptr = p.k_pool + ((int64_t)page * p.nkv + kvh) * (int64_t)(16 * HD);
+#pragma unroll
+      for (int b = 0; b < 2; b++)
+#pragma unroll
+        for (int ds = 0; ds < HD / 32; ds++)
+          c.k[b][ds] = *reinterpret_cast<const u32x4*>(kb_ptr + (slot0 + 4 * b) * HD + ds * 32 + 8 * g4);
+    } else {
+#pragma unroll
+      for (int b = 0; b < 2; b++)
+#pragma unroll
+        for (int ds = 0; ds < HD / 32; ds++) c.k[b][ds] = u32x4{0, 0, 0, 0};
+    }
+  }
+  // values: lane group g reads keys 8 (g % 2) .. +7 of page g / 2 at d = 16 db + col
+  {
+    const int page = (g4 < 2) ? pid0 : pid1;
+    if (page >= 0) {
+      const uint16_t* vb_ptr = p.v_pool + ((int64_t)page * p.nkv + kvh) * (int64_t)(16 * HD) + 8 * (g4 & 1);
+#pragma unroll
+      for (int db = 0; db < HD / 16; db++)
+        c.v[db] = *reinterpret_cast<const u32x4*>(vb_ptr + (db * 16 + col) * 16);
+    } else {
+#pragma unroll
+      for (int db = 0; db < HD / 16; db++) c.v[db] = u32x4{0, 0, 0, 0};
+    }
+  }
+}
+
+// One 32-key step of the online softmax for this lane's query row.  Lane group
+// g4 owns keys pi0 * 16 + 8 * g4 + i' (i' = 4 b + i for score block b, row i).
+template <int HD>
+__device__ __forceinline__ void process_chunk(const Chunk<HD>& c, const bf16x8 (&qf)[HD / 32],
+                                              f32x4 (&o)[HD / 16], float& m, float& l,
+                                              int pi0, int page_end, int row_pos, int kv_len,
+                                              float scale_log2, int g4) {
+  f32x4 s[2];
+#pragma unroll
+  for (int b = 0; b < 2; b++) {
+    s[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ds = 0; ds < HD / 32; ds++) s[b] = mfma16(as_bf16x8(c.k[b][ds]), qf[ds], s[b]);
+  }
+  const bool pvalid = (pi0 + (g4 >> 1)) < page_end;
+  const int j0 = pi0 * 16 + 8 * g4;
+  float sv[2][4];
+  float mx = kNegBig;
+#pragma unroll
+  for (int b = 0; b < 2; b++)
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      const int j = j0 + 4 * b + i;
+      const float x = s[b][i] * scale_log2;
+      sv[b][i] = (pvalid && j <= row_pos) ? x : kNegBig;
+      mx = fmaxf(mx, sv[b][i]);
+    }
+  mx = fmaxf(mx, __shfl_xor(mx, 16));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const float m_new = fmaxf(m, mx);
+  const float alpha = exp2f(m - m_new);
+  float ps = 0.f;
+  float pv[2][4];
+#pragma unroll
+  for (int b = 0; b < 2; b++)
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      pv[b][i] = exp2f(sv[b][i] - m_new);
+      ps += pv[b][i];
+    }
+  ps += __shfl_xor(ps, 16);
+  ps += __shfl_xor(ps, 32);
+  l = l * alpha + ps;
+  m = m_new;
+  // P^T as the B operand: k index i' = 4 b + i <-> key j0 + i'
+  u32x4 pb_bits;
+  pb_bits[0] = pack_bf16x2(pv[0][0], pv[0][1]);
+  pb_bits[1] = pack_bf16x2(pv[0][2], pv[0][3]);
+  pb_bits[2] = pack_bf16x2(pv[1][0], pv[1][1]);
+  pb_bits[3] = pack_bf16x2(pv[1][2], pv[1][3]);
+  const bf16x8 pb = as_bf16x8(pb_bits);
+  // V^T as the A operand; values of keys past the request's length are zeroed
+  // (select, not multiply) so that NaN-filled slots stay out of the sum.
+  uint32_t keep[4];
+#pragma unroll
+  for (int h = 0; h < 4; h++) {
+    const bool k0 = pvalid && (j0 + 2 * h) < kv_len;
+    const bool k1 = pvalid && (j0 + 2 * h + 1) < kv_len;
+    keep[h] = (k0 ? 0x0000FFFFu : 0u) | (k1 ? 0xFFFF0000u : 0u);
+  }
+#pragma unroll
+  for (int db = 0; db < HD / 16; db++) {
+    u32x4 va;
+#pragma unroll
+    for (int h = 0; h < 4; h++) va[h] = c.v[db][h] & keep[h];
+    o[db] = o[db] * alpha;
+    o[db] = mfma16(as_bf16x8(va), pb, o[db]);
+  }
+}
+
+template <int HD>
+__global__ __launch_bounds__(256) void paged_attn_kernel(AttnParams p) {
+  const AttnItem it = p.items[blockIdx.x];
+  const ReqDev rq = p.reqs[it.req];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int col = lane & 15;  // query row of this lane
+  const int g4 = lane >> 4;   // lane group
+
+  float m = kNegBig, l = 0.f;
+  f32x4 o[HD / 16];
+#pragma unroll
+  for (int db = 0; db < HD / 16; db++) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  bf16x8 qf[HD / 32];
+
+  int kvh, qhead, row_pos, page_first, page_end, chunk_first, chunk_step;
+  bool row_valid;
+  int64_t qtok;
+  if (it.kind == 0) {
+    // decode: rows are q heads it.head .. it.head + nrows - 1 of the request's token
+    qhead = it.head + col;
+    row_valid = col < it.nrows;
+    kvh = it.head / p.group;
+    qtok = rq.tok_start;
+    row_pos = rq.kv_len - 1;
+    page_first = it.start;
+    page_end = min(it.start + p.split_pages, rq.n_pages);
+    chunk_first = page_first + 2 * wave;
+    chunk_step = 8;
+  } else {
+    // prefill: rows are 16 consecutive tokens of the chunk, one q head
+    qhead = it.head;
+    kvh = qhead / p.group;
+    const int row0 = it.start + 16 * wave;
+    const int row = row0 + col;
+    row_valid = row < rq.n_new;
+    const int rowc = row_valid ? row : rq.n_new - 1;
+    qtok = rq.tok_start + rowc;
+    row_pos = rq.ctx_len + rowc;
+    const int last_row = min(row0 + 15, rq.n_new - 1);
+    page_first = 0;
+    page_end = row0 < rq.n_new ? (rq.ctx_len + last_row) / 16 + 1 : 0;
+    chunk_first = 0;
+    chunk_step = 2;
+  }
+  {
+    const uint16_t* qp = p.q + qtok * p.q_tok_stride + (int64_t)qhead * HD + 8 * g4;
+#pragma unroll
+    for (int ds = 0; ds < HD / 32; ds++) {
+      u32x4 v = row_valid ? *reinterpret_cast<const u32x4*>(qp + ds * 32) : u32x4{0, 0, 0, 0};
+      qf[ds] = as_bf16x8(v);
+    }
+  }
+
+  // page ids are fetched two chunks ahead of use, so that the id lookup is not
+  // on the critical path of the key/value loads
+  auto pid = [&](int pi) -> int { return pi < page_end ? p.pages[rq.page_start + pi] : -1; };
+  Chunk<HD> cur, nxt;
+  int pi = chunk_first;
+  int n0 = pid(pi + chunk_step), n1 = pid(pi + chunk_step + 1);
+  if (pi < page_end) load_chunk<HD>(cur, p, kvh, pid(pi), pid(pi + 1), col, g4);
+  while (pi < page_end) {
+    const int pn = pi + chunk_step;
+    const int nn0 = pid(pn + chunk_step), nn1 = pid(pn + chunk_step + 1);
+    if (pn < page_end) load_chunk<HD>(nxt, p, kvh, n0, n1, col, g4);
+    process_chunk<HD>(cur, qf, o, m, l, pi, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
+    cur = nxt;
+    n0 = nn0;
+    n1 = nn1;
+    pi = pn;
+  }
+
+  if (it.kind == 1) {
+    if (row_valid) {
+      const float inv = 1.f / l;
+      uint16_t* op = p.out + qtok * p.out_tok_stride + (int64_t)qhead * HD + 4 * g4;
+#pragma unroll
+      for (int db = 0; db < HD / 16; db++) {
+        u32x2 w;
+        w[0] = pack_bf16x2(o[db][0] * inv, o[db][1] * inv);
+        w[1] = pack_bf16x2(o[db][2] * inv, o[db][3] * inv);
+        *reinterpret_cast<u32x2*>(op + db * 16) = w;
+      }
+    }
+    return;
+  }
+
+  // decode: combine the four waves' partial softmax states through LDS
+  __shared__ float s_o[4][16][HD + 4];
+  __shared__ float s_m[4][16], s_l[4][16];
+#pragma unroll
+  for (int db = 0; db < HD / 16; db++)
+#pragma unroll
+    for (int i = 0; i < 4; i++) s_o[wave][col][db * 16 + 4 * g4 + i] = o[db][i];
+  if (g4 == 0) {
+    s_m[wave][col] = m;
+    s_l[wave][col] = l;
+  }
+  __syncthreads();
+  const int row = threadIdx.x >> 4;         // 16 rows
+  const int dseg = (threadIdx.x & 15) * (HD / 16);
+  if (row >= it.nrows) return;
+  float M = kNegBig;
+#pragma unroll
+  for (int w = 0; w < 4; w++) M = fmaxf(M, s_m[w][row]);
+  float wt[4], L = 0.f;
+#pragma unroll
+  for (int w = 0; w < 4; w++) {
+    wt[w] = exp2f(s_m[w][row] - M);
+    L += s_l[w][row] * wt[w];
+  }
+  float acc[HD / 16];
+#pragma unroll
+  for (int e = 0; e < HD / 16; e++) {
+    float a = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; w++) a += s_o[w][row][dseg + e] * wt[w];
+    acc[e] = a;
+  }
+  const int h = it.head + row;
+  if (rq.n_split == 1) {
+    const float inv = 1.f / L;
+    uint16_t* op = p.out + qtok * p.out_tok_stride + (int64_t)h * HD + dseg;
+#pragma unroll
+    for (int e = 0; e < HD / 16; e += 2)
+      *reinterpret_cast<uint32_t*>(op + e) = pack_bf16x2(acc[e] * inv, acc[e + 1] * inv);
+  } else {
+    const int64_t part = (int64_t)it.part + (int64_t)row * rq.n_split;
+    float* po = p.part_o + part * HD + dseg;
+#pragma unroll
+    for (int e = 0; e < HD / 16; e += 4)
+      *reinterpret_cast<f32x4*>(po + e) = f32x4{acc[e], acc[e + 1], acc[e + 2], acc[e + 3]};
+    if ((threadIdx.x & 15) == 0) {
+      p.part_ml[part * 2 + 0] = M;
+      p.part_ml[part * 2 + 1] = L;
+    }
+  }
+}
+
+// Deterministic merge of the key splits of one (decode request, q head).
+template <int HD>
+__global__ __launch_bounds__(HD) void attn_merge_kernel(AttnParams p, const MergeItem* merges) {
+  const MergeItem mi = merges[blockIdx.x];
+  const ReqDev rq = p.reqs[mi.req];
+  const int h = blockIdx.y;
+  const int d = threadIdx.x;
+  const int ns = rq.n_split;
+  const int64_t base = (int64_t)mi.part_base + (int64_t)h * ns;
+  float M = kNegBig;
+  for (int s = 0; s < ns; s++) M = fmaxf(M, p.part_ml[(base + s) * 2]);
+  float L = 0.f, acc = 0.f;
+  for (int s = 0; s < ns; s++) {
+    const float w = exp2f(p.part_ml[(base + s) * 2] - M);
+    L += p.part_ml[(base + s) * 2 + 1] * w;
+    acc += p.part_o[(base + s) * HD + d] * w;
+  }
+  p.out[(int64_t)rq.tok_start * p.out_tok_stride + (int64_t)h * HD + d] = f32_to_bf16(acc / L);
+}
+
+}  // namespace
+
+hipError_t launch_paged_attn(const AttnParams& p, int n_items, const MergeItem* merges,
+                             int n_merges, int head_dim, hipStream_t stream) {
+  if (n_items > 0) {
+    if (head_dim == 128)
+      paged_attn_kernel<128><<<n_items, 256, 0, stream>>>(p);
+    else
+      paged_attn_kernel<64><<<n_items, 256, 0, stream>>>(p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (n_merges > 0) {
+    dim3 grid(n_merges, p.nq);
+    if (head_dim == 128)
+      attn_merge_kernel<128><<<grid, 128, 0, stream>>>(p, merges);
+    else
+      attn_merge_kernel<64><<<grid, 64, 0, stream>>>(p, merges);
+    return hipGetLastError();
+  }
+  return hipSuccess;
+}
+
+}  // namespace mx

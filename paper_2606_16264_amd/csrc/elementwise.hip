@@ -1,0 +1,215 @@
+// elementwise.hip -- the memory-bound kernels of the layer step on gfx950:
+// token map + rotary table, RMSNorm, KV append, gather, weight packing.
+#include "mx_device.h"
+#include "mx_kernels.h"
+
+namespace mx {
+
+namespace {
+
+// ---------------------------------------------------------------- token map
+// One thread per (token, rotary pair).  The token's request is found by binary
+// search over the requests' first rows; token t = tok_start + i of request r
+// sits at position ctx_len + i and writes slot page * 16 + pos % 16.  The
+// rotary angle pos * theta^(-2i/d) is formed and reduced modulo 2 pi in double
+// precision; its cosine and sine are then taken in single precision.
+__global__ __launch_bounds__(256) void token_map_kernel(const ReqDev* __restrict__ reqs, int R,
+                                                        int T, const int32_t* __restrict__ pages,
+                                                        int32_t* tok_req, int32_t* tok_pos,
+                                                        int64_t* tok_slot,
+                                                        const double* __restrict__ inv_freq,
+                                                        float2* rope_cs, int half) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int t = (int)(idx / half), i = (int)(idx % half);
+  if (t >= T) return;
+  int lo = 0, hi = R - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (reqs[mid].tok_start <= t) lo = mid; else hi = mid - 1;
+  }
+  const ReqDev rq = reqs[lo];
+  const int pos = rq.ctx_len + (t - rq.tok_start);
+  if (i == 0) {
+    const int64_t page = pages[rq.page_start + pos / 16];
+    tok_req[t] = lo;
+    tok_pos[t] = pos;
+    tok_slot[t] = page * 16 + pos % 16;
+  }
+  if (rope_cs) {
+    const double a = (double)pos * inv_freq[i];
+    const double two_pi = 6.283185307179586476925286766559;
+    const double r = a - rint(a / two_pi) * two_pi;
+    float sn, cs;
+    sincosf((float)r, &sn, &cs);
+    rope_cs[(int64_t)t * half + i] = make_float2(cs, sn);
+  }
+}
+
+// ---------------------------------------------------------------- RMSNorm
+__device__ __forceinline__ float block_sum_256(float v, float* red) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[wave] = v;
+  __syncthreads();
+  return red[0] + red[1] + red[2] + red[3];
+}
+
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict__ x,
+                                                      const uint16_t* __restrict__ g,
+                                                      uint16_t* __restrict__ out, int H,
+                                                      float eps) {
+  __shared__ float red[4];
+  const int64_t row = blockIdx.x;
+  const u32x4* xr = reinterpret_cast<const u32x4*>(x + row * H);
+  const u32x4* gr = reinterpret_cast<const u32x4*>(g);
+  u32x4* outr = reinterpret_cast<u32x4*>(out + row * H);
+  const int nchunk = H / 8;
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < nchunk; c += 256) {
+    u32x4 v = xr[c];
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      const float a = __uint_as_float(v[j] << 16), b = __uint_as_float(v[j] & 0xFFFF0000u);
+      ss += a * a + b * b;
+    }
+  }
+  const float total = block_sum_256(ss, red);
+  const float inv = 1.0f / sqrtf(total / (float)H + eps);
+  for (int c = threadIdx.x; c < nchunk; c += 256) {
+    u32x4 v = xr[c], gv = gr[c], w;
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      const float a = __uint_as_float(v[j] << 16) * inv * __uint_as_float(gv[j] << 16);
+      const float b = __uint_as_float(v[j] & 0xFFFF0000u) * inv * __uint_as_float(gv[j] & 0xFFFF0000u);
+      w[j] = pack_bf16x2(a, b);
+    }
+    outr[c] = w;
+  }
+}
+
+// ---------------------------------------------------------------- KV append
+__global__ __launch_bounds__(256) void kv_append_kernel(const uint16_t* __restrict__ k_new,
+                                                        const uint16_t* __restrict__ v_new,
+                                                        uint16_t* __restrict__ k_pool,
+                                                        uint16_t* __restrict__ v_pool,
+                                                        const int64_t* __restrict__ tok_slot,
+                                                        int nkv, int d) {
+  const int64_t t = blockIdx.x;
+  const int64_t slot = tok_slot[t];
+  const int64_t page = slot / 16;
+  const int s_in = (int)(slot % 16);
+  const int n = nkv * d;
+  const uint16_t* ks = k_new + t * n;
+  const uint16_t* vs = v_new + t * n;
+  // keys: 16-byte chunks, token-major within the page
+  for (int c = threadIdx.x; c < n / 8; c += blockDim.x) {
+    const int g = (c * 8) / d, e = (c * 8) % d;
+    *reinterpret_cast<u32x4*>(k_pool + ((page * nkv + g) * 16 + s_in) * d + e) =
+        *reinterpret_cast<const u32x4*>(ks + c * 8);
+  }
+  for (int u = threadIdx.x; u < n; u += blockDim.x) {
+    const int g = u / d, e = u % d;
+    v_pool[((page * nkv + g) * d + e) * 16 + s_in] = vs[u];
+  }
+}
+
+// ---------------------------------------------------------------- gather
+__global__ __launch_bounds__(256) void gather_kernel(const uint16_t* __restrict__ k_pool,
+                                                     const uint16_t* __restrict__ v_pool,
+                                                     const int32_t* __restrict__ pages, int nkv,
+                                                     int d, uint16_t* __restrict__ k_out,
+                                                     uint16_t* __restrict__ v_out) {
+  const int64_t j = blockIdx.x;
+  const int64_t page = pages[j / 16];
+  const int s_in = (int)(j % 16);
+  const int n = nkv * d;
+  for (int u = threadIdx.x; u < n; u += blockDim.x) {
+    const int g = u / d, e = u % d;
+    k_out[j * n + u] = k_pool[((page * nkv + g) * 16 + s_in) * d + e];
+    v_out[j * n + u] = v_pool[((page * nkv + g) * d + e) * 16 + s_in];
+  }
+}
+
+// ---------------------------------------------------------------- weight packing
+// Packed row p of w_qkv: rows of q and k heads with head_dim 128 are permuted
+// within the head so that packed rows 64 g + w and 64 g + 32 + w hold dims
+// 32 g + w and 64 + 32 g + w (the two halves of a rotary pair); v rows and
+// head_dim 64 keep their order.
+__global__ __launch_bounds__(256) void pack_qkv_kernel(const uint16_t* __restrict__ src,
+                                                       uint16_t* __restrict__ dst, int nq, int nkv,
+                                                       int d, int H) {
+  const int p = blockIdx.x;
+  const int head = p / d, within = p % d;
+  int sw = within;
+  if (head < nq + nkv && d == 128) {
+    const int g = within / 64, blk = (within % 64) / 32, w = within % 32;
+    sw = blk * 64 + g * 32 + w;
+  }
+  const u32x4* s = reinterpret_cast<const u32x4*>(src + ((int64_t)head * d + sw) * H);
+  u32x4* o = reinterpret_cast<u32x4*>(dst + (int64_t)p * H);
+  for (int c = threadIdx.x; c < H / 8; c += blockDim.x) o[c] = s[c];
+}
+
+// Packed row p of w_gate_up: block b = p / 32; even blocks are gate rows, odd
+// blocks the up rows of the same 32 features.
+__global__ __launch_bounds__(256) void interleave_kernel(const uint16_t* __restrict__ src,
+                                                         uint16_t* __restrict__ dst, int F, int H) {
+  const int p = blockIdx.x;
+  const int b = p / 32, w = p % 32, fb = b / 2;
+  const int srow = (b % 2 == 0) ? fb * 32 + w : F + fb * 32 + w;
+  const u32x4* s = reinterpret_cast<const u32x4*>(src + (int64_t)srow * H);
+  u32x4* o = reinterpret_cast<u32x4*>(dst + (int64_t)p * H);
+  for (int c = threadIdx.x; c < H / 8; c += blockDim.x) o[c] = s[c];
+}
+
+}  // namespace
+
+hipError_t launch_token_map(const ReqDev* reqs, int R, int T, const int32_t* pages,
+                            int32_t* tok_req, int32_t* tok_pos, int64_t* tok_slot,
+                            const double* inv_freq, float2* rope_cs, int half,
+                            hipStream_t stream) {
+  if (R == 0 || T == 0) return hipSuccess;
+  if (!rope_cs) half = 1;
+  const int64_t n = (int64_t)T * half;
+  token_map_kernel<<<(unsigned)((n + 255) / 256), 256, 0, stream>>>(
+      reqs, R, T, pages, tok_req, tok_pos, tok_slot, inv_freq, rope_cs, half);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* g, uint16_t* out, int T, int H,
+                          float eps, hipStream_t stream) {
+  if (T == 0) return hipSuccess;
+  rmsnorm_kernel<<<T, 256, 0, stream>>>(x, g, out, H, eps);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_append(const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_pool,
+                            uint16_t* v_pool, const int64_t* tok_slot, int T, int nkv, int d,
+                            hipStream_t stream) {
+  if (T == 0) return hipSuccess;
+  kv_append_kernel<<<T, 256, 0, stream>>>(k_new, v_new, k_pool, v_pool, tok_slot, nkv, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const uint16_t* k_pool, const uint16_t* v_pool, const int32_t* pages,
+                         int len, int nkv, int d, uint16_t* k_out, uint16_t* v_out,
+                         hipStream_t stream) {
+  if (len == 0) return hipSuccess;
+  gather_kernel<<<len, 256, 0, stream>>>(k_pool, v_pool, pages, nkv, d, k_out, v_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_qkv(const uint16_t* src, uint16_t* dst, int nq, int nkv, int d, int H,
+                           hipStream_t stream) {
+  pack_qkv_kernel<<<(nq + 2 * nkv) * d, 256, 0, stream>>>(src, dst, nq, nkv, d, H);
+  return hipGetLastError();
+}
+
+hipError_t launch_interleave_gate_up(const uint16_t* src, uint16_t* dst, int F, int H,
+                                     hipStream_t stream) {
+  interleave_kernel<<<2 * F, 256, 0, stream>>>(src, dst, F, H);
+  return hipGetLastError();
+}
+
+}  // namespace mx

@@ -1,0 +1,832 @@
+// mx_abi.cpp -- host side of libmx: argument validation, batch planning,
+// metadata upload and the orchestration of the gfx950 kernels behind the C ABI
+// declared in include/mx.h.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "mx.h"
+#include "mx_kernels.h"
+
+#define MX_EXPORT extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+using namespace mx;
+
+thread_local std::string g_err;
+
+mx_status fail(mx_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+mx_status hip_fail(hipError_t e, const char* what) {
+  return fail(MX_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// ------------------------------------------------------------------ validation
+mx_status validate_shape(const mx_attn_shape* s) {
+  if (!s) return fail(MX_ERR_NULL, "attention shape is NULL");
+  if (s->n_q_heads <= 0 || s->n_kv_heads <= 0)
+    return fail(MX_ERR_INVALID, "head counts must be positive (nq=%d, nkv=%d)", s->n_q_heads,
+                s->n_kv_heads);
+  if (s->n_q_heads % s->n_kv_heads != 0)
+    return fail(MX_ERR_INVALID, "n_q_heads %d is not a multiple of n_kv_heads %d", s->n_q_heads,
+                s->n_kv_heads);
+  if (s->n_q_heads > 32767) return fail(MX_ERR_UNSUPPORTED, "more than 32767 q heads");
+  if (s->head_dim != 64 && s->head_dim != 128)
+    return fail(MX_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", s->head_dim);
+  if (s->page_size != 16) return fail(MX_ERR_UNSUPPORTED, "page_size %d not supported (16)", s->page_size);
+  if (s->pool_pages <= 0) return fail(MX_ERR_INVALID, "pool_pages must be positive");
+  if (!(s->scale >= 0.f) || std::isinf(s->scale)) return fail(MX_ERR_INVALID, "invalid scale");
+  return MX_OK;
+}
+
+mx_status validate_batch(const mx_batch* b, const mx_attn_shape* s, int64_t* T_out) {
+  if (!b) return fail(MX_ERR_NULL, "batch is NULL");
+  mx_status st = validate_shape(s);
+  if (st != MX_OK) return st;
+  if (b->num_reqs < 0) return fail(MX_ERR_INVALID, "num_reqs %d < 0", b->num_reqs);
+  if (b->num_reqs > 0 && !b->reqs) return fail(MX_ERR_NULL, "reqs is NULL");
+  int64_t T = 0;
+  std::vector<int64_t> slots;
+  for (int r = 0; r < b->num_reqs; r++) {
+    const mx_request& q = b->reqs[r];
+    if (q.phase != MX_PREFILL && q.phase != MX_DECODE)
+      return fail(MX_ERR_INVALID, "request %d: bad phase %d", r, q.phase);
+    if (q.n_new < 1) return fail(MX_ERR_INVALID, "request %d: n_new %d < 1", r, q.n_new);
+    if (q.ctx_len < 0) return fail(MX_ERR_INVALID, "request %d: ctx_len %d < 0", r, q.ctx_len);
+    if (q.phase == MX_DECODE && (q.n_new != 1 || q.ctx_len < 1))
+      return fail(MX_ERR_INVALID, "request %d: a decode needs n_new == 1 and ctx_len >= 1", r);
+    const int64_t kv_len = (int64_t)q.ctx_len + q.n_new;
+    if (kv_len > (int64_t)INT32_MAX - 16) return fail(MX_ERR_TOO_LARGE, "request %d: context too long", r);
+    const int64_t need = ceil_div(kv_len, 16);
+    if (q.n_pages < need)
+      return fail(MX_ERR_NO_SPACE, "request %d: %d pages for %lld tokens (need %lld)", r, q.n_pages,
+                  (long long)kv_len, (long long)need);
+    if (!q.pages) return fail(MX_ERR_NULL, "request %d: pages is NULL", r);
+    for (int i = 0; i < q.n_pages; i++)
+      if (q.pages[i] < 0 || q.pages[i] >= s->pool_pages)
+        return fail(MX_ERR_INVALID, "request %d: page id %d outside [0, %lld)", r, q.pages[i],
+                    (long long)s->pool_pages);
+    for (int i = 0; i < q.n_new; i++) {
+      const int64_t p = (int64_t)q.ctx_len + i;
+      slots.push_back((int64_t)q.pages[p / 16] * 16 + p % 16);
+    }
+    T += q.n_new;
+    if (T > INT32_MAX / 2) return fail(MX_ERR_TOO_LARGE, "too many tokens");
+  }
+  std::sort(slots.begin(), slots.end());
+  for (size_t i = 1; i < slots.size(); i++)
+    if (slots[i] == slots[i - 1])
+      return fail(MX_ERR_INVALID, "two new tokens write the same KV slot %lld", (long long)slots[i]);
+  if (T_out) *T_out = T;
+  return MX_OK;
+}
+
+mx_status validate_cfg(const mx_layer_cfg* c) {
+  if (!c) return fail(MX_ERR_NULL, "layer cfg is NULL");
+  mx_status st = validate_shape(&c->attn);
+  if (st != MX_OK) return st;
+  if (c->hidden <= 0 || c->hidden % 64)
+    return fail(MX_ERR_UNSUPPORTED, "hidden %d must be a positive multiple of 64", c->hidden);
+  if (c->ffn <= 0 || c->ffn % 64)
+    return fail(MX_ERR_UNSUPPORTED, "ffn %d must be a positive multiple of 64", c->ffn);
+  if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f))
+    return fail(MX_ERR_INVALID, "invalid rms_eps or rope_theta");
+  return MX_OK;
+}
+
+// ------------------------------------------------------------------ planning
+struct Plan {
+  int R = 0, T = 0;
+  std::vector<ReqDev> reqs;
+  std::vector<int32_t> pages;
+  std::vector<AttnItem> items;
+  std::vector<MergeItem> merges;
+  int64_t n_parts = 0;
+  int split_pages = 16;
+  int group = 1;
+};
+
+// Decode splits: enough work items to fill the chip several times over, but at
+// least 8 pages (four waves x two pages) per split.
+int choose_split_pages(const mx_batch* b, const mx_attn_shape* s) {
+  const int group = s->n_q_heads / s->n_kv_heads;
+  const int64_t sub = s->n_kv_heads * ceil_div(group, 16);
+  int64_t total = 0;
+  for (int r = 0; r < b->num_reqs; r++)
+    if (b->reqs[r].phase == MX_DECODE)
+      total += ceil_div((int64_t)b->reqs[r].ctx_len + 1, 16) * sub;
+  const int64_t target_items = 2048;
+  int64_t sp = ceil_div(std::max<int64_t>(total, 1), target_items);
+  sp = std::max<int64_t>(8, std::min<int64_t>(sp, 4096));
+  sp = (sp + 1) / 2 * 2;
+  return (int)sp;
+}
+
+void build_plan(const mx_batch* b, const mx_attn_shape* s, bool with_items, Plan& p) {
+  p.R = b->num_reqs;
+  p.group = s->n_q_heads / s->n_kv_heads;
+  p.split_pages = choose_split_pages(b, s);
+  p.reqs.resize(p.R);
+  int tok = 0, pg = 0;
+  for (int r = 0; r < p.R; r++) {
+    const mx_request& q = b->reqs[r];
+    ReqDev& d = p.reqs[r];
+    d.tok_start = tok;
+    d.n_new = q.n_new;
+    d.ctx_len = q.ctx_len;
+    d.kv_len = q.ctx_len + q.n_new;
+    d.page_start = pg;
+    d.n_pages = (int)ceil_div(d.kv_len, 16);
+    d.phase = q.phase;
+    d.n_split = 1;
+    for (int i = 0; i < d.n_pages; i++) p.pages.push_back(q.pages[i]);
+    tok += q.n_new;
+    pg += d.n_pages;
+  }
+  p.T = tok;
+  if (!with_items) return;
+  const int nq = s->n_q_heads;
+  // prefill q tiles first (heaviest work first: later tiles see more keys)
+  for (int r = 0; r < p.R; r++) {
+    const ReqDev& d = p.reqs[r];
+    if (d.phase != MX_PREFILL) continue;
+    const int tiles = (int)ceil_div(d.n_new, 64);
+    for (int qt = tiles - 1; qt >= 0; qt--)
+      for (int h = 0; h < nq; h++) {
+        AttnItem it;
+        it.req = r;
+        it.head = (int16_t)h;
+        it.kind = 1;
+        it.nrows = 16;
+        it.start = qt * 64;
+        it.part = 0;
+        p.items.push_back(it);
+      }
+  }
+  // decode splits
+  for (int r = 0; r < p.R; r++) {
+    ReqDev& d = p.reqs[r];
+    if (d.phase != MX_DECODE) continue;
+    const int ns = (int)ceil_div(d.n_pages, p.split_pages);
+    d.n_split = ns;
+    int64_t part_base = 0;
+    if (ns > 1) {
+      part_base = p.n_parts;
+      p.n_parts += (int64_t)nq * ns;
+      p.merges.push_back(MergeItem{r, (int32_t)part_base});
+    }
+    for (int sp = 0; sp < ns; sp++)
+      for (int g = 0; g < s->n_kv_heads; g++)
+        for (int h0 = 0; h0 < p.group; h0 += 16) {
+          AttnItem it;
+          it.req = r;
+          it.head = (int16_t)(g * p.group + h0);
+          it.kind = 0;
+          it.nrows = (int8_t)std::min(16, p.group - h0);
+          it.start = sp * p.split_pages;
+          it.part = (int32_t)(part_base + (int64_t)it.head * ns + sp);
+          p.items.push_back(it);
+        }
+  }
+}
+
+// ------------------------------------------------------------------ workspace layout
+struct Layout {
+  size_t reqs = 0, pages = 0, items = 0, merges = 0, inv_freq = 0, meta_end = 0;
+  size_t tok_req = 0, tok_pos = 0, tok_slot = 0, rope_cs = 0;
+  size_t part_o = 0, part_ml = 0;
+  size_t h = 0, q = 0, o = 0, x1 = 0, a = 0, scratch = 0, scratch_floats = 0;
+  size_t total = 0;
+};
+
+size_t gemm_scratch_bound(const mx_layer_cfg* c, int64_t T) {
+  const int H = c->hidden, F = c->ffn, nq = c->attn.n_q_heads, nkv = c->attn.n_kv_heads,
+            d = c->attn.head_dim;
+  const int M = (int)T;
+  size_t m = gemm_scratch_floats(M, (nq + 2 * nkv) * d, H);
+  m = std::max(m, gemm_scratch_floats(M, H, nq * d));
+  m = std::max(m, gemm_scratch_floats(M, 2 * F, H));
+  m = std::max(m, gemm_scratch_floats(M, H, F));
+  return m;
+}
+
+Layout make_layout(int64_t R, int64_t T, int64_t n_pages, int64_t n_items, int64_t n_merges,
+                   int64_t n_parts, const mx_attn_shape* s, const mx_layer_cfg* c,
+                   size_t scratch_floats) {
+  Layout L;
+  size_t o = 0;
+  const int d = s->head_dim;
+  L.reqs = o; o = align_up(o + R * sizeof(ReqDev));
+  L.pages = o; o = align_up(o + n_pages * sizeof(int32_t));
+  L.items = o; o = align_up(o + n_items * sizeof(AttnItem));
+  L.merges = o; o = align_up(o + n_merges * sizeof(MergeItem));
+  L.inv_freq = o; o = align_up(o + (d / 2) * sizeof(double));
+  L.meta_end = o;
+  L.tok_req = o; o = align_up(o + T * 4);
+  L.tok_pos = o; o = align_up(o + T * 4);
+  L.tok_slot = o; o = align_up(o + T * 8);
+  L.part_o = o; o = align_up(o + n_parts * d * 4);
+  L.part_ml = o; o = align_up(o + n_parts * 8);
+  if (c) {
+    const int64_t H = c->hidden, F = c->ffn, nq = s->n_q_heads;
+    L.rope_cs = o; o = align_up(o + T * (d / 2) * 8);
+    L.h = o; o = align_up(o + T * H * 2);
+    L.q = o; o = align_up(o + T * nq * d * 2);
+    L.o = o; o = align_up(o + T * nq * d * 2);
+    L.x1 = o; o = align_up(o + T * H * 2);
+    L.a = o; o = align_up(o + T * F * 2);
+    L.scratch = o; o = align_up(o + scratch_floats * 4);
+    L.scratch_floats = scratch_floats;
+  }
+  L.total = o;
+  return L;
+}
+
+Layout layout_for(const Plan& p, const mx_attn_shape* s, const mx_layer_cfg* c) {
+  const size_t sc = c ? gemm_scratch_bound(c, p.T) : 0;
+  return make_layout(p.R, p.T, (int64_t)p.pages.size(), (int64_t)p.items.size(),
+                     (int64_t)p.merges.size(), p.n_parts, s, c, sc);
+}
+
+// ------------------------------------------------------------------ per-device state
+struct DeviceState {
+  std::mutex mu;
+  bool init = false;
+  static constexpr int kRing = 8;
+  void* buf[kRing] = {};
+  size_t cap[kRing] = {};
+  hipEvent_t ev[kRing] = {};
+  bool used[kRing] = {};
+  int next = 0;
+};
+
+std::mutex g_dev_mu;
+std::map<int, DeviceState*> g_devs;
+
+mx_status device_state(DeviceState** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  DeviceState* ds;
+  {
+    std::lock_guard<std::mutex> g(g_dev_mu);
+    auto it = g_devs.find(dev);
+    if (it == g_devs.end()) {
+      ds = new DeviceState();
+      g_devs[dev] = ds;
+    } else {
+      ds = it->second;
+    }
+  }
+  std::lock_guard<std::mutex> g(ds->mu);
+  if (!ds->init) {
+    e = gemm_init();
+    if (e != hipSuccess) return hip_fail(e, "kernel attribute setup");
+    for (int i = 0; i < DeviceState::kRing; i++) {
+      e = hipEventCreateWithFlags(&ds->ev[i], hipEventDisableTiming);
+      if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
+    }
+    ds->init = true;
+  }
+  *out = ds;
+  return MX_OK;
+}
+
+// Packs the plan's metadata into a pinned staging buffer and enqueues its copy
+// into the workspace.  A staging slot is reused only after its previous copy
+// has completed.
+mx_status upload_meta(const Plan& p, const Layout& L, const mx_attn_shape* s, float theta,
+                      void* ws, hipStream_t stream) {
+  DeviceState* ds;
+  mx_status st = device_state(&ds);
+  if (st != MX_OK) return st;
+  std::lock_guard<std::mutex> g(ds->mu);
+  const int i = ds->next;
+  ds->next = (ds->next + 1) % DeviceState::kRing;
+  hipError_t e;
+  if (ds->used[i]) {
+    e = hipEventSynchronize(ds->ev[i]);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+  }
+  if (ds->cap[i] < L.meta_end) {
+    if (ds->buf[i]) hipHostFree(ds->buf[i]);
+    ds->buf[i] = nullptr;
+    const size_t cap = std::max<size_t>(L.meta_end * 2, 1 << 16);
+    e = hipHostMalloc(&ds->buf[i], cap, hipHostMallocDefault);
+    if (e != hipSuccess) { ds->cap[i] = 0; return hip_fail(e, "hipHostMalloc"); }
+    ds->cap[i] = cap;
+  }
+  char* h = (char*)ds->buf[i];
+  memset(h, 0, L.meta_end);
+  if (!p.reqs.empty()) memcpy(h + L.reqs, p.reqs.data(), p.reqs.size() * sizeof(ReqDev));
+  if (!p.pages.empty()) memcpy(h + L.pages, p.pages.data(), p.pages.size() * sizeof(int32_t));
+  if (!p.items.empty()) memcpy(h + L.items, p.items.data(), p.items.size() * sizeof(AttnItem));
+  if (!p.merges.empty()) memcpy(h + L.merges, p.merges.data(), p.merges.size() * sizeof(MergeItem));
+  double* inv = (double*)(h + L.inv_freq);
+  const int d = s->head_dim;
+  for (int k = 0; k < d / 2; k++) inv[k] = std::pow((double)theta, -2.0 * k / d);
+  e = hipMemcpyAsync(ws, h, L.meta_end, hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (metadata)");
+  e = hipEventRecord(ds->ev[i], stream);
+  if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+  ds->used[i] = true;
+  return MX_OK;
+}
+
+template <typename T>
+T* at(void* ws, size_t off) { return reinterpret_cast<T*>((char*)ws + off); }
+
+float eff_scale(const mx_attn_shape* s) {
+  return s->scale > 0.f ? s->scale : 1.0f / std::sqrt((float)s->head_dim);
+}
+
+AttnParams attn_params(const Plan& p, const Layout& L, const mx_attn_shape* s, void* ws,
+                       const uint16_t* q, int64_t q_stride, const uint16_t* kp,
+                       const uint16_t* vp, uint16_t* out) {
+  AttnParams a;
+  a.q = q;
+  a.q_tok_stride = q_stride;
+  a.k_pool = kp;
+  a.v_pool = vp;
+  a.out = out;
+  a.out_tok_stride = (int64_t)s->n_q_heads * s->head_dim;
+  a.reqs = at<ReqDev>(ws, L.reqs);
+  a.pages = at<int32_t>(ws, L.pages);
+  a.items = at<AttnItem>(ws, L.items);
+  a.part_o = at<float>(ws, L.part_o);
+  a.part_ml = at<float>(ws, L.part_ml);
+  a.nq = s->n_q_heads;
+  a.nkv = s->n_kv_heads;
+  a.group = p.group;
+  a.split_pages = p.split_pages;
+  a.scale_log2 = eff_scale(s) * 1.4426950408889634f;
+  return a;
+}
+
+// packed weight regions
+struct WLayout {
+  size_t g1, qkv, o, g2, gu, down, total;
+};
+WLayout wlayout(const mx_layer_cfg* c) {
+  const size_t H = c->hidden, F = c->ffn, nq = c->attn.n_q_heads, nkv = c->attn.n_kv_heads,
+               d = c->attn.head_dim;
+  WLayout w;
+  size_t o = 0;
+  w.g1 = o; o = align_up(o + H * 2);
+  w.qkv = o; o = align_up(o + (nq + 2 * nkv) * d * H * 2);
+  w.o = o; o = align_up(o + H * nq * d * 2);
+  w.g2 = o; o = align_up(o + H * 2);
+  w.gu = o; o = align_up(o + 2 * F * H * 2);
+  w.down = o; o = align_up(o + H * F * 2);
+  w.total = o;
+  return w;
+}
+
+// ------------------------------------------------------------------ launch timing
+// Optional per-launch timing (hipEvents recorded on the caller's stream around
+// each kernel launch).  Off by default; costs two event records per launch.
+struct Profiler {
+  std::mutex mu;
+  bool on = false;
+  struct Rec {
+    const char* name;
+    hipEvent_t a, b;
+  };
+  std::vector<Rec> pending;
+  std::vector<hipEvent_t> free_events;
+  std::vector<const char*> names;
+  std::vector<double> total_ms;
+  std::vector<int> counts;
+
+  hipEvent_t get() {
+    if (!free_events.empty()) {
+      hipEvent_t e = free_events.back();
+      free_events.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+};
+Profiler g_prof;
+
+template <typename F>
+hipError_t timed(const char* name, hipStream_t stream, F&& launch) {
+  bool on;
+  {
+    std::lock_guard<std::mutex> g(g_prof.mu);
+    on = g_prof.on;
+  }
+  if (!on) return launch();
+  hipEvent_t a, b;
+  {
+    std::lock_guard<std::mutex> g(g_prof.mu);
+    a = g_prof.get();
+    b = g_prof.get();
+  }
+  if (!a || !b) return launch();
+  hipError_t e = hipEventRecord(a, stream);
+  if (e != hipSuccess) return e;
+  e = launch();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(b, stream);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> g(g_prof.mu);
+  g_prof.pending.push_back({name, a, b});
+  return hipSuccess;
+}
+
+}  // namespace
+
+// ======================================================================= ABI
+MX_EXPORT const char* mx_status_str(mx_status s) {
+  switch (s) {
+    case MX_OK: return "MX_OK";
+    case MX_ERR_INVALID: return "MX_ERR_INVALID";
+    case MX_ERR_NO_SPACE: return "MX_ERR_NO_SPACE";
+    case MX_ERR_TOO_LARGE: return "MX_ERR_TOO_LARGE";
+    case MX_ERR_UNSUPPORTED: return "MX_ERR_UNSUPPORTED";
+    case MX_ERR_NULL: return "MX_ERR_NULL";
+    case MX_ERR_HIP: return "MX_ERR_HIP";
+  }
+  return "MX_ERR_UNKNOWN";
+}
+
+MX_EXPORT const char* mx_last_error(void) { return g_err.c_str(); }
+
+MX_EXPORT uint32_t mx_version(void) { return (1u << 16) | 0u; }
+
+MX_EXPORT mx_status mx_batch_validate(const mx_batch* batch, const mx_attn_shape* shape) {
+  g_err.clear();
+  return validate_batch(batch, shape, nullptr);
+}
+
+MX_EXPORT size_t mx_workspace_bytes_for(const mx_batch* batch, const mx_attn_shape* shape,
+                                        const mx_layer_cfg* cfg) {
+  g_err.clear();
+  if (cfg) {
+    if (validate_cfg(cfg) != MX_OK) return 0;
+    shape = &cfg->attn;
+  }
+  if (validate_batch(batch, shape, nullptr) != MX_OK) return 0;
+  Plan p;
+  build_plan(batch, shape, true, p);
+  return layout_for(p, shape, cfg).total;
+}
+
+MX_EXPORT size_t mx_workspace_bytes(const mx_layer_cfg* cfg, const mx_attn_shape* shape,
+                                    int32_t max_tokens, int32_t max_reqs, int64_t max_pages) {
+  g_err.clear();
+  if (cfg) {
+    if (validate_cfg(cfg) != MX_OK) return 0;
+    shape = &cfg->attn;
+  } else if (validate_shape(shape) != MX_OK) {
+    return 0;
+  }
+  if (max_tokens < 0 || max_reqs < 0 || max_pages < 0) {
+    fail(MX_ERR_INVALID, "negative bound");
+    return 0;
+  }
+  const int64_t nq = shape->n_q_heads, nkv = shape->n_kv_heads, group = nq / nkv;
+  // every split has at least 8 pages, so splits <= pages / 8 + requests
+  const int64_t splits = max_pages / 8 + max_reqs;
+  const int64_t items = splits * nkv * ceil_div(group, 16) + (max_tokens / 64 + max_reqs) * nq;
+  const int64_t parts = splits * nq;
+  const size_t scratch = cfg ? kMaxSplitFloats : 0;
+  return make_layout(max_reqs, max_tokens, max_pages, items, max_reqs, parts, shape, cfg, scratch)
+      .total;
+}
+
+MX_EXPORT size_t mx_packed_weights_bytes(const mx_layer_cfg* cfg) {
+  g_err.clear();
+  if (validate_cfg(cfg) != MX_OK) return 0;
+  return wlayout(cfg).total;
+}
+
+MX_EXPORT mx_status mx_pack_weights(const mx_layer_cfg* cfg, const mx_layer_weights* w,
+                                    void* packed, size_t packed_bytes, hipStream_t stream) {
+  g_err.clear();
+  mx_status st = validate_cfg(cfg);
+  if (st != MX_OK) return st;
+  if (!w || !packed || !w->ln1_g || !w->w_qkv || !w->w_o || !w->ln2_g || !w->w_gate_up || !w->w_down)
+    return fail(MX_ERR_NULL, "weight pointer is NULL");
+  const WLayout L = wlayout(cfg);
+  if (packed_bytes < L.total)
+    return fail(MX_ERR_TOO_LARGE, "packed buffer %zu bytes < %zu", packed_bytes, L.total);
+  DeviceState* ds;
+  st = device_state(&ds);
+  if (st != MX_OK) return st;
+  const size_t H = cfg->hidden, F = cfg->ffn, nq = cfg->attn.n_q_heads,
+               nkv = cfg->attn.n_kv_heads, d = cfg->attn.head_dim;
+  char* P = (char*)packed;
+  hipError_t e;
+#define MX_CP(off, src, bytes)                                                        \
+  e = hipMemcpyAsync(P + (off), (src), (bytes), hipMemcpyDeviceToDevice, stream);    \
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (pack)");
+  MX_CP(L.g1, w->ln1_g, H * 2)
+  MX_CP(L.o, w->w_o, H * nq * d * 2)
+  MX_CP(L.g2, w->ln2_g, H * 2)
+  MX_CP(L.down, w->w_down, H * F * 2)
+#undef MX_CP
+  e = launch_interleave_gate_up(w->w_gate_up, (uint16_t*)(P + L.gu), (int)F, (int)H, stream);
+  if (e != hipSuccess) return hip_fail(e, "interleave launch");
+  e = launch_pack_qkv(w->w_qkv, (uint16_t*)(P + L.qkv), (int)nq, (int)nkv, (int)d, (int)H, stream);
+  if (e != hipSuccess) return hip_fail(e, "qkv packing launch");
+  return MX_OK;
+}
+
+static mx_status check_ws(const Layout& L, void* ws, size_t ws_bytes) {
+  if (!ws) return fail(MX_ERR_NULL, "workspace is NULL");
+  if (ws_bytes < L.total)
+    return fail(MX_ERR_TOO_LARGE, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
+  return MX_OK;
+}
+
+MX_EXPORT mx_status mx_kv_append(const mx_batch* batch, const mx_attn_shape* shape,
+                                 const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_pool,
+                                 uint16_t* v_pool, void* ws, size_t ws_bytes, hipStream_t stream) {
+  g_err.clear();
+  int64_t T;
+  mx_status st = validate_batch(batch, shape, &T);
+  if (st != MX_OK) return st;
+  if (T == 0) return MX_OK;
+  if (!k_new || !v_new || !k_pool || !v_pool) return fail(MX_ERR_NULL, "tensor pointer is NULL");
+  Plan p;
+  build_plan(batch, shape, false, p);
+  const Layout L = layout_for(p, shape, nullptr);
+  if ((st = check_ws(L, ws, ws_bytes)) != MX_OK) return st;
+  if ((st = upload_meta(p, L, shape, 1e4f, ws, stream)) != MX_OK) return st;
+  hipError_t e = launch_token_map(at<ReqDev>(ws, L.reqs), p.R, p.T, at<int32_t>(ws, L.pages),
+                                  at<int32_t>(ws, L.tok_req), at<int32_t>(ws, L.tok_pos),
+                                  at<int64_t>(ws, L.tok_slot), nullptr, nullptr, 0, stream);
+  if (e != hipSuccess) return hip_fail(e, "token map launch");
+  e = launch_kv_append(k_new, v_new, k_pool, v_pool, at<int64_t>(ws, L.tok_slot), p.T,
+                       shape->n_kv_heads, shape->head_dim, stream);
+  if (e != hipSuccess) return hip_fail(e, "kv append launch");
+  return MX_OK;
+}
+
+MX_EXPORT mx_status mx_paged_attn(const mx_batch* batch, const mx_attn_shape* shape,
+                                  const uint16_t* q, const uint16_t* k_pool, const uint16_t* v_pool,
+                                  uint16_t* out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  g_err.clear();
+  int64_t T;
+  mx_status st = validate_batch(batch, shape, &T);
+  if (st != MX_OK) return st;
+  if (T == 0) return MX_OK;
+  if (!q || !k_pool || !v_pool || !out) return fail(MX_ERR_NULL, "tensor pointer is NULL");
+  Plan p;
+  build_plan(batch, shape, true, p);
+  const Layout L = layout_for(p, shape, nullptr);
+  if ((st = check_ws(L, ws, ws_bytes)) != MX_OK) return st;
+  if ((st = upload_meta(p, L, shape, 1e4f, ws, stream)) != MX_OK) return st;
+  AttnParams a = attn_params(p, L, shape, ws, q, (int64_t)shape->n_q_heads * shape->head_dim,
+                             k_pool, v_pool, out);
+  hipError_t e = timed("paged_attn", stream, [&] {
+    return launch_paged_attn(a, (int)p.items.size(), at<MergeItem>(ws, L.merges),
+                             (int)p.merges.size(), shape->head_dim, stream);
+  });
+  if (e != hipSuccess) return hip_fail(e, "attention launch");
+  return MX_OK;
+}
+
+MX_EXPORT mx_status mx_layer_step(const mx_batch* batch, const mx_layer_cfg* cfg,
+                                  const void* packed_weights, const uint16_t* x, uint16_t* y,
+                                  uint16_t* k_pool, uint16_t* v_pool, void* ws, size_t ws_bytes,
+                                  hipStream_t stream) {
+  g_err.clear();
+  mx_status st = validate_cfg(cfg);
+  if (st != MX_OK) return st;
+  const mx_attn_shape* s = &cfg->attn;
+  int64_t T;
+  if ((st = validate_batch(batch, s, &T)) != MX_OK) return st;
+  if (T == 0) return MX_OK;
+  if (!packed_weights || !x || !y || !k_pool || !v_pool)
+    return fail(MX_ERR_NULL, "tensor pointer is NULL");
+  if (x == y) return fail(MX_ERR_INVALID, "y must not alias x");
+  Plan p;
+  build_plan(batch, s, true, p);
+  const Layout L = layout_for(p, s, cfg);
+  if ((st = check_ws(L, ws, ws_bytes)) != MX_OK) return st;
+  if ((st = upload_meta(p, L, s, cfg->rope_theta, ws, stream)) != MX_OK) return st;
+  const WLayout W = wlayout(cfg);
+  const char* P = (const char*)packed_weights;
+  const int H = cfg->hidden, F = cfg->ffn, nq = s->n_q_heads, nkv = s->n_kv_heads,
+            d = s->head_dim;
+  const int Nqkv = (nq + 2 * nkv) * d;
+  const int M = p.T;
+  uint16_t* h = at<uint16_t>(ws, L.h);
+  uint16_t* q = at<uint16_t>(ws, L.q);
+  uint16_t* o = at<uint16_t>(ws, L.o);
+  uint16_t* x1 = at<uint16_t>(ws, L.x1);
+  uint16_t* act = at<uint16_t>(ws, L.a);
+  float* scratch = at<float>(ws, L.scratch);
+  float2* rope_cs = at<float2>(ws, L.rope_cs);
+  hipError_t e;
+#define MX_CK(call, what) \
+  if ((e = (call)) != hipSuccess) return hip_fail(e, what);
+  // a1: token map and rotary table
+  MX_CK(timed("token_map", stream, [&] {
+          return launch_token_map(at<ReqDev>(ws, L.reqs), p.R, p.T, at<int32_t>(ws, L.pages),
+                                  at<int32_t>(ws, L.tok_req), at<int32_t>(ws, L.tok_pos),
+                                  at<int64_t>(ws, L.tok_slot), at<double>(ws, L.inv_freq),
+                                  rope_cs, d / 2, stream);
+        }), "token map launch")
+  // a2: RMSNorm 1
+  MX_CK(timed("rmsnorm_1", stream, [&] {
+          return launch_rmsnorm(x, (const uint16_t*)(P + W.g1), h, M, H, cfg->rms_eps, stream);
+        }), "rmsnorm launch")
+  // a3-a5: QKV projection with RoPE and the KV append fused into its epilogue
+  {
+    GemmArgs g{h, (const uint16_t*)(P + W.qkv), nullptr, nullptr, scratch, M, Nqkv, H, H, H, 0, 0, EPI_QKV,
+               QkvEpilogue{rope_cs, at<int64_t>(ws, L.tok_slot), q, k_pool, v_pool, nq, nkv, d}};
+    MX_CK(timed("gemm_qkv", stream, [&] { return launch_gemm(g, L.scratch_floats, stream); }),
+          "qkv gemm launch")
+  }
+  // a6: paged attention, prefill and decode rows in one launch (+ split merge)
+  {
+    AttnParams a = attn_params(p, L, s, ws, q, (int64_t)nq * d, k_pool, v_pool, o);
+    MX_CK(timed("paged_attn", stream, [&] {
+            return launch_paged_attn(a, (int)p.items.size(), at<MergeItem>(ws, L.merges),
+                                     (int)p.merges.size(), d, stream);
+          }), "attention launch")
+  }
+  // a7: output projection + residual
+  {
+    GemmArgs g{o, (const uint16_t*)(P + W.o), x1, x, scratch, M, H, nq * d, nq * d, nq * d, H, H, EPI_RESIDUAL, {}};
+    MX_CK(timed("gemm_o", stream, [&] { return launch_gemm(g, L.scratch_floats, stream); }),
+          "o gemm launch")
+  }
+  // a8: RMSNorm 2
+  MX_CK(timed("rmsnorm_2", stream, [&] {
+          return launch_rmsnorm(x1, (const uint16_t*)(P + W.g2), h, M, H, cfg->rms_eps, stream);
+        }), "rmsnorm launch")
+  // a9: gate/up projection + SwiGLU
+  {
+    GemmArgs g{h, (const uint16_t*)(P + W.gu), act, nullptr, scratch, M, 2 * F, H, H, H, F, 0, EPI_SWIGLU, {}};
+    MX_CK(timed("gemm_gate_up", stream, [&] { return launch_gemm(g, L.scratch_floats, stream); }),
+          "gate/up gemm launch")
+  }
+  // a10: down projection + residual
+  {
+    GemmArgs g{act, (const uint16_t*)(P + W.down), y, x1, scratch, M, H, F, F, F, H, H, EPI_RESIDUAL, {}};
+    MX_CK(timed("gemm_down", stream, [&] { return launch_gemm(g, L.scratch_floats, stream); }),
+          "down gemm launch")
+  }
+#undef MX_CK
+  return MX_OK;
+}
+
+MX_EXPORT mx_status mx_layer_workspace_offsets(const mx_batch* batch, const mx_layer_cfg* cfg,
+                                               size_t off[5]) {
+  g_err.clear();
+  mx_status st = validate_cfg(cfg);
+  if (st != MX_OK) return st;
+  if ((st = validate_batch(batch, &cfg->attn, nullptr)) != MX_OK) return st;
+  if (!off) return fail(MX_ERR_NULL, "off is NULL");
+  Plan p;
+  build_plan(batch, &cfg->attn, true, p);
+  const Layout L = layout_for(p, &cfg->attn, cfg);
+  off[0] = L.h;
+  off[1] = L.q;
+  off[2] = L.o;
+  off[3] = L.x1;
+  off[4] = L.a;
+  return MX_OK;
+}
+
+MX_EXPORT mx_status mx_debug_token_map(const mx_batch* batch, const mx_attn_shape* shape,
+                                       int32_t* tok_req, int32_t* tok_pos, int64_t* tok_slot,
+                                       void* ws, size_t ws_bytes, hipStream_t stream) {
+  g_err.clear();
+  int64_t T;
+  mx_status st = validate_batch(batch, shape, &T);
+  if (st != MX_OK) return st;
+  if (T == 0) return MX_OK;
+  if (!tok_req || !tok_pos || !tok_slot) return fail(MX_ERR_NULL, "output pointer is NULL");
+  Plan p;
+  build_plan(batch, shape, false, p);
+  const Layout L = layout_for(p, shape, nullptr);
+  if ((st = check_ws(L, ws, ws_bytes)) != MX_OK) return st;
+  if ((st = upload_meta(p, L, shape, 1e4f, ws, stream)) != MX_OK) return st;
+  hipError_t e = launch_token_map(at<ReqDev>(ws, L.reqs), p.R, p.T, at<int32_t>(ws, L.pages),
+                                  at<int32_t>(ws, L.tok_req), at<int32_t>(ws, L.tok_pos),
+                                  at<int64_t>(ws, L.tok_slot), nullptr, nullptr, 0, stream);
+  if (e != hipSuccess) return hip_fail(e, "token map launch");
+  e = hipMemcpyAsync(tok_req, at<int32_t>(ws, L.tok_req), T * 4, hipMemcpyDeviceToDevice, stream);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(tok_pos, at<int32_t>(ws, L.tok_pos), T * 4, hipMemcpyDeviceToDevice, stream);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(tok_slot, at<int64_t>(ws, L.tok_slot), T * 8, hipMemcpyDeviceToDevice, stream);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (token map)");
+  return MX_OK;
+}
+
+MX_EXPORT mx_status mx_debug_gather(const mx_batch* batch, const mx_attn_shape* shape, int32_t req,
+                                    const uint16_t* k_pool, const uint16_t* v_pool,
+                                    uint16_t* k_out, uint16_t* v_out, void* ws, size_t ws_bytes,
+                                    hipStream_t stream) {
+  g_err.clear();
+  mx_status st = validate_batch(batch, shape, nullptr);
+  if (st != MX_OK) return st;
+  if (req < 0 || req >= batch->num_reqs) return fail(MX_ERR_INVALID, "request %d out of range", req);
+  if (!k_pool || !v_pool || !k_out || !v_out) return fail(MX_ERR_NULL, "tensor pointer is NULL");
+  Plan p;
+  build_plan(batch, shape, false, p);
+  const Layout L = layout_for(p, shape, nullptr);
+  if ((st = check_ws(L, ws, ws_bytes)) != MX_OK) return st;
+  if ((st = upload_meta(p, L, shape, 1e4f, ws, stream)) != MX_OK) return st;
+  const ReqDev& rq = p.reqs[req];
+  hipError_t e = launch_gather(k_pool, v_pool, at<int32_t>(ws, L.pages) + rq.page_start, rq.kv_len,
+                               shape->n_kv_heads, shape->head_dim, k_out, v_out, stream);
+  if (e != hipSuccess) return hip_fail(e, "gather launch");
+  return MX_OK;
+}
+
+MX_EXPORT size_t mx_debug_gemm_ws_bytes(int32_t M, int32_t N, int32_t K) {
+  if (M < 0 || N <= 0 || K <= 0) return 0;
+  return align_up(gemm_scratch_floats(M, N, K) * 4 + 4);
+}
+
+MX_EXPORT mx_status mx_debug_gemm(int32_t M, int32_t N, int32_t K, const uint16_t* A,
+                                  const uint16_t* B, uint16_t* C, const uint16_t* R,
+                                  int32_t epilogue, void* ws, size_t ws_bytes, hipStream_t stream) {
+  g_err.clear();
+  if (M < 0 || N <= 0 || K <= 0) return fail(MX_ERR_INVALID, "bad GEMM shape %d x %d x %d", M, N, K);
+  if (K % 64) return fail(MX_ERR_UNSUPPORTED, "K %d is not a multiple of 64", K);
+  if (epilogue < 0 || epilogue > 2) return fail(MX_ERR_INVALID, "bad epilogue %d", epilogue);
+  if (epilogue == EPI_SWIGLU && N % 64) return fail(MX_ERR_UNSUPPORTED, "SwiGLU needs N % 64 == 0");
+  if (M == 0) return MX_OK;
+  if (!A || !B || !C || (epilogue == EPI_RESIDUAL && !R)) return fail(MX_ERR_NULL, "NULL operand");
+  const size_t need = gemm_scratch_floats(M, N, K);
+  if (need && (!ws || ws_bytes < need * 4))
+    return fail(MX_ERR_TOO_LARGE, "GEMM scratch %zu bytes < %zu", ws_bytes, need * 4);
+  DeviceState* ds;
+  mx_status st = device_state(&ds);
+  if (st != MX_OK) return st;
+  const int ldc = epilogue == EPI_SWIGLU ? N / 2 : N;
+  GemmArgs g{A, B, C, R, (float*)ws, M, N, K, K, K, ldc, N, epilogue, {}};
+  hipError_t e = launch_gemm(g, ws ? ws_bytes / 4 : 0, stream);
+  if (e != hipSuccess) return hip_fail(e, "gemm launch");
+  return MX_OK;
+}
+
+MX_EXPORT mx_status mx_profile_enable(int32_t on) {
+  std::lock_guard<std::mutex> g(g_prof.mu);
+  g_prof.on = on != 0;
+  return MX_OK;
+}
+
+MX_EXPORT int32_t mx_profile_read(const char** names, float* total_ms, int32_t* counts,
+                                  int32_t max_entries) {
+  std::lock_guard<std::mutex> g(g_prof.mu);
+  for (auto& r : g_prof.pending) {
+    float ms = 0.f;
+    if (hipEventSynchronize(r.b) == hipSuccess && hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
+      size_t i = 0;
+      while (i < g_prof.names.size() && strcmp(g_prof.names[i], r.name) != 0) i++;
+      if (i == g_prof.names.size()) {
+        g_prof.names.push_back(r.name);
+        g_prof.total_ms.push_back(0.0);
+        g_prof.counts.push_back(0);
+      }
+      g_prof.total_ms[i] += ms;
+      g_prof.counts[i] += 1;
+    }
+    g_prof.free_events.push_back(r.a);
+    g_prof.free_events.push_back(r.b);
+  }
+  g_prof.pending.clear();
+  const int32_t n = (int32_t)std::min<size_t>(g_prof.names.size(), (size_t)std::max(0, max_entries));
+  for (int32_t i = 0; i < n; i++) {
+    if (names) names[i] = g_prof.names[i];
+    if (total_ms) total_ms[i] = (float)g_prof.total_ms[i];
+    if (counts) counts[i] = g_prof.counts[i];
+  }
+  g_prof.names.clear();
+  g_prof.total_ms.clear();
+  g_prof.counts.clear();
+  return n;
+}

@@ -1,0 +1,80 @@
+// mx_device.h -- device-side types and helpers shared by the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mx {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
+typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
+
+#define MX_LDS __attribute__((address_space(3)))
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __uint_as_float(((uint32_t)b) << 16);
+}
+
+// Round-to-nearest-even float -> bf16 bits; NaN stays NaN.
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  return __builtin_bit_cast(uint16_t, (__bf16)f);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+// 16x16x32 bf16 matrix-core product, fp32 accumulate.
+// A: lane l holds row (l % 16), k = 8 * (l / 16) .. +7
+// B: lane l holds col (l % 16), k = 8 * (l / 16) .. +7
+// C: lane l holds col (l % 16), rows 4 * (l / 16) .. +3
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// 32x32x16 bf16 matrix-core product, fp32 accumulate.
+// A: lane l holds row (l % 32), k = 8 * (l / 32) .. +7
+// B: lane l holds col (l % 32), k = 8 * (l / 32) .. +7
+// C: lane l, register 4j + i holds col (l % 32), row 8j + 4 (l / 32) + i
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// Request record uploaded by the host planner.
+struct ReqDev {
+  int32_t tok_start;  // first row of the request in the batch
+  int32_t n_new;
+  int32_t ctx_len;
+  int32_t kv_len;     // ctx_len + n_new
+  int32_t page_start; // offset of the page table in the flat page array
+  int32_t n_pages;    // pages the request actually uses: ceil(kv_len / 16)
+  int32_t phase;
+  int32_t n_split;    // decode: number of key splits (1 = no merge)
+};
+
+// Attention work item (16 bytes).
+//   kind 0 (decode): q heads [head, head + nrows) of the request's single token,
+//                    pages [start, start + split_pages) of its table; part =
+//                    split index (ignored when the request has one split).
+//   kind 1 (prefill): q head `head`, query rows [start, start + 64) of the request.
+struct AttnItem {
+  int32_t req;
+  int16_t head;
+  int8_t kind;
+  int8_t nrows;
+  int32_t start;
+  int32_t part;
+};
+
+struct MergeItem {
+  int32_t req;
+  int32_t part_base;  // partial index of (req, q head 0, split 0)
+};
+
+}  // namespace mx

@@ -1,0 +1,100 @@
+// mx_kernels.h -- launchers of the gfx950 kernels (internal to libmx).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "mx_device.h"
+
+namespace mx {
+
+struct AttnParams {
+  const uint16_t* q;
+  int64_t q_tok_stride;    // elements between consecutive tokens of q
+  const uint16_t* k_pool;
+  const uint16_t* v_pool;
+  uint16_t* out;
+  int64_t out_tok_stride;  // elements between consecutive tokens of out
+  const ReqDev* reqs;
+  const int32_t* pages;
+  const AttnItem* items;
+  float* part_o;           // [parts][head_dim] unnormalised split outputs
+  float* part_ml;          // [parts][2] running max (log2 units) and sum
+  int32_t nq, nkv, group, split_pages;
+  float scale_log2;        // softmax scale * log2(e)
+};
+
+hipError_t launch_paged_attn(const AttnParams& p, int n_items, const MergeItem* merges,
+                             int n_merges, int head_dim, hipStream_t stream);
+
+// Plan kernel: tok_req/tok_pos/tok_slot of every new token from the request
+// table and, when rope_cs is given, the RoPE (cos, sin) table [T][d/2] of the
+// tokens' positions (angle formed and reduced in double precision).
+hipError_t launch_token_map(const ReqDev* reqs, int R, int T, const int32_t* pages,
+                            int32_t* tok_req, int32_t* tok_pos, int64_t* tok_slot,
+                            const double* inv_freq, float2* rope_cs, int half,
+                            hipStream_t stream);
+
+// RMSNorm: out[t] = x[t] / sqrt(mean(x[t]^2) + eps) * g, bf16 in/out, fp32 math.
+hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* g, uint16_t* out, int T, int H,
+                          float eps, hipStream_t stream);
+
+// KV append of given k/v rows [T][nkv][d] into the pools.
+hipError_t launch_kv_append(const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_pool,
+                            uint16_t* v_pool, const int64_t* tok_slot, int T, int nkv, int d,
+                            hipStream_t stream);
+
+// Gather of one request's keys/values (positions 0 .. len-1) into [len][nkv][d].
+hipError_t launch_gather(const uint16_t* k_pool, const uint16_t* v_pool, const int32_t* pages,
+                         int len, int nkv, int d, uint16_t* k_out, uint16_t* v_out,
+                         hipStream_t stream);
+
+// GEMM  C[M][N] = A[M][K] * B[N][K]^T, bf16 in, fp32 accumulate, fused epilogue.
+enum GemmEpilogue : int {
+  EPI_STORE = 0,    // C = acc
+  EPI_RESIDUAL = 1, // C = acc + R   (R [M][N] bf16)
+  EPI_SWIGLU = 2,   // B rows interleaved gate/up in 32-row blocks; C [M][N/2] = silu(gate) * up
+  EPI_QKV = 3,      // QKV projection: RoPE on q/k heads, q -> q_out, k/v -> the paged pools
+};
+
+// Extra operands of the fused QKV epilogue.  The B rows of every q and k head
+// (head_dim 128) are packed so that packed columns 64 g + w and 64 g + 32 + w
+// of the head hold dims 32 g + w and 64 + 32 g + w: the two halves of a RoPE
+// pair land in the same lane of two adjacent 32-column MFMA blocks.
+struct QkvEpilogue {
+  const float2* rope_cs;   // [T][head_dim / 2] (cos, sin)
+  const int64_t* tok_slot; // [T] KV slot of each token
+  uint16_t* q_out;         // [T][nq][head_dim]
+  uint16_t* k_pool;        // [pages][nkv][16][head_dim]
+  uint16_t* v_pool;        // [pages][nkv][head_dim][16]
+  int nq, nkv, head_dim;
+};
+
+struct GemmArgs {
+  const uint16_t* A;
+  const uint16_t* B;
+  uint16_t* C;
+  const uint16_t* R;
+  float* partial;      // split-K scratch [ksplit][M][N] fp32
+  int M, N, K;
+  int lda, ldb, ldc, ldr;
+  int epilogue;
+  QkvEpilogue qkv;
+};
+
+// Chooses a tile shape and split for the problem; ws_floats is the fp32
+// scratch available at args.partial.  A K split never needs more than
+// kMaxSplitFloats of scratch.
+constexpr size_t kMaxSplitFloats = size_t(16) << 20;
+hipError_t launch_gemm(const GemmArgs& args, size_t ws_floats, hipStream_t stream);
+size_t gemm_scratch_floats(int M, int N, int K);
+hipError_t gemm_init();
+
+// Weight packing: row permutation copies for the gate/up interleave and for
+// the RoPE pair layout of the q/k rows of w_qkv.
+hipError_t launch_interleave_gate_up(const uint16_t* src, uint16_t* dst, int F, int H,
+                                     hipStream_t stream);
+hipError_t launch_pack_qkv(const uint16_t* src, uint16_t* dst, int nq, int nkv, int d, int H,
+                           hipStream_t stream);
+
+}  // namespace mx

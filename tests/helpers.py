@@ -1,0 +1,94 @@
+"""Shared test helpers: tolerance metric, batch/shape marshalling, device setup.
+The oracle side and the HIP side never meet here except through the seeded
+inputs of ``workload``."""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+import workload as wl
+
+TOL = 2e-2  # max relative error per row (bf16 compute, fp32 accumulate)
+
+
+def rel_err_rows(got, exp) -> np.ndarray:
+    """Per row: max_j |got - exp| / max_j |exp| (rows = leading axis)."""
+    got = np.asarray(got, np.float64).reshape(len(got), -1)
+    exp = np.asarray(exp, np.float64).reshape(len(exp), -1)
+    num = np.abs(got - exp).max(axis=1)
+    den = np.abs(exp).max(axis=1)
+    return num / np.maximum(den, 1e-30)
+
+
+def assert_rows_close(got, exp, tol=TOL, what=""):
+    got = np.asarray(got, np.float64)
+    assert np.isfinite(got).all(), f"{what}: non-finite values in the GPU result"
+    err = rel_err_rows(got, exp)
+    worst = int(np.argmax(err)) if len(err) else 0
+    assert len(err) == 0 or err.max() <= tol, \
+        f"{what}: max per-row relative error {err.max():.3e} (row {worst}) > {tol}"
+    return float(err.max()) if len(err) else 0.0
+
+
+def mx_batch(mx, b: wl.Batch):
+    return mx.Batch(b.phase, b.n_new, b.ctx_len, b.page_tables)
+
+
+def mx_shape(mx, cfg: wl.LayerConfig, pool_pages: int):
+    return mx.attn_shape(cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, pool_pages)
+
+
+def mx_cfg(mx, cfg: wl.LayerConfig, pool_pages: int):
+    return mx.layer_cfg(cfg.hidden, cfg.ffn, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim,
+                        pool_pages, cfg.rms_eps, cfg.rope_theta)
+
+
+def dev(bits, device="cuda"):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(bits, dtype=np.uint16)).to(device)
+
+
+def host_bits(t) -> np.ndarray:
+    return t.cpu().numpy().view(np.uint16)
+
+
+def bits_to_f64(t) -> np.ndarray:
+    return wl.bf16_bits_to_f64(host_bits(t))
+
+
+def sample_rows(b: wl.Batch, rng, n_decode=16, n_prefill_random=62):
+    """All decode rows of n_decode random decode requests, plus the first, the
+    last and n_prefill_random random rows of every prefill chunk."""
+    start = np.concatenate([[0], np.cumsum(b.n_new)])
+    dec = [r for r in range(b.R) if b.phase[r] == wl.DECODE]
+    rows = [int(start[r]) for r in rng.choice(dec, size=min(n_decode, len(dec)), replace=False)]
+    for r in range(b.R):
+        if b.phase[r] != wl.PREFILL:
+            continue
+        n = int(b.n_new[r])
+        pick = {0, n - 1}
+        pick.update(rng.choice(n, size=min(n_prefill_random, n), replace=False).tolist())
+        rows += [int(start[r]) + i for i in sorted(pick)]
+    return np.array(sorted(set(rows)), np.int64)
+
+
+def truncated_subbatch(b: wl.Batch, rows):
+    """The requests that own the sampled rows, each cut after its last sampled
+    row (later tokens cannot influence earlier rows: attention is causal).
+    Returns (sub_batch, request ids, row indices inside the sub-batch, token
+    indices in the full batch of the sub-batch's tokens)."""
+    start = np.concatenate([[0], np.cumsum(b.n_new)])
+    req_of = np.searchsorted(start, rows, side="right") - 1
+    reqs = sorted(set(req_of.tolist()))
+    n_new, tok_idx, sub_rows, off = [], [], [], 0
+    for r in reqs:
+        last = int(max(rows[req_of == r])) - int(start[r])
+        n_new.append(last + 1)
+        tok_idx += list(range(int(start[r]), int(start[r]) + last + 1))
+        for t in rows[req_of == r]:
+            sub_rows.append(off + int(t) - int(start[r]))
+        off += last + 1
+    sub = b.subset(reqs)
+    sub.n_new = np.array(n_new, np.int32)
+    return sub, reqs, np.array(sub_rows, np.int64), np.array(tok_idx, np.int64)

@@ -1,0 +1,440 @@
+"""GPU parity of the HIP path (through the C ABI) against the fp64 oracle on the
+same seeded inputs.  Integer/byte work is compared bit for bit; floating point
+per row with max relative error 2e-2 (bf16 compute, fp32 accumulate).
+
+Unused pool slots (pages no request owns, and slots at or beyond each request's
+cached length before the step) are filled with bf16 NaN, so any read of a slot
+outside a request's keys poisons the result and fails the finiteness check."""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workload as wl
+from helpers import (TOL, assert_rows_close, bits_to_f64, dev, host_bits, mx_batch, mx_cfg,
+                     mx_shape, rel_err_rows, sample_rows, truncated_subbatch)
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+import paper_2606_16264_amd as mx  # noqa: E402
+import workload.device as wdev      # noqa: E402
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def ws_tensor(nbytes):
+    return torch.empty(int(nbytes), dtype=torch.uint8, device="cuda")
+
+
+def sync():
+    torch.cuda.synchronize()
+
+
+# ----------------------------------------------------------------------- generator
+def test_device_pool_fill_matches_host():
+    cfg = wl.CONFIGS["c1"]
+    b = wl.make_batch("c1")
+    say("case: device pool fill c1")
+    k, v = wdev.alloc_pools(cfg, b.pool_pages)
+    wdev.fill_pools(k, v, cfg, b, 1000, poison=True)
+    sync()
+    hk, hv = wl.host_pool(cfg, b, 1000, poison=True)
+    np.testing.assert_array_equal(host_bits(k), hk)
+    np.testing.assert_array_equal(wdev.v_pool_canonical(v), hv)
+
+
+# ----------------------------------------------------------------------- token map
+TOKEN_MAP_CASES = [("c1", 128), ("c2", 512), ("c3", 4096), ("c4", 2048), ("c5", 8192)]
+
+
+@pytest.mark.parametrize("key,P", TOKEN_MAP_CASES)
+def test_token_map_bit_exact(key, P):
+    say(f"case: token map {key} P={P}")
+    cfg = wl.CONFIGS[key]
+    b = wl.make_batch(key, P)
+    mb = mx_batch(mx, b)
+    shape = mx_shape(mx, cfg, b.pool_pages)
+    ws = ws_tensor(mx.mx_workspace_bytes_for(mb, shape=shape))
+    T = b.T
+    tr = torch.empty(T, dtype=torch.int32, device="cuda")
+    tp = torch.empty(T, dtype=torch.int32, device="cuda")
+    ts = torch.empty(T, dtype=torch.int64, device="cuda")
+    mx.mx_debug_token_map(mb, shape, tr, tp, ts, ws)
+    sync()
+    ref = oracle.token_map(b.n_new, b.ctx_len, b.page_tables, 16)
+    np.testing.assert_array_equal(tr.cpu().numpy(), ref.tok_req)
+    np.testing.assert_array_equal(tp.cpu().numpy(), ref.tok_pos)
+    np.testing.assert_array_equal(ts.cpu().numpy(), ref.tok_slot)
+
+
+def boundary_batch(rng, pool=None):
+    """Decodes at and around page boundaries, prefills with and without a cached prefix."""
+    return wl.custom_batch(rng, [1, 15, 16, 17, 31, 32, 33, 100, 255, 256, 1000],
+                           [(1, 0), (7, 0), (16, 0), (64, 0), (65, 0), (130, 0), (50, 17),
+                            (33, 48), (16, 16)], pool_pages=pool)
+
+
+# ----------------------------------------------------------------------- KV append / gather
+@pytest.mark.parametrize("nkv,d", [(4, 64), (8, 128), (2, 128)])
+def test_kv_append_bit_exact(nkv, d):
+    say(f"case: kv append nkv={nkv} d={d}")
+    rng = np.random.default_rng(20 + nkv + d)
+    cfg = wl.LayerConfig("t", 256, 256, nkv, nkv, d)
+    b = boundary_batch(rng)
+    k, v = wdev.alloc_pools(cfg, b.pool_pages)
+    wdev.fill_pools(k, v, cfg, b, 7, poison=True)
+    sync()
+    k0, v0 = host_bits(k).copy(), wdev.v_pool_canonical(v)
+    kn = rng.integers(0, 65536, (b.T, nkv, d), dtype=np.uint16)
+    vn = rng.integers(0, 65536, (b.T, nkv, d), dtype=np.uint16)
+    mb = mx_batch(mx, b)
+    shape = mx_shape(mx, cfg, b.pool_pages)
+    ws = ws_tensor(mx.mx_workspace_bytes_for(mb, shape=shape))
+    mx.mx_kv_append(mb, shape, dev(kn), dev(vn), k, v, ws)
+    sync()
+    ek, ev = oracle.kv_append(b.n_new, b.ctx_len, b.page_tables, kn, vn, k0, v0)
+    np.testing.assert_array_equal(host_bits(k), ek)
+    np.testing.assert_array_equal(wdev.v_pool_canonical(v), ev)
+
+
+def test_gather_bit_exact():
+    say("case: gather")
+    rng = np.random.default_rng(31)
+    cfg = wl.LayerConfig("t", 256, 256, 4, 4, 128)
+    b = boundary_batch(rng)
+    k, v = wdev.alloc_pools(cfg, b.pool_pages)
+    wdev.fill_pools(k, v, cfg, b, 9, poison=False)
+    sync()
+    mb = mx_batch(mx, b)
+    shape = mx_shape(mx, cfg, b.pool_pages)
+    ws = ws_tensor(mx.mx_workspace_bytes_for(mb, shape=shape))
+    hk, hv = wl.host_pool(cfg, b, 9, poison=False)
+    for r in (0, 3, 10, 13, 17, 19):
+        L = int(b.kv_len[r])
+        ko = torch.empty((L, 4, 128), dtype=torch.uint16, device="cuda")
+        vo = torch.empty((L, 4, 128), dtype=torch.uint16, device="cuda")
+        mx.mx_debug_gather(mb, shape, r, k, v, ko, vo, ws)
+        sync()
+        j = np.arange(L)
+        pg = b.page_tables[r][j // 16]
+        np.testing.assert_array_equal(host_bits(ko), hk[pg, :, j % 16])
+        np.testing.assert_array_equal(host_bits(vo), hv[pg, :, j % 16])
+
+
+# ----------------------------------------------------------------------- attention
+def attention_case(cfg, b, seed, rng, needle=False):
+    """Pools filled (NaN-poisoned), new K/V appended through the ABI, random q.
+    Returns device tensors and the oracle's expected output."""
+    k, v = wdev.alloc_pools(cfg, b.pool_pages)
+    wdev.fill_pools(k, v, cfg, b, seed, poison=True)
+    nq, nkv, d = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    kn = wl.f32_to_bf16_bits(rng.uniform(-math.sqrt(3), math.sqrt(3), (b.T, nkv, d)))
+    vn = wl.f32_to_bf16_bits(rng.uniform(-math.sqrt(3), math.sqrt(3), (b.T, nkv, d)))
+    qf = rng.standard_normal((b.T, nq, d)).astype(np.float32)
+    kp, vp = wl.prior_kv_concat(cfg, b, seed)
+    if needle:
+        # per request: the key of one cached position is set to 20x the first
+        # q head's direction (scaled by sqrt(d)), so the softmax is dominated by it
+        start = np.concatenate([[0], np.cumsum(b.n_new)])
+        pstart = np.concatenate([[0], np.cumsum(b.ctx_len)])
+        for r in range(b.R):
+            if b.ctx_len[r] == 0:
+                continue
+            j = int(rng.integers(0, int(b.ctx_len[r])))
+            t = int(start[r])
+            for g in range(nkv):
+                h0 = g * (nq // nkv)
+                qd = qf[t:t + int(b.n_new[r]), h0].mean(axis=0)
+                qf[t:t + int(b.n_new[r]), g * (nq // nkv):(g + 1) * (nq // nkv)] = qd
+                kp[pstart[r] + j, g] = wl.f32_to_bf16_bits(20.0 * qd / np.linalg.norm(qd) * math.sqrt(d) / 4)
+        # write the needle keys into the device pool
+        kh = host_bits(k).copy()
+        for r in range(b.R):
+            for j in range(int(b.ctx_len[r])):
+                page = b.page_tables[r][j // 16]
+                kh[page, :, j % 16] = kp[pstart[r] + j]
+        k.copy_(torch.from_numpy(kh).cuda())
+    q = wl.f32_to_bf16_bits(qf)
+    mb = mx_batch(mx, b)
+    shape = mx_shape(mx, cfg, b.pool_pages)
+    ws = ws_tensor(mx.mx_workspace_bytes_for(mb, shape=shape))
+    mx.mx_kv_append(mb, shape, dev(kn), dev(vn), k, v, ws)
+    # oracle inputs: cached prefix then the new tokens, per request
+    ks, vs, t0, p0 = [], [], 0, 0
+    for r in range(b.R):
+        c, n = int(b.ctx_len[r]), int(b.n_new[r])
+        ks += [kp[p0:p0 + c], kn[t0:t0 + n]]
+        vs += [vp[p0:p0 + c], vn[t0:t0 + n]]
+        t0 += n
+        p0 += c
+    kc = wl.bf16_bits_to_f64(np.concatenate(ks))
+    vc = wl.bf16_bits_to_f64(np.concatenate(vs))
+    off = np.concatenate([[0], np.cumsum(b.kv_len)])[:-1]
+    exp = oracle.attention_contig(b.n_new, b.ctx_len, wl.bf16_bits_to_f64(q), kc, vc, off,
+                                  cfg.scale)
+    return dict(k=k, v=v, q=dev(q), mb=mb, shape=shape, ws=ws, exp=exp, vc=vc, off=off)
+
+
+ATTN_SHAPES = [(4, 4, 64), (8, 8, 128), (32, 8, 128), (16, 2, 128), (32, 1, 64), (64, 8, 128)]
+
+
+@pytest.mark.parametrize("nq,nkv,d", ATTN_SHAPES)
+def test_paged_attn_boundaries(nq, nkv, d):
+    say(f"case: paged attn boundaries nq={nq} nkv={nkv} d={d}")
+    rng = np.random.default_rng(100 + nq + nkv + d)
+    cfg = wl.LayerConfig("t", 256, 256, nq, nkv, d)
+    b = boundary_batch(rng)
+    c = attention_case(cfg, b, 11, rng)
+    out = torch.empty((b.T, nq, d), dtype=torch.uint16, device="cuda")
+    mx.mx_paged_attn(c["mb"], c["shape"], c["q"], c["k"], c["v"], out, c["ws"])
+    sync()
+    err = assert_rows_close(bits_to_f64(out).reshape(b.T * nq, d), c["exp"].reshape(b.T * nq, d),
+                            what="attention")
+    say(f"  max row rel err {err:.2e}")
+
+
+@pytest.mark.parametrize("key", ["c2", "c4"])
+def test_paged_attn_long_contexts_split(key):
+    """Long decode contexts (several key splits and the merge) at a real shape."""
+    say(f"case: paged attn long contexts {key}")
+    rng = np.random.default_rng(5)
+    cfg = wl.CONFIGS[key]
+    b = wl.custom_batch(rng, [3000, 8191, 16384, 777, 4096, 2048, 16, 5000],
+                        [(300, 0), (128, 900)])
+    c = attention_case(cfg, b, 12, rng)
+    out = torch.empty((b.T, cfg.n_q_heads, cfg.head_dim), dtype=torch.uint16, device="cuda")
+    mx.mx_paged_attn(c["mb"], c["shape"], c["q"], c["k"], c["v"], out, c["ws"])
+    sync()
+    n = cfg.n_q_heads
+    assert_rows_close(bits_to_f64(out).reshape(-1, cfg.head_dim),
+                      c["exp"].reshape(-1, cfg.head_dim), what="attention")
+    # deterministic: a second launch is bit-identical
+    out2 = torch.empty_like(out)
+    mx.mx_paged_attn(c["mb"], c["shape"], c["q"], c["k"], c["v"], out2, c["ws"])
+    sync()
+    assert torch.equal(out, out2)
+
+
+def test_paged_attn_needle():
+    say("case: paged attn needle")
+    rng = np.random.default_rng(6)
+    cfg = wl.LayerConfig("t", 256, 256, 8, 2, 128)
+    b = wl.custom_batch(rng, [40, 300, 1000, 33], [(20, 70)])
+    c = attention_case(cfg, b, 13, rng, needle=True)
+    out = torch.empty((b.T, 8, 128), dtype=torch.uint16, device="cuda")
+    mx.mx_paged_attn(c["mb"], c["shape"], c["q"], c["k"], c["v"], out, c["ws"])
+    sync()
+    assert_rows_close(bits_to_f64(out).reshape(-1, 128), c["exp"].reshape(-1, 128),
+                      what="attention (needle)")
+
+
+# ----------------------------------------------------------------------- GEMM
+@pytest.mark.parametrize("M,N,K,epi", [
+    (1, 768, 256, 0), (64, 12288, 4096, 0), (132, 1024, 256, 1), (576, 4096, 4096, 1),
+    (577, 2048, 512, 2), (1000, 22016, 4096, 2), (2304, 6144, 4096, 0), (256, 4096, 11008, 1),
+    (8, 256, 1024, 2),
+])
+def test_gemm_matches_oracle(M, N, K, epi):
+    say(f"case: gemm M={M} N={N} K={K} epi={epi}")
+    rng = np.random.default_rng(M + N + K + epi)
+    a = wl.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
+    w = wl.f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * 0.02)
+    r = wl.f32_to_bf16_bits(rng.standard_normal((M, N), dtype=np.float32))
+    ncol = N // 2 if epi == 2 else N
+    C = torch.empty((M, ncol), dtype=torch.uint16, device="cuda")
+    ws = ws_tensor(max(mx.mx_debug_gemm_ws_bytes(M, N, K), 256))
+    mx.mx_debug_gemm(dev(a), dev(w), C, dev(r) if epi == 1 else None, epi, ws)
+    sync()
+    # sampled rows keep the fp64 reference cheap at the large shapes
+    rows = np.unique(np.concatenate([[0, M - 1], rng.integers(0, M, size=min(M, 48))]))
+    acc = oracle.linear(wl.bf16_bits_to_f64(a[rows]), w)
+    if epi == 1:
+        exp = acc + wl.bf16_bits_to_f64(r[rows])
+    elif epi == 2:
+        # packed rows: 32-row blocks alternate gate and up of the same features
+        blocks = acc.reshape(len(rows), N // 64, 2, 32)
+        exp = oracle.silu_mul(np.concatenate([blocks[:, :, 0].reshape(len(rows), -1),
+                                              blocks[:, :, 1].reshape(len(rows), -1)], axis=1))
+    else:
+        exp = acc
+    assert_rows_close(bits_to_f64(C)[rows], exp, what="gemm")
+
+
+# ----------------------------------------------------------------------- layer step
+def pack_layer(cfg, b, w):
+    c = mx_cfg(mx, cfg, b.pool_pages)
+    packed = torch.empty(mx.mx_packed_weights_bytes(c), dtype=torch.uint8, device="cuda")
+    dw = {k: dev(v) for k, v in w.items()}
+    mx.mx_pack_weights(c, dw, packed)
+    sync()
+    return c, packed
+
+
+def run_layer(cfg, b, w, x, seed, reps=1):
+    c, packed = pack_layer(cfg, b, w)
+    k, v = wdev.alloc_pools(cfg, b.pool_pages)
+    wdev.fill_pools(k, v, cfg, b, seed, poison=True)
+    mb = mx_batch(mx, b)
+    ws = ws_tensor(mx.mx_workspace_bytes_for(mb, cfg=c))
+    xd = dev(x)
+    y = torch.empty_like(xd)
+    for _ in range(reps):
+        mx.mx_layer_step(mb, c, packed, xd, y, k, v, ws)
+    sync()
+    off = mx.mx_layer_workspace_offsets(mb, c)
+    T, H, F = b.T, cfg.hidden, cfg.ffn
+    nqd = cfg.n_q_heads * cfg.head_dim
+
+    def view(name, cols):
+        o = off[name]
+        return ws[o:o + T * cols * 2].view(torch.uint16).reshape(T, cols)
+
+    return dict(y=y, k=k, v=v, q=view("q", nqd), o=view("o", nqd), x1=view("x1", H),
+                a=view("a", F), h2=view("h", H))
+
+
+def staged_attention(cfg, sub, x_sub, w, kp, vp, sub_rows):
+    """Attention output of the evaluated rows from an oracle pipeline that
+    stores each stage boundary in bf16 exactly where the HIP path does
+    (RMSNorm output h; post-RoPE q and k; v), with every step computed by the
+    pinned oracle functions (rmsnorm, linear, rope, attention) in fp64.  This
+    isolates the attention kernel's own arithmetic (bf16 probabilities, fp32
+    accumulation) from the bf16 storage of its inputs, which attention can
+    amplify for short, sharply peaked contexts.  Oracle values only."""
+    rnd = lambda a: wl.bf16_bits_to_f64(wl.f32_to_bf16_bits(np.asarray(a, np.float32)))
+    H, nq, nkv, d = cfg.hidden, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    start = np.concatenate([[0], np.cumsum(sub.n_new)])
+    pstart = np.concatenate([[0], np.cumsum(sub.ctx_len)])
+    pos_all = np.concatenate([np.arange(c, c + n) for n, c in zip(sub.n_new, sub.ctx_len)])
+    h = rnd(oracle.rmsnorm(wl.bf16_bits_to_f64(x_sub), wl.bf16_bits_to_f64(w["g1"]), cfg.rms_eps))
+    k = oracle.linear(h, w["w_qkv"][nq * d:(nq + nkv) * d]).reshape(-1, nkv, d)
+    v = oracle.linear(h, w["w_qkv"][(nq + nkv) * d:]).reshape(-1, nkv, d)
+    k = rnd(oracle.rope(k, pos_all, cfg.rope_theta))
+    v = rnd(v)
+    q = oracle.linear(h[sub_rows], w["w_qkv"][:nq * d]).reshape(-1, nq, d)
+    q = rnd(oracle.rope(q, pos_all[sub_rows], cfg.rope_theta))
+    ks, vs = [], []
+    for r in range(sub.R):
+        c, n = int(sub.ctx_len[r]), int(sub.n_new[r])
+        ks += [wl.bf16_bits_to_f64(kp[pstart[r]:pstart[r] + c]), k[start[r]:start[r] + n]]
+        vs += [wl.bf16_bits_to_f64(vp[pstart[r]:pstart[r] + c]), v[start[r]:start[r] + n]]
+    kc, vc = np.concatenate(ks), np.concatenate(vs)
+    koff = np.concatenate([[0], np.cumsum(sub.ctx_len + sub.n_new)])
+    req_of = np.searchsorted(start, sub_rows, side="right") - 1
+    return oracle.attention_contig(np.ones(len(sub_rows), np.int32),
+                                   pos_all[sub_rows].astype(np.int32), q, kc, vc, koff[req_of],
+                                   cfg.scale)
+
+
+def check_layer(cfg, b, got, exp, rows_gpu, what, o_ref=None):
+    """Stage-by-stage comparison of the GPU iteration with the oracle on the
+    evaluated rows.  Every stage is measured; the layer output y, the branch
+    sum y - x, the projections and the SwiGLU output are gated at 2e-2 against
+    the exact oracle; the attention output is gated at 2e-2 against the
+    stage-emulating oracle pipeline (o_ref, see staged_attention), and its
+    error against the exact oracle is reported."""
+    d = cfg.head_dim
+    g = lambda name: bits_to_f64(got[name])[rows_gpu]
+    errs = {
+        "q": rel_err_rows(g("q").reshape(-1, d), exp.q.reshape(-1, d)).max(),
+        "o_vs_exact": rel_err_rows(g("o").reshape(-1, d), exp.o.reshape(-1, d)).max(),
+        "x1": rel_err_rows(g("x1"), exp.x1).max(),
+        "h2": rel_err_rows(g("h2"), exp.h2).max(),
+        "a": rel_err_rows(g("a"), exp.a).max(),
+        "y": rel_err_rows(g("y"), exp.y).max(),
+    }
+    if o_ref is not None:
+        errs["o"] = rel_err_rows(g("o").reshape(-1, d), o_ref.reshape(-1, d)).max()
+    say(f"  {what} stage errors: " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+    for name in ("q", "x1", "h2", "a", "y"):
+        assert_rows_close(g(name).reshape(len(rows_gpu), -1), getattr(exp, name).reshape(len(rows_gpu), -1),
+                          what=f"{what} {name}")
+    if o_ref is not None:
+        assert_rows_close(g("o").reshape(-1, d), o_ref.reshape(-1, d), what=f"{what} attention o")
+    return errs
+
+
+def check_pool_rows(cfg, b, got, exp_k, exp_v, tok_idx):
+    """New keys/values at their slots (tolerance) for the given tokens."""
+    tm = oracle.token_map(b.n_new, b.ctx_len, b.page_tables, 16)
+    slots = tm.tok_slot[tok_idx]
+    pg = torch.from_numpy(slots // 16).cuda()
+    sl = torch.from_numpy(slots % 16).cuda()
+    # uint16 tensors cannot be gathered on the device; gather their int16 view
+    kk = got["k"].view(torch.int16)[pg, :, sl].view(torch.uint16)
+    vv = got["v"].view(torch.int16)[pg, :, :, sl].view(torch.uint16)
+    assert_rows_close(bits_to_f64(kk).reshape(-1, cfg.head_dim),
+                      exp_k.reshape(-1, cfg.head_dim), what="appended k")
+    assert_rows_close(bits_to_f64(vv).reshape(-1, cfg.head_dim),
+                      exp_v.reshape(-1, cfg.head_dim), what="appended v")
+
+
+def test_layer_step_c1_full():
+    say("case: layer step c1 (all rows)")
+    cfg = wl.CONFIGS["c1"]
+    b = wl.make_batch("c1")
+    w = wl.make_weights(cfg, "c1")
+    x = wl.make_x(cfg, b.T, "c1")
+    got = run_layer(cfg, b, w, x, wl.kv_seed("c1"), reps=2)
+    kp, vp = wl.prior_kv_concat(cfg, b, wl.kv_seed("c1"))
+    exp = oracle.layer_step(cfg.as_dict(), b.n_new, b.ctx_len, x, w, kp, vp)
+    rows = np.arange(b.T)
+    o_ref = staged_attention(cfg, b, x, w, kp, vp, rows)
+    errs = check_layer(cfg, b, got, exp, rows, "c1", o_ref)
+    check_pool_rows(cfg, b, got, exp.k_new, exp.v_new, rows)
+    say("  errors", {k: f"{v:.2e}" for k, v in errs.items()})
+
+
+SMALL_GQA = wl.LayerConfig("small-gqa", 512, 1408, 8, 2, 128, rope_theta=5e5)
+
+
+def test_layer_step_small_gqa_full():
+    say("case: layer step small GQA (all rows)")
+    cfg = SMALL_GQA
+    rng = np.random.default_rng(77)
+    b = wl.custom_batch(rng, [1, 16, 33, 500, 1500, 64, 17], [(200, 0), (70, 33), (1, 0)])
+    ws = {k: wl.f32_to_bf16_bits(rng.standard_normal(s, dtype=np.float32) * 0.02) for k, s in (
+        ("w_qkv", (cfg.qkv_rows, cfg.hidden)), ("w_o", (cfg.hidden, 1024)),
+        ("w_gu", (2 * cfg.ffn, cfg.hidden)), ("w_down", (cfg.hidden, cfg.ffn)))}
+    ws["g1"] = wl.f32_to_bf16_bits(1 + 0.1 * rng.standard_normal(cfg.hidden, dtype=np.float32))
+    ws["g2"] = wl.f32_to_bf16_bits(1 + 0.1 * rng.standard_normal(cfg.hidden, dtype=np.float32))
+    x = wl.f32_to_bf16_bits(rng.standard_normal((b.T, cfg.hidden), dtype=np.float32))
+    got = run_layer(cfg, b, ws, x, 4242)
+    kp, vp = wl.prior_kv_concat(cfg, b, 4242)
+    exp = oracle.layer_step(cfg.as_dict(), b.n_new, b.ctx_len, x, ws, kp, vp)
+    rows = np.arange(b.T)
+    check_layer(cfg, b, got, exp, rows, "small-gqa", staged_attention(cfg, b, x, ws, kp, vp, rows))
+    check_pool_rows(cfg, b, got, exp.k_new, exp.v_new, rows)
+
+
+@pytest.mark.parametrize("key,P", [("c2", 512), ("c2", 0), ("c3", 1024), ("c4", 2048)])
+def test_layer_step_sampled(key, P):
+    """Full-size layer iteration (the benchmark's launch configuration),
+    checked on sampled rows: the oracle evaluates the requests that own them,
+    cut after their last sampled row."""
+    say(f"case: layer step {key} P={P} (sampled rows)")
+    cfg = wl.CONFIGS[key]
+    b = wl.make_batch(key, P)
+    w = wl.make_weights(cfg, key)
+    x = wl.make_x(cfg, b.T, key)
+    seed = wl.kv_seed(key)
+    got = run_layer(cfg, b, w, x, seed)
+    rng = np.random.default_rng(3)
+    rows = sample_rows(b, rng, n_decode=16, n_prefill_random=30)
+    sub, reqs, sub_rows, tok_idx = truncated_subbatch(b, rows)
+    kp, vp = wl.prior_kv_concat(cfg, sub, seed)
+    exp = oracle.layer_step(cfg.as_dict(), sub.n_new, sub.ctx_len, x[tok_idx], w, kp, vp,
+                            rows=sub_rows)
+    o_ref = staged_attention(cfg, sub, x[tok_idx], w, kp, vp, sub_rows)
+    errs = check_layer(cfg, b, got, exp, rows, key, o_ref)
+    check_pool_rows(cfg, b, got, exp.k_new, exp.v_new, tok_idx)
+    say("  errors", {k: f"{v:.2e}" for k, v in errs.items()})
