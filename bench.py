@@ -37,7 +37,7 @@ def parse():
     ap.add_argument("--prefill", type=int, nargs="*", default=None,
                     help="mixed prefill tokens per point (default: the shape's sweep)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--kernels", action="store_true", default=True)
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB before timing (the "
