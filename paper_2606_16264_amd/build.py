@@ -46,6 +46,16 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+def device_asm(src: str, out: str) -> str:
+    """gfx950 assembly of one library source, compiled with the library's flags."""
+    cmd = [HIPCC] + FLAGS + ["-x", "hip", "--cuda-device-only", "-S",
+                             os.path.join(CSRC, src), "-o", out]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"hipcc -S failed on {src}:\n{res.stderr}")
+    return out
+
+
 def build_workload_gen(verbose: bool = False) -> str:
     """The device-side input generator (workload/libmxgen.so)."""
     src = os.path.join(ROOT, "workload", "csrc", "mxgen.hip")

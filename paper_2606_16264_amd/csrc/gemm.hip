@@ -5,12 +5,13 @@
 // Design:
 //  - workgroup tile BM x BN, K step 64; waves of 64 lanes each own a WM x WN
 //    sub-tile computed with v_mfma_f32_32x32x16_bf16;
-//  - the next K slice is fetched global -> registers while the matrix cores
-//    work on the current one, then written to the other half of a double-
-//    buffered LDS stage (one barrier per 64-wide K slice);
-//  - fragment reads of k-step ks+1 are issued before the MFMAs of k-step ks;
-//  - LDS rows are 128 bytes (64 bf16 of K); the 16-byte chunk c of row r is
-//    stored at position c ^ (r & 7), which makes the fragment reads of 8
+//  - K is consumed in 32-wide slices through a 4-deep LDS ring filled by the
+//    DMA path (global_load_lds): three slices are in flight while the matrix
+//    cores work on the fourth, and no registers are spent on staging;
+//  - fragment reads of the next k-step are issued before the MFMAs of the
+//    current one; one barrier per slice;
+//  - LDS rows are 64 bytes (32 bf16 of K); the 16-byte chunk c of row r is
+//    stored at c ^ ((r >> 1) & 3), which makes the fragment reads of 8
 //    consecutive rows hit 8 distinct bank groups;
 //  - tile order is XCD-aware: workgroup b runs on XCD b % 8, and each XCD is
 //    handed a contiguous run of tiles taken in M-grouped order, so that the
@@ -27,8 +28,42 @@ namespace mx {
 
 namespace {
 
-constexpr int BK = 64;
+constexpr int BK = 64;    // K granularity of a split (and of the problem)
+constexpr int BKS = 32;   // K per LDS stage
+constexpr int NS = 4;     // LDS ring depth: NS - 1 stages in flight
 constexpr int kGroupM = 8;
+
+// LDS ring discipline.  The K slices are copied global -> LDS by the DMA path
+// (global_load_lds, 16 bytes per lane), which the hardware tracks with vmcnt
+// only, and the MFMA fragments are read with ds_read_b128 issued from inline
+// assembly, so that every wait is placed here by hand rather than inferred
+// (the compiler would otherwise wait for all DMA in flight before any LDS
+// read).  pin() ties fragment registers to the preceding wait so that no
+// consumer is scheduled above it.
+template <int N>
+__device__ __forceinline__ void lgkm_wait() {
+  static_assert(N >= 0 && N <= 15, "lgkmcnt range");
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"i"(N) : "memory");
+}
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"i"(N) : "memory");
+}
+__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
+template <int K>
+__device__ __forceinline__ void pin(u32x4 (&f)[K]) {
+#pragma unroll
+  for (int i = 0; i < K; i++) asm volatile("" : "+v"(f[i]));
+}
+__device__ __forceinline__ u32x4 lds_read16(unsigned addr) {
+  u32x4 v;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr));
+  return v;
+}
+__device__ __forceinline__ void dma16(const void* g, unsigned lds_addr) {
+  __builtin_amdgcn_global_load_lds(g, (MX_LDS void*)(size_t)lds_addr, 16, 0, 0);
+}
 
 __device__ __forceinline__ void tile_coords(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
   const int nt = tiles_m * tiles_n;
@@ -84,10 +119,16 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   constexpr int WAVES_N = BN / WN;
   constexpr int NWAVES = (BM / WM) * WAVES_N;
   constexpr int MB = WM / 32, NB = WN / 32;
-  constexpr int STAGE = (BM + BN) * 128;  // bytes per LDS stage
+  constexpr int ROWB = BKS * 2;                // bytes of one tile row in a stage (64)
+  constexpr int STAGE = (BM + BN) * ROWB;      // bytes per LDS stage
+  constexpr int L = STAGE / 1024 / NWAVES;     // DMA instructions per wave per stage
+  static_assert(L * NWAVES * 1024 == STAGE, "stage does not split into whole DMA rows");
+  constexpr int VM_KEEP = (NS - 2) * L;        // in flight after the oldest stage landed
+  constexpr int NREAD = MB + NB;               // fragment reads per k-step
   static_assert((EPI != EPI_SWIGLU && EPI != EPI_QKV) || NB % 2 == 0,
                 "SwiGLU and the QKV epilogue need pairs of 32-column blocks");
   extern __shared__ __attribute__((aligned(16))) char smem[];
+  const unsigned sbase = (unsigned)(size_t)(MX_LDS char*)smem;
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -97,44 +138,25 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   const int m0 = tm * BM, n0 = tn * BN;
   const int kz = blockIdx.y;
   const int kbeg = kz * k_per_split;
-  const int nk = k_per_split / BK;
+  const int nk = k_per_split / BKS;
 
-  // Global -> register -> LDS staging.  Each thread owns NA + NB_ 16-byte
-  // chunks of the stage: chunk q of the A tile is row (q * 256 + tid) / 8,
-  // logical 16-byte column (tid % 8), stored at column (tid % 8) ^ (row % 8).
-  constexpr int NTHREADS = NWAVES * 64;
-  constexpr int NA = BM * 8 / NTHREADS, NBC = BN * 8 / NTHREADS;
-  static_assert(NA * NTHREADS == BM * 8 && NBC * NTHREADS == BN * 8, "tile/thread mismatch");
-  const int tid = threadIdx.x;
-  const int lcol = tid & 7;
-  const uint16_t* a_src[NA];
-  const uint16_t* b_src[NBC];
-  int a_dst[NA], b_dst[NBC];
+  // DMA: instruction j (wave w issues j = w L .. w L + L - 1) fills rows
+  // 16 j .. 16 j + 15 of the stacked A|B tile; lane l lands at row 16 j + l / 4,
+  // stored chunk l % 4, which holds logical chunk (l % 4) ^ ((row >> 1) & 3).
+  // That XOR makes the fragment reads of 8 consecutive rows conflict-free.
+  const uint16_t* src[L];
 #pragma unroll
-  for (int q = 0; q < NA; q++) {
-    const int row = (q * NTHREADS + tid) >> 3;
-    a_src[q] = a.A + (int64_t)min(m0 + row, a.M - 1) * a.lda + kbeg + lcol * 8;
-    a_dst[q] = row * 128 + ((lcol ^ (row & 7)) << 4);
+  for (int i = 0; i < L; i++) {
+    const int row = (wave * L + i) * 16 + (lane >> 2);
+    const int c = (lane & 3) ^ ((row >> 1) & 3);
+    src[i] = (row < BM) ? a.A + (int64_t)min(m0 + row, a.M - 1) * a.lda + kbeg + c * 8
+                        : a.B + (int64_t)min(n0 + row - BM, a.N - 1) * a.ldb + kbeg + c * 8;
   }
+  auto issue = [&](int st) {
+    const int kk = min(st, nk - 1);  // past the end: re-fetch the last slice (never read)
+    const unsigned slot = sbase + (unsigned)((st % NS) * STAGE);
 #pragma unroll
-  for (int q = 0; q < NBC; q++) {
-    const int row = (q * NTHREADS + tid) >> 3;
-    b_src[q] = a.B + (int64_t)min(n0 + row, a.N - 1) * a.ldb + kbeg + lcol * 8;
-    b_dst[q] = BM * 128 + row * 128 + ((lcol ^ (row & 7)) << 4);
-  }
-  u32x4 ra[NA], rb[NBC];
-  auto gload = [&](int kt) {
-#pragma unroll
-    for (int q = 0; q < NA; q++) ra[q] = *reinterpret_cast<const u32x4*>(a_src[q] + kt * BK);
-#pragma unroll
-    for (int q = 0; q < NBC; q++) rb[q] = *reinterpret_cast<const u32x4*>(b_src[q] + kt * BK);
-  };
-  auto lstore = [&](int stage) {
-    char* base = smem + stage * STAGE;
-#pragma unroll
-    for (int q = 0; q < NA; q++) *reinterpret_cast<u32x4*>(base + a_dst[q]) = ra[q];
-#pragma unroll
-    for (int q = 0; q < NBC; q++) *reinterpret_cast<u32x4*>(base + b_dst[q]) = rb[q];
+    for (int i = 0; i < L; i++) dma16(src[i] + kk * BKS, slot + (wave * L + i) * 1024);
   };
 
   f32x16 acc[MB][NB];
@@ -146,51 +168,72 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
       for (int r = 0; r < 16; r++) acc[i][j][r] = 0.f;
 
   const int frow = lane & 31, fk = lane >> 5;
-  // fragment double buffer: the reads of k-step ks+1 are in flight while the
-  // matrix cores work on k-step ks
-  bf16x8 af[2][MB], bfr[2][NB];
-  auto load_frags = [&](int buf, const char* sa, int ks) {
-    const char* sb = sa + BM * 128;
-    const int c = ks * 2 + fk;
+  unsigned aoff[MB], boff[NB];
 #pragma unroll
-    for (int i = 0; i < MB; i++) {
-      const int row = wave_m * WM + i * 32 + frow;
-      af[buf][i] = as_bf16x8(*reinterpret_cast<const u32x4*>(sa + row * 128 + ((c ^ (row & 7)) << 4)));
-    }
-#pragma unroll
-    for (int j = 0; j < NB; j++) {
-      const int row = wave_n * WN + j * 32 + frow;
-      bfr[buf][j] = as_bf16x8(*reinterpret_cast<const u32x4*>(sb + row * 128 + ((c ^ (row & 7)) << 4)));
-    }
-  };
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  load_frags(0, smem, 0);
-  for (int kt = 0; kt < nk; kt++) {
-    const char* sa = smem + (kt & 1) * STAGE;
-    // the last iteration re-fetches its own K slice, keeping the body one block
-    gload(min(kt + 1, nk - 1));
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ks++) {
-      if (ks + 1 < BK / 16) load_frags((ks + 1) & 1, sa, ks + 1);
-#pragma unroll
-      for (int i = 0; i < MB; i++)
-#pragma unroll
-        for (int j = 0; j < NB; j++) acc[i][j] = mfma32(af[ks & 1][i], bfr[ks & 1][j], acc[i][j]);
-      // issue order inside the k-step: the global fetch of the next slice (first
-      // step only), the next step's fragment reads, then this step's MFMAs
-      if (ks == 0) __builtin_amdgcn_sched_group_barrier(0x020, NA + NBC, 0);
-      if (ks + 1 < BK / 16) __builtin_amdgcn_sched_group_barrier(0x100, MB + NB, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, MB * NB, 0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    // buffer (kt + 1) & 1 was last read in iteration kt - 1, before the barrier
-    // that closed it
-    lstore((kt + 1) & 1);
-    __syncthreads();
-    load_frags(0, smem + ((kt + 1) & 1) * STAGE, 0);
+  for (int i = 0; i < MB; i++) {
+    const int r = wave_m * WM + i * 32 + frow;
+    aoff[i] = r * ROWB + (((unsigned)fk ^ ((r >> 1) & 3)) << 4);
   }
+#pragma unroll
+  for (int j = 0; j < NB; j++) {
+    const int r = wave_n * WN + j * 32 + frow;
+    boff[j] = (BM + r) * ROWB + (((unsigned)fk ^ ((r >> 1) & 3)) << 4);
+  }
+  // k-step ks of a stage reads logical chunk 2 ks + fk; the XOR with the row
+  // term commutes with the +2 (bit 1 only), so ks = 1 is the base ^ 32 bytes
+  u32x4 fa[2][MB], fb[2][NB];
+  auto read_frags = [&](int buf, int st, int ks) {
+    const unsigned slot = sbase + (unsigned)((st % NS) * STAGE);
+    const unsigned kx = ks ? 32u : 0u;
+#pragma unroll
+    for (int i = 0; i < MB; i++) fa[buf][i] = lds_read16(slot + (aoff[i] ^ kx));
+#pragma unroll
+    for (int j = 0; j < NB; j++) fb[buf][j] = lds_read16(slot + (boff[j] ^ kx));
+  };
+
+  // One slice: its two k-steps.  `more` issues the fragment reads of the next
+  // slice's first k-step behind the barrier.  The last slice must not: the
+  // compiler sees the result of a read that is never consumed as dead and may
+  // hand its registers to the epilogue while the read is still in flight, and
+  // the landing data would then overwrite them.
+  auto slice = [&](int kt, bool more) {
+    __builtin_amdgcn_sched_barrier(0);
+    // slot (kt + NS - 1) % NS was last read in slice kt - 1, before its barrier
+    issue(kt + NS - 1);
+    read_frags(1, kt, 1);
+    lgkm_wait<NREAD>();  // the k-step 0 fragments (older reads) have landed
+    pin(fa[0]);
+    pin(fb[0]);
+#pragma unroll
+    for (int i = 0; i < MB; i++)
+#pragma unroll
+      for (int j = 0; j < NB; j++) acc[i][j] = mfma32(as_bf16x8(fa[0][i]), as_bf16x8(fb[0][j]), acc[i][j]);
+    __builtin_amdgcn_sched_barrier(0);
+    // own DMA of stage kt + 1 landed, own reads of stage kt done; after the
+    // barrier everyone's are, so stage kt + 1 is readable and slot kt % NS free
+    vm_wait<VM_KEEP>();
+    lgkm_wait<0>();
+    pin(fa[1]);
+    pin(fb[1]);
+    wg_barrier();
+    if (more) read_frags(0, kt + 1, 0);
+#pragma unroll
+    for (int i = 0; i < MB; i++)
+#pragma unroll
+      for (int j = 0; j < NB; j++) acc[i][j] = mfma32(as_bf16x8(fa[1][i]), as_bf16x8(fb[1][j]), acc[i][j]);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+#pragma unroll
+  for (int st = 0; st < NS - 1; st++) issue(st);
+  vm_wait<VM_KEEP>();
+  wg_barrier();
+  read_frags(0, 0, 0);
+  for (int kt = 0; kt < nk - 1; kt++) slice(kt, true);
+  slice(nk - 1, false);
+  // drain: no DMA may still target this workgroup's LDS when it exits (no
+  // fragment read is outstanding: the last slice waited for all of them)
+  vm_wait<0>();
 
   // epilogue
   const int ccol = lane & 31, crow = 4 * (lane >> 5);
@@ -319,7 +362,7 @@ template <int BM, int BN, int WM, int WN, int EPI, bool SPLIT>
 hipError_t run(const GemmArgs& a, int ksplit, hipStream_t stream) {
   const int tiles_m = (a.M + BM - 1) / BM, tiles_n = (a.N + BN - 1) / BN;
   const int threads = (BM / WM) * (BN / WN) * 64;
-  const size_t lds = 2 * (BM + BN) * 128;
+  const size_t lds = (size_t)NS * (BM + BN) * BKS * 2;
   dim3 grid(tiles_m * tiles_n, ksplit);
   gemm_kernel<BM, BN, WM, WN, EPI, SPLIT><<<grid, threads, lds, stream>>>(a, tiles_m, tiles_n,
                                                                           a.K / ksplit);
@@ -354,7 +397,7 @@ hipError_t run_shape(const GemmArgs& a, int ksplit, hipStream_t stream) {
 
 template <int BM, int BN, int WM, int WN>
 hipError_t set_lds_attr() {
-  const int lds = 2 * (BM + BN) * 128;
+  const int lds = NS * (BM + BN) * BKS * 2;
   hipError_t e;
 #define MX_SET(EPI, SPLIT)                                                                  \
   e = hipFuncSetAttribute((const void*)gemm_kernel<BM, BN, WM, WN, EPI, SPLIT>,             \
@@ -387,8 +430,20 @@ size_t gemm_scratch_floats(int M, int N, int K) {
 }
 
 hipError_t launch_gemm(const GemmArgs& a, size_t ws_floats, hipStream_t stream) {
+  return launch_gemm_config(a, ws_floats, -1, 0, stream);
+}
+
+int gemm_num_configs() { return kNumShapes; }
+
+hipError_t launch_gemm_config(const GemmArgs& a, size_t ws_floats, int cfg, int ksplit,
+                              hipStream_t stream) {
   if (a.M == 0) return hipSuccess;
   Plan p = choose(a.M, a.N, a.K);
+  if (cfg >= 0 && cfg < kNumShapes) {
+    p.cfg = cfg;
+    p.ksplit = ksplit >= 1 ? ksplit : 1;
+    if (a.K % (BK * p.ksplit) != 0) return hipErrorInvalidValue;
+  }
   if (p.ksplit > 1 && (size_t)p.ksplit * a.M * a.N > ws_floats) p.ksplit = 1;
   switch (p.cfg) {
     case 0: return run_shape<256, 256, 128, 64>(a, p.ksplit, stream);

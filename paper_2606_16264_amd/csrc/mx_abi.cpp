@@ -773,14 +773,26 @@ MX_EXPORT size_t mx_debug_gemm_ws_bytes(int32_t M, int32_t N, int32_t K) {
 MX_EXPORT mx_status mx_debug_gemm(int32_t M, int32_t N, int32_t K, const uint16_t* A,
                                   const uint16_t* B, uint16_t* C, const uint16_t* R,
                                   int32_t epilogue, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return mx_debug_gemm_config(M, N, K, A, B, C, R, epilogue, -1, 0, ws, ws_bytes, stream);
+}
+
+MX_EXPORT mx_status mx_debug_gemm_config(int32_t M, int32_t N, int32_t K, const uint16_t* A,
+                                         const uint16_t* B, uint16_t* C, const uint16_t* R,
+                                         int32_t epilogue, int32_t tile_cfg, int32_t ksplit,
+                                         void* ws, size_t ws_bytes, hipStream_t stream) {
   g_err.clear();
   if (M < 0 || N <= 0 || K <= 0) return fail(MX_ERR_INVALID, "bad GEMM shape %d x %d x %d", M, N, K);
   if (K % 64) return fail(MX_ERR_UNSUPPORTED, "K %d is not a multiple of 64", K);
+  if (tile_cfg < -1 || tile_cfg >= gemm_num_configs())
+    return fail(MX_ERR_INVALID, "tile config %d out of range", tile_cfg);
+  if (tile_cfg >= 0 && (ksplit < 1 || ksplit > 64 || K % (64 * ksplit) != 0))
+    return fail(MX_ERR_INVALID, "K split %d does not divide K %d into multiples of 64", ksplit, K);
   if (epilogue < 0 || epilogue > 2) return fail(MX_ERR_INVALID, "bad epilogue %d", epilogue);
   if (epilogue == EPI_SWIGLU && N % 64) return fail(MX_ERR_UNSUPPORTED, "SwiGLU needs N % 64 == 0");
   if (M == 0) return MX_OK;
   if (!A || !B || !C || (epilogue == EPI_RESIDUAL && !R)) return fail(MX_ERR_NULL, "NULL operand");
-  const size_t need = gemm_scratch_floats(M, N, K);
+  const size_t need = tile_cfg >= 0 ? (ksplit > 1 ? (size_t)ksplit * M * N : 0)
+                                    : gemm_scratch_floats(M, N, K);
   if (need && (!ws || ws_bytes < need * 4))
     return fail(MX_ERR_TOO_LARGE, "GEMM scratch %zu bytes < %zu", ws_bytes, need * 4);
   DeviceState* ds;
@@ -788,7 +800,7 @@ MX_EXPORT mx_status mx_debug_gemm(int32_t M, int32_t N, int32_t K, const uint16_
   if (st != MX_OK) return st;
   const int ldc = epilogue == EPI_SWIGLU ? N / 2 : N;
   GemmArgs g{A, B, C, R, (float*)ws, M, N, K, K, K, ldc, N, epilogue, {}};
-  hipError_t e = launch_gemm(g, ws ? ws_bytes / 4 : 0, stream);
+  hipError_t e = launch_gemm_config(g, ws ? ws_bytes / 4 : 0, tile_cfg, ksplit, stream);
   if (e != hipSuccess) return hip_fail(e, "gemm launch");
   return MX_OK;
 }

@@ -87,6 +87,11 @@ struct GemmArgs {
 // kMaxSplitFloats of scratch.
 constexpr size_t kMaxSplitFloats = size_t(16) << 20;
 hipError_t launch_gemm(const GemmArgs& args, size_t ws_floats, hipStream_t stream);
+// The same with a forced tile shape (index < gemm_num_configs()) and K split;
+// cfg < 0 uses the cost model.
+hipError_t launch_gemm_config(const GemmArgs& args, size_t ws_floats, int cfg, int ksplit,
+                              hipStream_t stream);
+int gemm_num_configs();
 size_t gemm_scratch_floats(int M, int N, int K);
 hipError_t gemm_init();
 

@@ -134,3 +134,21 @@ def test_workspace_bound_covers_batch(key, P):
     need_attn = mx.mx_workspace_bytes_for(mx_batch(mx, b), shape=mx_shape(mx, cfg, b.pool_pages))
     assert need_attn < need
     assert mx.mx_packed_weights_bytes(c) >= 2 * cfg.params
+
+
+@pytest.mark.parametrize("args,status", [
+    ((64, 256, 256, 0, 4, 1), "MX_ERR_INVALID"),       # tile shape out of range
+    ((64, 256, 256, 0, -2, 1), "MX_ERR_INVALID"),
+    ((64, 256, 256, 0, 0, 0), "MX_ERR_INVALID"),       # forced shape without a split count
+    ((64, 256, 256, 0, 0, 3), "MX_ERR_INVALID"),       # split not dividing K into 64s
+    ((64, 256, 160, 0, 0, 1), "MX_ERR_UNSUPPORTED"),   # K not a multiple of 64
+    ((-1, 256, 256, 0, 0, 1), "MX_ERR_INVALID"),       # negative M
+    ((64, 96, 256, 2, 0, 1), "MX_ERR_UNSUPPORTED"),    # SwiGLU needs N % 64 == 0
+    ((64, 256, 256, 3, 0, 1), "MX_ERR_INVALID"),       # the QKV epilogue is not exposed here
+    ((64, 256, 512, 0, 0, 2), "MX_ERR_TOO_LARGE"),     # split scratch larger than ws
+])
+def test_debug_gemm_config_errors(args, status):
+    M, N, K, epi, cfg, ks = args
+    st = mx.lib().mx_debug_gemm_config(M, N, K, 0x1000, 0x2000, 0x3000, 0x4000, epi, cfg, ks,
+                                       0x5000, 16, None)
+    assert st == getattr(mx, status), st

@@ -238,24 +238,34 @@ def test_paged_attn_needle():
 
 
 # ----------------------------------------------------------------------- GEMM
-@pytest.mark.parametrize("M,N,K,epi", [
-    (1, 768, 256, 0), (64, 12288, 4096, 0), (132, 1024, 256, 1), (576, 4096, 4096, 1),
-    (577, 2048, 512, 2), (1000, 22016, 4096, 2), (2304, 6144, 4096, 0), (256, 4096, 11008, 1),
-    (8, 256, 1024, 2),
-])
-def test_gemm_matches_oracle(M, N, K, epi):
-    say(f"case: gemm M={M} N={N} K={K} epi={epi}")
+CANARY = 0x7FC1  # a NaN pattern no GEMM output takes
+
+
+def gemm_case(M, N, K, epi, tile_cfg=-1, ksplit=0):
+    """C = epi(A B^T) through the C-ABI against the oracle; C sits between two
+    canary rows on each side, which must come back untouched."""
+    say(f"case: gemm M={M} N={N} K={K} epi={epi} cfg={tile_cfg} ksplit={ksplit}")
     rng = np.random.default_rng(M + N + K + epi)
     a = wl.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
     w = wl.f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * 0.02)
     r = wl.f32_to_bf16_bits(rng.standard_normal((M, N), dtype=np.float32))
     ncol = N // 2 if epi == 2 else N
-    C = torch.empty((M, ncol), dtype=torch.uint16, device="cuda")
-    ws = ws_tensor(max(mx.mx_debug_gemm_ws_bytes(M, N, K), 256))
-    mx.mx_debug_gemm(dev(a), dev(w), C, dev(r) if epi == 1 else None, epi, ws)
+    # filled and checked through the int16 view: few device ops exist for uint16
+    buf16 = torch.full(((M + 4) * ncol,), CANARY, dtype=torch.int16, device="cuda")
+    C = buf16.view(torch.uint16)[2 * ncol:(M + 2) * ncol].view(M, ncol)
+    need = mx.mx_debug_gemm_ws_bytes(M, N, K) if tile_cfg < 0 else \
+        (ksplit * M * N * 4 if ksplit > 1 else 0)
+    ws = ws_tensor(max(need, 256))
+    mx.mx_debug_gemm(dev(a), dev(w), C, dev(r) if epi == 1 else None, epi, ws,
+                     tile_cfg=tile_cfg, ksplit=ksplit)
     sync()
-    # sampled rows keep the fp64 reference cheap at the large shapes
-    rows = np.unique(np.concatenate([[0, M - 1], rng.integers(0, M, size=min(M, 48))]))
+    guard = torch.cat([buf16[:2 * ncol], buf16[(M + 2) * ncol:]]).cpu().numpy()
+    assert (guard == CANARY).all(), "GEMM wrote outside C"
+    # every row at small shapes, sampled rows keep the fp64 reference cheap at large ones
+    if M * N * K <= (1 << 31):
+        rows = np.arange(M)
+    else:
+        rows = np.unique(np.concatenate([[0, M - 1], rng.integers(0, M, size=min(M, 48))]))
     acc = oracle.linear(wl.bf16_bits_to_f64(a[rows]), w)
     if epi == 1:
         exp = acc + wl.bf16_bits_to_f64(r[rows])
@@ -267,6 +277,25 @@ def test_gemm_matches_oracle(M, N, K, epi):
     else:
         exp = acc
     assert_rows_close(bits_to_f64(C)[rows], exp, what="gemm")
+
+
+@pytest.mark.parametrize("M,N,K,epi", [
+    (1, 768, 256, 0), (64, 12288, 4096, 0), (132, 1024, 256, 1), (576, 4096, 4096, 1),
+    (577, 2048, 512, 2), (1000, 22016, 4096, 2), (2304, 6144, 4096, 0), (256, 4096, 11008, 1),
+    (8, 256, 1024, 2),
+])
+def test_gemm_matches_oracle(M, N, K, epi):
+    gemm_case(M, N, K, epi)
+
+
+# every tile shape with every epilogue, ragged M and N edges, with and without a K split
+@pytest.mark.parametrize("tile_cfg", [0, 1, 2, 3])
+@pytest.mark.parametrize("M,N,K,epi,ksplit", [
+    (577, 2048, 512, 2, 1), (300, 1344, 768, 0, 1), (131, 1088, 512, 1, 1),
+    (97, 640, 1024, 2, 2), (33, 384, 2048, 1, 4), (257, 320, 256, 0, 2),
+])
+def test_gemm_forced_tile_shapes(tile_cfg, M, N, K, epi, ksplit):
+    gemm_case(M, N, K, epi, tile_cfg=tile_cfg, ksplit=ksplit)
 
 
 # ----------------------------------------------------------------------- layer step
