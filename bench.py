@@ -138,6 +138,8 @@ class Point:
 
 
 def time_fn(fn, steps, warmup):
+    """Mean ms per step over `steps` back-to-back steps (events bracketing the
+    whole run), plus the per-step distribution from events around each step."""
     import torch
     for _ in range(warmup):
         fn()
@@ -148,7 +150,35 @@ def time_fn(fn, steps, warmup):
         fn()
     e.record()
     torch.cuda.synchronize()
-    return s.elapsed_time(e) / steps  # ms
+    mean = s.elapsed_time(e) / steps
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev[0].record()
+    for i in range(steps):
+        fn()
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    per = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(steps))
+
+    def q(f):
+        return per[min(len(per) - 1, int(round(f * (len(per) - 1))))]
+    return mean, {"median": q(0.5), "p10": q(0.1), "p90": q(0.9)}
+
+
+def linear_fit(xs, ys):
+    """Least-squares line y = a + b x with R^2 (the latency-vs-prefill curve)."""
+    n = len(xs)
+    if n < 2:
+        return None
+    mx_, my = sum(xs) / n, sum(ys) / n
+    sxx = sum((x - mx_) ** 2 for x in xs)
+    if sxx == 0:
+        return None
+    b = sum((x - mx_) * (y - my) for x, y in zip(xs, ys)) / sxx
+    a = my - b * mx_
+    ss_tot = sum((y - my) ** 2 for y in ys)
+    ss_res = sum((y - a - b * x) ** 2 for x, y in zip(xs, ys))
+    return {"intercept_us": round(a, 2), "slope_us_per_prefill_token": round(b, 5),
+            "r2": round(1.0 - ss_res / ss_tot, 5) if ss_tot > 0 else 1.0, "points": n}
 
 
 def kernel_breakdown(pt, steps, warmup):
@@ -260,28 +290,39 @@ def main():
 
     curve = []
     headline = None
+    kernels = {}
     for P in sweep:
         pt = Point(key, P, None, packed, cfg)
         torch.cuda.synchronize()
-        ms = time_fn(pt.step, args.steps, args.warmup)
+        ms, dist = time_fn(pt.step, args.steps, args.warmup)
         us = ms * 1e3
         roof = t_roof(pt.parts) * 1e6
         rec = dict(P=int(P), T=pt.b.T, R=pt.b.R, us=round(us, 2),
+                   us_median=round(dist["median"] * 1e3, 2), us_p10=round(dist["p10"] * 1e3, 2),
+                   us_p90=round(dist["p90"] * 1e3, 2),
                    tokens_per_s=pt.b.T / (us * 1e-6),
                    decode_tokens_per_s=int((pt.b.phase == wl.DECODE).sum()) / (us * 1e-6),
                    t_roof_us=round(roof, 2), roof_frac=roof / us)
-        print(f"# P={P}: {us:.1f} us/step, {rec['tokens_per_s']:.0f} tok/s, "
+        print(f"# P={P}: {us:.1f} us/step (median {rec['us_median']}, p10 {rec['us_p10']}, "
+              f"p90 {rec['us_p90']}), {rec['tokens_per_s']:.0f} tok/s, "
               f"roofline {roof:.1f} us ({rec['roof_frac']:.2f})", file=sys.stderr, flush=True)
+        if args.kernels:
+            kernels = kernel_breakdown(pt, max(5, args.steps // 2), 2)
+            rec["kernel_us"] = {k: round(v["us"], 2) for k, v in kernels.items()}
+            pa = kernels.get("paged_attn")
+            if pa:
+                rec["attn_hbm_frac"] = round(pa["hbm_frac"], 4)
+                rec["attn_mfma_frac"] = round(pa["mfma_frac"], 4)
+            for k, v in kernels.items():
+                print(f"#   kernel {k}: {v['us']:.1f} us  hbm_frac={v['hbm_frac']:.3f}  "
+                      f"mfma_frac={v['mfma_frac']:.3f}", file=sys.stderr, flush=True)
         if P == sweep[-1]:
             headline = (pt, rec)
         else:
             pt.release()
         curve.append(rec)
     pt, rec = headline
-    kernels = kernel_breakdown(pt, max(5, args.steps // 2), 2) if args.kernels else {}
-    for k, v in kernels.items():
-        print(f"# kernel {k}: {v['us']:.1f} us  hbm_frac={v['hbm_frac']:.3f}  "
-              f"mfma_frac={v['mfma_frac']:.3f}", file=sys.stderr, flush=True)
+    fit = linear_fit([c["P"] for c in curve], [c["us"] for c in curve])
     # dominant kernel and its roofline: the attention is HBM-bound (decode
     # K/V streaming), the projections MFMA-bound at these token counts
     dom = max(kernels, key=lambda k: kernels[k]["us"]) if kernels else None
@@ -325,6 +366,7 @@ def main():
                                f"{pt.b.prefill_tokens} mixed prefill tokens",
                    "T": pt.b.T, "R": pt.b.R, "P": pt.b.prefill_tokens},
         "curve": curve,
+        "curve_fit": fit,
         "t_roof_us": rec["t_roof_us"],
         "roof_frac": round(rec["roof_frac"], 4),
         "roofline": roofline,

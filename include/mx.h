@@ -26,6 +26,9 @@
  *                                                     so that the matrix-core
  *                                                     operands load contiguously)
  *    Byte offsets are 64-bit; pools larger than 4 GiB are supported.
+ *  - Every device tensor and the workspace must be 16-byte aligned (the
+ *    kernels move data in 16-byte vectors); a misaligned pointer is rejected
+ *    with MX_ERR_INVALID.
  *  - Ownership: the caller allocates and owns every device buffer (weights,
  *    pools, activations, workspace) and the stream.  The library keeps no
  *    pointer after a call returns except for work already enqueued.  Host
@@ -55,7 +58,7 @@ extern "C" {
 
 typedef enum {
   MX_OK = 0,
-  MX_ERR_INVALID = 1,     /* malformed batch or shape */
+  MX_ERR_INVALID = 1,     /* malformed batch or shape, or a misaligned pointer */
   MX_ERR_NO_SPACE = 2,    /* a page table is too short for the request's positions */
   MX_ERR_TOO_LARGE = 3,   /* the workspace is too small for this batch */
   MX_ERR_UNSUPPORTED = 4, /* head_dim not in {64, 128}, page size not 16, ... */

@@ -112,6 +112,77 @@ __device__ __forceinline__ void qkv_pair_store(const GemmArgs& a, int t, int c, 
   }
 }
 
+// QKV epilogue of one wave's block (rows r0.., columns c0..).  q and k heads
+// go through qkv_pair_store.  A v head goes to the transposed value pages
+// [page][kv head][dim][16 slots], where one dim of consecutive slots is a
+// contiguous run: when rows 8 jj .. 8 jj + 7 of a 32-row block hold tokens in
+// eight consecutive slots starting at a multiple of 8, the lane pair
+// (l, l ^ 32) trades halves so that each lane holds the eight tokens of one dim
+// and writes them with a single 16-byte store; otherwise every value is stored
+// on its own.
+template <int MB, int NB>
+__device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&acc)[MB][NB],
+                                             int r0, int c0, int lane) {
+  const QkvEpilogue& e = a.qkv;
+  const int hd = e.head_dim;
+  const int ccol = lane & 31, crow = 4 * (lane >> 5);
+  const bool upper = lane >= 32;
+  const int first_v_col = (e.nq + e.nkv) * hd;
+  const bool has_v = c0 + NB * 32 > first_v_col;  // the same for the whole wave
+#pragma unroll
+  for (int i = 0; i < MB; i++) {
+#pragma unroll
+    for (int jj = 0; jj < 4; jj++) {
+      const int rbase = r0 + i * 32 + 8 * jj;
+      if (rbase >= a.M) continue;
+      bool run8 = false;
+      int64_t s0 = 0;
+      if (has_v && rbase + 7 < a.M) {
+        s0 = e.tok_slot[rbase];
+        run8 = (s0 & 7) == 0;
+#pragma unroll
+        for (int k = 1; k < 8; k++) run8 = run8 && e.tok_slot[rbase + k] == s0 + k;
+      }
+#pragma unroll
+      for (int jp = 0; jp < NB / 2; jp++) {
+        const int cb = c0 + jp * 64;
+        if (cb >= a.N) continue;
+        const int colg = cb + ccol;
+        float lo[4], hi[4];
+#pragma unroll
+        for (int ii = 0; ii < 4; ii++) {
+          lo[ii] = acc[i][2 * jp][4 * jj + ii];
+          hi[ii] = acc[i][2 * jp + 1][4 * jj + ii];
+        }
+        if (cb >= first_v_col && run8) {
+          // lower lane: dim c, tokens 0..3 (own) + 4..7 (partner);
+          // upper lane: dim c + 32, tokens 0..3 (partner) + 4..7 (own)
+          float tok[8];
+#pragma unroll
+          for (int ii = 0; ii < 4; ii++) {
+            const float got = __shfl_xor(upper ? lo[ii] : hi[ii], 32);
+            tok[ii] = upper ? got : lo[ii];
+            tok[4 + ii] = upper ? hi[ii] : got;
+          }
+          const int within = colg % hd + (upper ? 32 : 0);
+          const int vh = cb / hd - e.nq - e.nkv;
+          u32x4 w;
+#pragma unroll
+          for (int h = 0; h < 4; h++) w[h] = pack_bf16x2(tok[2 * h], tok[2 * h + 1]);
+          *reinterpret_cast<u32x4*>(e.v_pool + (((s0 >> 4) * e.nkv + vh) * hd + within) * 16 +
+                                    (s0 & 15)) = w;
+        } else {
+#pragma unroll
+          for (int ii = 0; ii < 4; ii++) {
+            const int row = rbase + crow + ii;
+            if (row < a.M) qkv_pair_store(a, row, colg, lo[ii], hi[ii]);
+          }
+        }
+      }
+    }
+  }
+}
+
 template <int BM, int BN, int WM, int WN, int EPI, bool SPLIT>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmArgs a, int tiles_m,
                                                                            int tiles_n,
@@ -236,6 +307,10 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   vm_wait<0>();
 
   // epilogue
+  if constexpr (EPI == EPI_QKV && !SPLIT) {
+    qkv_epilogue<MB, NB>(a, acc, m0 + wave_m * WM, n0 + wave_n * WN, lane);
+    return;
+  }
   const int ccol = lane & 31, crow = 4 * (lane >> 5);
 #pragma unroll
   for (int i = 0; i < MB; i++) {
@@ -248,13 +323,6 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
         for (int j = 0; j < NB; j++) {
           const int colg = n0 + wave_n * WN + j * 32 + ccol;
           if (colg < a.N) a.partial[((int64_t)kz * a.M + row) * a.N + colg] = acc[i][j][r];
-        }
-      } else if constexpr (EPI == EPI_QKV) {
-#pragma unroll
-        for (int jp = 0; jp < NB / 2; jp++) {
-          const int colg = n0 + wave_n * WN + jp * 64 + ccol;  // low block column
-          if (colg >= a.N) continue;
-          qkv_pair_store(a, row, colg, acc[i][2 * jp][r], acc[i][2 * jp + 1][r]);
         }
       } else if constexpr (EPI == EPI_SWIGLU) {
 #pragma unroll

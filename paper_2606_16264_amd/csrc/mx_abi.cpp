@@ -8,6 +8,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <initializer_list>
 #include <map>
 #include <mutex>
 #include <string>
@@ -478,6 +479,13 @@ MX_EXPORT const char* mx_last_error(void) { return g_err.c_str(); }
 
 MX_EXPORT uint32_t mx_version(void) { return (1u << 16) | 0u; }
 
+// Device tensors are read and written with 16-byte vector accesses.
+static mx_status check_aligned(std::initializer_list<const void*> ptrs) {
+  for (const void* q : ptrs)
+    if ((uintptr_t)q & 15) return fail(MX_ERR_INVALID, "device pointer %p is not 16-byte aligned", q);
+  return MX_OK;
+}
+
 MX_EXPORT mx_status mx_batch_validate(const mx_batch* batch, const mx_attn_shape* shape) {
   g_err.clear();
   return validate_batch(batch, shape, nullptr);
@@ -532,6 +540,9 @@ MX_EXPORT mx_status mx_pack_weights(const mx_layer_cfg* cfg, const mx_layer_weig
   if (st != MX_OK) return st;
   if (!w || !packed || !w->ln1_g || !w->w_qkv || !w->w_o || !w->ln2_g || !w->w_gate_up || !w->w_down)
     return fail(MX_ERR_NULL, "weight pointer is NULL");
+  if ((st = check_aligned({packed, w->ln1_g, w->w_qkv, w->w_o, w->ln2_g, w->w_gate_up, w->w_down})) !=
+      MX_OK)
+    return st;
   const WLayout L = wlayout(cfg);
   if (packed_bytes < L.total)
     return fail(MX_ERR_TOO_LARGE, "packed buffer %zu bytes < %zu", packed_bytes, L.total);
@@ -573,6 +584,7 @@ MX_EXPORT mx_status mx_kv_append(const mx_batch* batch, const mx_attn_shape* sha
   if (st != MX_OK) return st;
   if (T == 0) return MX_OK;
   if (!k_new || !v_new || !k_pool || !v_pool) return fail(MX_ERR_NULL, "tensor pointer is NULL");
+  if ((st = check_aligned({k_new, v_new, k_pool, v_pool, ws})) != MX_OK) return st;
   Plan p;
   build_plan(batch, shape, false, p);
   const Layout L = layout_for(p, shape, nullptr);
@@ -597,6 +609,7 @@ MX_EXPORT mx_status mx_paged_attn(const mx_batch* batch, const mx_attn_shape* sh
   if (st != MX_OK) return st;
   if (T == 0) return MX_OK;
   if (!q || !k_pool || !v_pool || !out) return fail(MX_ERR_NULL, "tensor pointer is NULL");
+  if ((st = check_aligned({q, k_pool, v_pool, out, ws})) != MX_OK) return st;
   Plan p;
   build_plan(batch, shape, true, p);
   const Layout L = layout_for(p, shape, nullptr);
@@ -626,6 +639,7 @@ MX_EXPORT mx_status mx_layer_step(const mx_batch* batch, const mx_layer_cfg* cfg
   if (!packed_weights || !x || !y || !k_pool || !v_pool)
     return fail(MX_ERR_NULL, "tensor pointer is NULL");
   if (x == y) return fail(MX_ERR_INVALID, "y must not alias x");
+  if ((st = check_aligned({packed_weights, x, y, k_pool, v_pool, ws})) != MX_OK) return st;
   Plan p;
   build_plan(batch, s, true, p);
   const Layout L = layout_for(p, s, cfg);
@@ -791,6 +805,7 @@ MX_EXPORT mx_status mx_debug_gemm_config(int32_t M, int32_t N, int32_t K, const 
   if (epilogue == EPI_SWIGLU && N % 64) return fail(MX_ERR_UNSUPPORTED, "SwiGLU needs N % 64 == 0");
   if (M == 0) return MX_OK;
   if (!A || !B || !C || (epilogue == EPI_RESIDUAL && !R)) return fail(MX_ERR_NULL, "NULL operand");
+  if (mx_status sa = check_aligned({A, B, C, R, ws}); sa != MX_OK) return sa;
   const size_t need = tile_cfg >= 0 ? (ksplit > 1 ? (size_t)ksplit * M * N : 0)
                                     : gemm_scratch_floats(M, N, K);
   if (need && (!ws || ws_bytes < need * 4))

@@ -152,3 +152,22 @@ def test_debug_gemm_config_errors(args, status):
     st = mx.lib().mx_debug_gemm_config(M, N, K, 0x1000, 0x2000, 0x3000, 0x4000, epi, cfg, ks,
                                        0x5000, 16, None)
     assert st == getattr(mx, status), st
+
+
+def test_misaligned_pointers_rejected_before_device_work():
+    cfg = wl.CONFIGS["c1"]
+    c = mx_cfg(mx, cfg, 64)
+    good = one(mx.MX_PREFILL, 4, 0, [1])
+    # x off by 8 bytes
+    st = mx.lib().mx_layer_step(good.ptr, mx.ctypes.byref(c), 0x1000, 0x2008, 0x3000, 0x4000,
+                                0x5000, 0x6000, 1 << 30, None)
+    assert st == mx.MX_ERR_INVALID
+    st = mx.lib().mx_paged_attn(good.ptr, mx.ctypes.byref(c.attn), 0x1000, 0x2000, 0x3002,
+                                0x4000, 0x6000, 1 << 30, None)
+    assert st == mx.MX_ERR_INVALID
+    st = mx.lib().mx_kv_append(good.ptr, mx.ctypes.byref(c.attn), 0x1000, 0x2000, 0x3000, 0x4000,
+                               0x6004, 1 << 30, None)
+    assert st == mx.MX_ERR_INVALID
+    st = mx.lib().mx_debug_gemm_config(64, 256, 256, 0x1000, 0x2000, 0x3006, None, 0, 0, 1,
+                                       0x5000, 1 << 20, None)
+    assert st == mx.MX_ERR_INVALID

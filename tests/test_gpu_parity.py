@@ -308,10 +308,11 @@ def pack_layer(cfg, b, w):
     return c, packed
 
 
-def run_layer(cfg, b, w, x, seed, reps=1):
+def run_layer(cfg, b, w, x, seed, reps=1, keep_before=False):
     c, packed = pack_layer(cfg, b, w)
     k, v = wdev.alloc_pools(cfg, b.pool_pages)
     wdev.fill_pools(k, v, cfg, b, seed, poison=True)
+    before = dict(k0=k.clone(), v0=v.clone()) if keep_before else {}
     mb = mx_batch(mx, b)
     ws = ws_tensor(mx.mx_workspace_bytes_for(mb, cfg=c))
     xd = dev(x)
@@ -328,7 +329,7 @@ def run_layer(cfg, b, w, x, seed, reps=1):
         return ws[o:o + T * cols * 2].view(torch.uint16).reshape(T, cols)
 
     return dict(y=y, k=k, v=v, q=view("q", nqd), o=view("o", nqd), x1=view("x1", H),
-                a=view("a", F), h2=view("h", H))
+                a=view("a", F), h2=view("h", H), **before)
 
 
 def staged_attention(cfg, sub, x_sub, w, kp, vp, sub_rows):
@@ -443,6 +444,48 @@ def test_layer_step_small_gqa_full():
     rows = np.arange(b.T)
     check_layer(cfg, b, got, exp, rows, "small-gqa", staged_attention(cfg, b, x, ws, kp, vp, rows))
     check_pool_rows(cfg, b, got, exp.k_new, exp.v_new, rows)
+
+
+def small_weights(rng, cfg):
+    ws = {k: wl.f32_to_bf16_bits(rng.standard_normal(s, dtype=np.float32) * 0.02) for k, s in (
+        ("w_qkv", (cfg.qkv_rows, cfg.hidden)), ("w_o", (cfg.hidden, cfg.n_q_heads * cfg.head_dim)),
+        ("w_gu", (2 * cfg.ffn, cfg.hidden)), ("w_down", (cfg.hidden, cfg.ffn)))}
+    ws["g1"] = wl.f32_to_bf16_bits(1 + 0.1 * rng.standard_normal(cfg.hidden, dtype=np.float32))
+    ws["g2"] = wl.f32_to_bf16_bits(1 + 0.1 * rng.standard_normal(cfg.hidden, dtype=np.float32))
+    return ws
+
+
+def changed_slots(before, after, transposed):
+    """Slots (page * 16 + s) where a pool differs bitwise between two images."""
+    diff = before.view(torch.int16) != after.view(torch.int16)
+    # keys [page][kv head][16][d], values [page][kv head][d][16]
+    per_slot = diff.any(dim=3).any(dim=1) if not transposed else diff.any(dim=2).any(dim=1)
+    pg, sl = torch.nonzero(per_slot, as_tuple=True)
+    return set((pg.cpu().numpy().astype(np.int64) * 16 + sl.cpu().numpy()).tolist())
+
+
+@pytest.mark.parametrize("cfg", [SMALL_GQA, wl.LayerConfig("small-mha64", 256, 704, 4, 4, 64)],
+                         ids=lambda c: c.name)
+def test_layer_step_aligned_value_runs(cfg):
+    """Eight decodes put the first prefill row on an 8-aligned row and slot, so
+    the QKV epilogue writes whole 16-byte runs of the value pages; a chunk with
+    40 cached tokens stays aligned across page boundaries, and a 5-token chunk
+    ends on a partial run that mixes two requests.  Every row and every new
+    slot is checked, and no pool entry outside the new slots may change."""
+    say(f"case: layer step aligned value runs {cfg.name}")
+    rng = np.random.default_rng(91)
+    b = wl.custom_batch(rng, [3, 16, 40, 100, 7, 64, 15, 31], [(200, 0), (77, 40), (5, 3)])
+    w = small_weights(rng, cfg)
+    x = wl.f32_to_bf16_bits(rng.standard_normal((b.T, cfg.hidden), dtype=np.float32))
+    got = run_layer(cfg, b, w, x, 4343, keep_before=True)
+    kp, vp = wl.prior_kv_concat(cfg, b, 4343)
+    exp = oracle.layer_step(cfg.as_dict(), b.n_new, b.ctx_len, x, w, kp, vp)
+    rows = np.arange(b.T)
+    check_layer(cfg, b, got, exp, rows, cfg.name, staged_attention(cfg, b, x, w, kp, vp, rows))
+    check_pool_rows(cfg, b, got, exp.k_new, exp.v_new, rows)
+    written = set(oracle.token_map(b.n_new, b.ctx_len, b.page_tables, 16).tok_slot.tolist())
+    assert changed_slots(got["k0"], got["k"], False) <= written
+    assert changed_slots(got["v0"], got["v"], True) <= written
 
 
 @pytest.mark.parametrize("key,P", [("c2", 512), ("c2", 0), ("c3", 1024), ("c4", 2048)])

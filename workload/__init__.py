@@ -150,7 +150,7 @@ SWEEPS = {
     "c1": [128],
     "c2": [0, 512],
     "c3": [0, 256, 512, 1024, 2048, 4096],
-    "c4": [2048],
+    "c4": [0, 2048],
     "c5": [0, 1024, 2048, 3072, 4096, 5120, 6144, 7168, 8192],
 }
 
