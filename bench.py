@@ -42,7 +42,81 @@ def parse():
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB before timing (the "
                          "known-size reference that scales rocprofv3 byte counters)")
+    ap.add_argument("--summarize-stats", nargs=3, metavar=("STATS_CSV", "COMMAND", "OUT_MD"),
+                    help="write a markdown summary of a rocprofv3 --stats kernel_stats.csv "
+                         "(no GPU needed)")
+    ap.add_argument("--summarize-traffic", nargs=5,
+                    metavar=("FETCH_CSV", "WRITE_CSV", "COMMANDS_TXT", "WORKLOAD", "OUT_JSON"),
+                    help="HBM bytes per launch of paged_attn_kernel from two rocprofv3 --pmc "
+                         "runs (FETCH_SIZE, WRITE_SIZE), scaled by the 1 GiB copy calibration "
+                         "they contain (no GPU needed)")
     return ap.parse_args()
+
+
+def summarize_stats(csv_path, command, out_md):
+    """Markdown table of a rocprofv3 --kernel-trace --stats summary."""
+    import csv
+    rows = list(csv.DictReader(open(csv_path)))
+    total = sum(float(r["TotalDurationNs"]) for r in rows)
+    lines = ["# Kernel trace statistics: the layer step on the Llama-7B-shaped layer", "",
+             "Workload: hidden 4096, 32 x 128 MHA, FFN 11008; 64 decodes (contexts uniform in "
+             "[512, 2048]) with 0 and with 512 mixed prefill tokens (the bench sweep), including "
+             "setup (weight packing, pool fill) and the per-kernel timing steps.", "",
+             "Command (one MI355X):", "", "```", command, "```", "",
+             "Durations in microseconds (rocprofv3 kernel trace).  gemm_kernel<BM, BN, WM, WN, "
+             "epilogue, split>: epilogue 0 store, 1 residual, 2 SwiGLU, 3 QKV.", "",
+             "| kernel | calls | average us | min us | max us | share % |",
+             "|---|---:|---:|---:|---:|---:|"]
+    rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    for r in rows:
+        name = r["Name"].replace("(anonymous namespace)::", "").replace("mx::", "")
+        name = name.split("(")[0].replace("void ", "")
+        lines.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                     f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | "
+                     f"{100.0 * float(r['TotalDurationNs']) / total:.1f} |")
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def summarize_traffic(fetch_csv, write_csv, commands_txt, workload, out_json,
+                      kernel="paged_attn_kernel", source="paper_2606_16264_amd/csrc/attention.hip"):
+    """HBM bytes per launch of `kernel`: FETCH_SIZE and WRITE_SIZE (KiB per
+    dispatch) scaled by what the same counters read for the 1 GiB device copy
+    (torch's copyBuffer) recorded in the same runs."""
+    import csv
+    calib = 1 << 30
+
+    def read(path, counter):
+        ks, cp = [], []
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            v = float(r["Counter_Value"])
+            if kernel in r["Kernel_Name"]:
+                ks.append(v)
+            elif "copyBuffer" in r["Kernel_Name"]:
+                cp.append(v)
+        return ks, max(cp)  # the calibration copy is the largest copy in the run
+    kf, cf = read(fetch_csv, "FETCH_SIZE")
+    kw, cw = read(write_csv, "WRITE_SIZE")
+    fs, ws_ = calib / (cf * 1024.0), calib / (cw * 1024.0)
+    fetch = sum(kf) / len(kf) * 1024.0 * fs
+    write = sum(kw) / len(kw) * 1024.0 * ws_
+    key, P = workload.split("_P")
+    import workload as wl
+    parts = algorithmic(wl.CONFIGS[key], wl.make_batch(key, int(P)))
+    rec = {"kernel": kernel, "workload": workload,
+           "commands": [l.strip() for l in open(commands_txt) if l.strip()],
+           "copy_calibration": {"bytes": calib, "FETCH_SIZE_KiB": cf, "WRITE_SIZE_KiB": cw,
+                                "fetch_scale": round(fs, 4), "write_scale": round(ws_, 4)},
+           "dispatches": len(kf), "FETCH_SIZE_KiB_mean": round(sum(kf) / len(kf), 1),
+           "WRITE_SIZE_KiB_mean": round(sum(kw) / len(kw), 1),
+           "fetch_bytes_per_launch": int(fetch), "write_bytes_per_launch": int(write),
+           "hbm_bytes_per_launch": int(fetch + write),
+           "algorithmic_bytes_per_launch": int(parts["attention"]["bytes"]),
+           "source_sha256": source_sha(source)}
+    with open(out_json, "w") as f:
+        json.dump(rec, f, indent=1)
 
 
 def source_sha(rel):
@@ -255,6 +329,12 @@ def cpu_baseline(key, cfg, w_host, budget_s):
 
 def main():
     args = parse()
+    if args.summarize_stats:
+        summarize_stats(*args.summarize_stats)
+        return
+    if args.summarize_traffic:
+        summarize_traffic(*args.summarize_traffic)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1 "
                                    "(multi-GPU sharding is described in DESIGN.md, not run)"}))

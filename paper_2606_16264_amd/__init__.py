@@ -65,6 +65,12 @@ def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
                           "(there is no fallback implementation)")
+    # torch first: it loads the HIP runtime it ships with, and libmx.so's own
+    # dependency on libamdhip64.so.7 then binds to that same runtime.  Loaded
+    # the other way round, the process ends up with two HIP runtimes (the
+    # system one for libmx.so, torch's for torch), and streams and pointers
+    # passed between them are invalid.
+    import torch  # noqa: F401
     L = ctypes.CDLL(LIB_PATH)
     P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     BP = ctypes.POINTER(_Batch)

@@ -45,37 +45,31 @@ struct Chunk {
 // indices the second product expects from this lane group.
 template <int HD>
 __device__ __forceinline__ void load_chunk(Chunk<HD>& c, const AttnParams& p, int kvh, int pid0,
-                                           int pid1, int col, int g4) {
+                                           int pid1, int safe, int col, int g4) {
+  // A page id of -1 (past the split's end) reads the request's first page
+  // instead: those keys and values are masked out by select in
+  // process_chunk, and every load stays unconditional, which keeps the
+  // count of loads in flight the same on every path.
   // keys: lane row m = col; its key kappa_b(col) lives in page col / 8
   {
-    const int page = (col < 8) ? pid0 : pid1;
+    const int page0 = (col < 8) ? pid0 : pid1;
+    const int page = page0 >= 0 ? page0 : safe;
     const int slot0 = 8 * ((col >> 2) & 1) + (col & 3);
-    if (page >= 0) {
-      const uint16_t* kb_ptr = p.k_pool + ((int64_t)page * p.nkv + kvh) * (int64_t)(16 * HD);
+    const uint16_t* kb_ptr = p.k_pool + ((int64_t)page * p.nkv + kvh) * (int64_t)(16 * HD);
 #pragma unroll
-      for (int b = 0; b < 2; b++)
+    for (int b = 0; b < 2; b++)
 #pragma unroll
-        for (int ds = 0; ds < HD / 32; ds++)
-          c.k[b][ds] = *reinterpret_cast<const u32x4*>(kb_ptr + (slot0 + 4 * b) * HD + ds * 32 + 8 * g4);
-    } else {
-#pragma unroll
-      for (int b = 0; b < 2; b++)
-#pragma unroll
-        for (int ds = 0; ds < HD / 32; ds++) c.k[b][ds] = u32x4{0, 0, 0, 0};
-    }
+      for (int ds = 0; ds < HD / 32; ds++)
+        c.k[b][ds] = *reinterpret_cast<const u32x4*>(kb_ptr + (slot0 + 4 * b) * HD + ds * 32 + 8 * g4);
   }
   // values: lane group g reads keys 8 (g % 2) .. +7 of page g / 2 at d = 16 db + col
   {
-    const int page = (g4 < 2) ? pid0 : pid1;
-    if (page >= 0) {
-      const uint16_t* vb_ptr = p.v_pool + ((int64_t)page * p.nkv + kvh) * (int64_t)(16 * HD) + 8 * (g4 & 1);
+    const int page0 = (g4 < 2) ? pid0 : pid1;
+    const int page = page0 >= 0 ? page0 : safe;
+    const uint16_t* vb_ptr = p.v_pool + ((int64_t)page * p.nkv + kvh) * (int64_t)(16 * HD) + 8 * (g4 & 1);
 #pragma unroll
-      for (int db = 0; db < HD / 16; db++)
-        c.v[db] = *reinterpret_cast<const u32x4*>(vb_ptr + (db * 16 + col) * 16);
-    } else {
-#pragma unroll
-      for (int db = 0; db < HD / 16; db++) c.v[db] = u32x4{0, 0, 0, 0};
-    }
+    for (int db = 0; db < HD / 16; db++)
+      c.v[db] = *reinterpret_cast<const u32x4*>(vb_ptr + (db * 16 + col) * 16);
   }
 }
 
@@ -150,7 +144,7 @@ __device__ __forceinline__ void process_chunk(const Chunk<HD>& c, const bf16x8 (
 }
 
 template <int HD>
-__global__ __launch_bounds__(256) void paged_attn_kernel(AttnParams p) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void paged_attn_kernel(AttnParams p) {
   const AttnItem it = p.items[blockIdx.x];
   const ReqDev rq = p.reqs[it.req];
   const int lane = threadIdx.x & 63;
@@ -203,22 +197,48 @@ __global__ __launch_bounds__(256) void paged_attn_kernel(AttnParams p) {
     }
   }
 
-  // page ids are fetched two chunks ahead of use, so that the id lookup is not
-  // on the critical path of the key/value loads
-  auto pid = [&](int pi) -> int { return pi < page_end ? p.pages[rq.page_start + pi] : -1; };
-  Chunk<HD> cur, nxt;
+  // Two chunk buffers used in turn: the loads of the next chunk are in flight
+  // while the current one is processed.  The loop is unrolled by two so that
+  // no buffer is ever copied (a register copy of a buffer whose loads are in
+  // flight waits for them and serialises the prefetch), and a chunk's loads
+  // are issued only on the path where that chunk exists, unconditionally
+  // there, so the compiler's wait before each chunk covers exactly its own
+  // loads.  Page ids are fetched one chunk ahead of their loads.
+  const int safe = p.pages[rq.page_start];
+  auto pid = [&](int pi) -> int {
+    const int v = p.pages[rq.page_start + min(pi, rq.n_pages - 1)];
+    return pi < page_end ? v : -1;
+  };
+  Chunk<HD> ca, cb;
   int pi = chunk_first;
-  int n0 = pid(pi + chunk_step), n1 = pid(pi + chunk_step + 1);
-  if (pi < page_end) load_chunk<HD>(cur, p, kvh, pid(pi), pid(pi + 1), col, g4);
-  while (pi < page_end) {
-    const int pn = pi + chunk_step;
-    const int nn0 = pid(pn + chunk_step), nn1 = pid(pn + chunk_step + 1);
-    if (pn < page_end) load_chunk<HD>(nxt, p, kvh, n0, n1, col, g4);
-    process_chunk<HD>(cur, qf, o, m, l, pi, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
-    cur = nxt;
-    n0 = nn0;
-    n1 = nn1;
-    pi = pn;
+  if (pi < page_end) {
+    int n0 = pid(pi + chunk_step), n1 = pid(pi + chunk_step + 1);
+    load_chunk<HD>(ca, p, kvh, pid(pi), pid(pi + 1), safe, col, g4);
+    while (true) {
+      int pn = pi + chunk_step;
+      if (pn >= page_end) {
+        process_chunk<HD>(ca, qf, o, m, l, pi, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
+        break;
+      }
+      int nn0 = pid(pn + chunk_step), nn1 = pid(pn + chunk_step + 1);
+      load_chunk<HD>(cb, p, kvh, n0, n1, safe, col, g4);
+      process_chunk<HD>(ca, qf, o, m, l, pi, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
+      pi = pn;
+      n0 = nn0;
+      n1 = nn1;
+      pn = pi + chunk_step;
+      if (pn >= page_end) {
+        process_chunk<HD>(cb, qf, o, m, l, pi, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
+        break;
+      }
+      nn0 = pid(pn + chunk_step);
+      nn1 = pid(pn + chunk_step + 1);
+      load_chunk<HD>(ca, p, kvh, n0, n1, safe, col, g4);
+      process_chunk<HD>(cb, qf, o, m, l, pi, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
+      pi = pn;
+      n0 = nn0;
+      n1 = nn1;
+    }
   }
 
   if (it.kind == 1) {

@@ -185,7 +185,15 @@ void build_plan(const mx_batch* b, const mx_attn_shape* s, bool with_items, Plan
         p.items.push_back(it);
       }
   }
-  // decode splits
+  // the hardware hands workgroups to free slots in list order, so the longest
+  // items must not be left for the end: prefill tiles by the keys their last
+  // rows scan, then the decode splits by page count, each longest first
+  std::stable_sort(p.items.begin(), p.items.end(), [&](const AttnItem& a, const AttnItem& b) {
+    const ReqDev& ra = p.reqs[a.req];
+    const ReqDev& rb = p.reqs[b.req];
+    return ra.ctx_len + std::min(a.start + 64, ra.n_new) > rb.ctx_len + std::min(b.start + 64, rb.n_new);
+  });
+  const size_t first_decode = p.items.size();
   for (int r = 0; r < p.R; r++) {
     ReqDev& d = p.reqs[r];
     if (d.phase != MX_DECODE) continue;
@@ -210,6 +218,11 @@ void build_plan(const mx_batch* b, const mx_attn_shape* s, bool with_items, Plan
           p.items.push_back(it);
         }
   }
+  auto pages_of = [&](const AttnItem& it) {
+    return std::min(p.split_pages, p.reqs[it.req].n_pages - it.start);
+  };
+  std::stable_sort(p.items.begin() + first_decode, p.items.end(),
+                   [&](const AttnItem& a, const AttnItem& b) { return pages_of(a) > pages_of(b); });
 }
 
 // ------------------------------------------------------------------ workspace layout

@@ -171,3 +171,20 @@ def test_misaligned_pointers_rejected_before_device_work():
     st = mx.lib().mx_debug_gemm_config(64, 256, 256, 0x1000, 0x2000, 0x3006, None, 0, 0, 1,
                                        0x5000, 1 << 20, None)
     assert st == mx.MX_ERR_INVALID
+
+
+def test_one_hip_runtime_whatever_the_import_order():
+    """Importing the binding before torch must not leave two HIP runtimes in
+    the process (the library's and torch's): streams and pointers handed from
+    one to the other are invalid.  Checked in a fresh interpreter that imports
+    the binding first, then torch, then the input generator library."""
+    code = (
+        "import paper_2606_16264_amd, torch, workload.device as d; d.lib()\n"
+        "maps = open('/proc/self/maps').read().split('\\n')\n"
+        "paths = {l.split()[-1] for l in maps if 'libamdhip64' in l}\n"
+        "print(len(paths)); print(sorted(paths))\n")
+    out = subprocess.run([__import__("sys").executable, "-c", code], cwd=ROOT, capture_output=True,
+                         text=True, timeout=300)
+    assert out.returncode == 0, out.stderr[-2000:]
+    n = int(out.stdout.split()[0])
+    assert n == 1, out.stdout

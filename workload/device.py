@@ -19,6 +19,7 @@ def lib():
     if _lib is None:
         if not os.path.exists(_LIB):
             raise ImportError(f"{_LIB} is not built; run __graft_entry__.build()")
+        import torch  # noqa: F401  (torch's HIP runtime must be the one loaded first)
         L = ctypes.CDLL(_LIB)
         P, I32, I64, U64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64
         L.mxgen_fill_pool.argtypes = [P, P, I64, I32, I32, U64, U64, P, P]
