@@ -390,16 +390,22 @@ struct Plan {
 
 struct Shape {
   int BM, BN;
-  double tflops;  // sustained rate of one full tile stream on the whole chip (measured)
+  // time of one tile-unit on one CU: a + b * (K slice length), microseconds
+  // (least-squares fit over measured layer-shape GEMMs, all tile shapes and
+  // K splits; the main loop is bound by its global->LDS feed, so a unit's
+  // time grows with the bytes it streams)
+  double a_us, b_us_per_k;
 };
 // 256x256 and 128x256 run eight waves (2 per SIMD), the smaller shapes four.
-constexpr Shape kShapes[] = {{256, 256, 1150.0}, {128, 256, 950.0}, {128, 128, 800.0},
-                             {64, 128, 420.0}};
+constexpr Shape kShapes[] = {{256, 256, 3.471, 0.02443},
+                             {128, 256, 0.978, 0.01544},
+                             {128, 128, 0.615, 0.01019},
+                             {64, 128, 0.0, 0.00729}};
 constexpr int kNumShapes = 4;
 
 // Estimated time of each (tile shape, K split) choice: the busiest CU runs
-// ceil(units / 256) tile-units at the shape's per-CU rate; K splits add the
-// fp32 partial round trip; nothing beats streaming the weights once.
+// ceil(units / 256) tile-units; nothing beats streaming the operands from HBM
+// once; a K split adds the fp32 partial round trip and the reduce launch.
 Plan choose(int M, int N, int K) {
   const double cus = 256.0, hbm = 5.0e12;
   Plan best{kNumShapes - 1, 1};
@@ -410,13 +416,12 @@ Plan choose(int M, int N, int K) {
     for (int ks = 1; ks <= 8; ks *= 2) {
       if (K % (BK * ks) != 0 || K / ks < 4 * BK) break;
       if (ks > 1 && (double)ks * M * N > (double)kMaxSplitFloats) break;
-      const double units = tiles * ks;
-      const double rounds = std::ceil(units / cus);
-      const double unit_flops = 2.0 * BM * BN * (double)(K / ks);
-      const double t_mfma = rounds * unit_flops / (kShapes[c].tflops * 1e12 / cus);
-      const double t_mem = 2.0 * ((double)N * K + (double)M * K) / hbm;
-      const double t_red = ks > 1 ? ((double)ks * M * N * 4.0 * 2.0 + 2.0 * M * N) / hbm + 3e-6 : 0.0;
-      const double t = std::max(t_mfma, t_mem) + t_red;
+      const double rounds = std::ceil(tiles * ks / cus);
+      const double t_units = rounds * (kShapes[c].a_us + kShapes[c].b_us_per_k * (double)(K / ks));
+      const double t_mem = 2.0 * ((double)N * K + (double)M * K) / hbm * 1e6;
+      const double t_red =
+          ks > 1 ? 0.197 * ((double)ks * M * N * 8.0 + 2.0 * M * N) / 1e6 + 3.39 : 0.0;
+      const double t = std::max(t_units, t_mem) + t_red;
       if (t < best_t * 0.98) {
         best_t = t;
         best = {c, ks};
