@@ -42,6 +42,15 @@ def parse():
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB before timing (the "
                          "known-size reference that scales rocprofv3 byte counters)")
+    ap.add_argument("--chunk-sweep", nargs=2, type=int, metavar=("CHUNK", "N"),
+                    help="chunk-index sweep: the shape's decode batch plus one CHUNK-token "
+                         "prefill chunk continuing a prompt with k*CHUNK tokens cached, "
+                         "k = 0..N-1; prints one JSON line with latency per chunk index")
+    ap.add_argument("--predictor", type=int, metavar="N",
+                    help="time N random batches of the shape (random decode count and "
+                         "contexts, random chunk length and prior context), fit the linear "
+                         "latency model on the even-numbered ones and report its residuals "
+                         "on the odd-numbered ones; prints one JSON line")
     ap.add_argument("--summarize-stats", nargs=3, metavar=("STATS_CSV", "COMMAND", "OUT_MD"),
                     help="write a markdown summary of a rocprofv3 --stats kernel_stats.csv "
                          "(no GPU needed)")
@@ -182,13 +191,13 @@ def t_roof(parts):
 class Point:
     """Device state of one sweep point."""
 
-    def __init__(self, key, P, w_dev, packed, cfg):
+    def __init__(self, key, P, w_dev, packed, cfg, batch=None):
         import torch
         import paper_2606_16264_amd as mx
         import workload as wl
         import workload.device as wdev
         self.key, self.P, self.cfg = key, P, cfg
-        self.b = wl.make_batch(key, P)
+        self.b = batch if batch is not None else wl.make_batch(key, P)
         b = self.b
         self.c = mx.layer_cfg(cfg.hidden, cfg.ffn, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim,
                               b.pool_pages, cfg.rms_eps, cfg.rope_theta)
@@ -238,7 +247,7 @@ def time_fn(fn, steps, warmup):
     return mean, {"median": q(0.5), "p10": q(0.1), "p90": q(0.9)}
 
 
-def linear_fit(xs, ys):
+def linear_fit(xs, ys, slope_name="slope_us_per_prefill_token"):
     """Least-squares line y = a + b x with R^2 (the latency-vs-prefill curve)."""
     n = len(xs)
     if n < 2:
@@ -251,7 +260,7 @@ def linear_fit(xs, ys):
     a = my - b * mx_
     ss_tot = sum((y - my) ** 2 for y in ys)
     ss_res = sum((y - a - b * x) ** 2 for x, y in zip(xs, ys))
-    return {"intercept_us": round(a, 2), "slope_us_per_prefill_token": round(b, 5),
+    return {"intercept_us": round(a, 2), slope_name: round(b, 5),
             "r2": round(1.0 - ss_res / ss_tot, 5) if ss_tot > 0 else 1.0, "points": n}
 
 
@@ -327,6 +336,75 @@ def cpu_baseline(key, cfg, w_host, budget_s):
                       f"({n} rows, full layer, fp64), {dt:.1f} s"}
 
 
+def chunk_sweep(args, key, cfg, packed):
+    """Latency of the step as the same chunk moves later in its prompt: chunk
+    k attends over k * CHUNK cached tokens plus its own causal triangle, so its
+    attention work grows linearly with k while the projections stay fixed."""
+    import numpy as np
+    import workload as wl
+    C, N = args.chunk_sweep
+    b0 = wl.make_batch(key, 0)
+    dec_ctx = [int(c) for c in b0.ctx_len]
+    pts = []
+    for k in range(N):
+        b = wl.make_batch(key, C, decode_ctx=dec_ctx, prefill_lens=[C], prefill_ctx=[k * C])
+        pt = Point(key, C, None, packed, cfg, batch=b)
+        ms, dist = time_fn(pt.step, args.steps, args.warmup)
+        kern = kernel_breakdown(pt, max(5, args.steps // 2), 2)
+        rec = dict(k=k, ctx=k * C, T=b.T, us=round(ms * 1e3, 2), us_median=round(dist["median"] * 1e3, 2),
+                   attn_us=round(kern["paged_attn"]["us"], 2),
+                   prefill_attn_flops=pt.parts["attention"]["prefill_flops"],
+                   t_roof_us=round(t_roof(pt.parts) * 1e6, 2))
+        print(f"# chunk {k}: ctx {k * C}: {rec['us']} us (attention {rec['attn_us']} us)",
+              file=sys.stderr, flush=True)
+        pts.append(rec)
+        pt.release()
+    fit = linear_fit([p["k"] for p in pts], [p["us"] for p in pts], "slope_us_per_chunk_index")
+    fit_attn = linear_fit([p["k"] for p in pts], [p["attn_us"] for p in pts], "slope_us_per_chunk_index")
+    print(json.dumps({"chunk_sweep": {"workload": f"{cfg.name} layer ({key}): "
+                                                  f"{int(b0.R)} decodes + one {C}-token chunk",
+                                      "chunk": C, "points": pts,
+                                      "fit_us_per_chunk_index": fit,
+                                      "fit_attention_us_per_chunk_index": fit_attn}}))
+
+
+def predictor_fit(args, key, cfg, packed):
+    """Fit of the iteration-latency model to measured steps of random batches
+    (held-out residuals test how predictable the mixed iteration is)."""
+    import numpy as np
+    import workload as wl
+    from paper_2606_16264_amd.sched import LatencyModel, batch_features
+    rng = np.random.default_rng(2024)
+    max_dec = 256
+    feats, lat, recs = [], [], []
+    for i in range(args.predictor):
+        n_dec = int(rng.integers(8, max_dec + 1))
+        dec_ctx = [int(c) for c in rng.integers(64, 4097, size=n_dec)]
+        P = int(rng.choice([0, 0, 128, 512, 1024, 2048, 4096]))
+        pctx = int(rng.choice([0, 0, 1024, 4096])) if P else 0
+        b = wl.make_batch(key, P, decode_ctx=dec_ctx, prefill_lens=[P] if P else [],
+                          prefill_ctx=[pctx] if P else [])
+        pt = Point(key, P, None, packed, cfg, batch=b)
+        ms, _ = time_fn(pt.step, args.steps, args.warmup)
+        f = batch_features(b.n_new, b.ctx_len, b.phase == wl.DECODE)
+        feats.append(f)
+        lat.append(ms * 1e3)
+        recs.append(dict(n_decode=n_dec, P=P, prefill_ctx=pctx, T=int(b.T), us=round(ms * 1e3, 2)))
+        print(f"# sample {i}: {recs[-1]}", file=sys.stderr, flush=True)
+        pt.release()
+    train = list(range(0, len(lat), 2))
+    test = list(range(1, len(lat), 2))
+    m = LatencyModel.fit([feats[i] for i in train], [lat[i] for i in train])
+    held = m.residuals([feats[i] for i in test], [lat[i] for i in test])
+    m_all = LatencyModel.fit(feats, lat)
+    print(json.dumps({"latency_model": {
+        "workload": f"{cfg.name} layer ({key}): random decode sets (8-256 decodes, contexts "
+                    f"U[64, 4096]) with 0-4096-token chunks at prior context 0-4096",
+        "coef_us": m.as_dict(), "held_out_residuals": held,
+        "coef_us_all_samples": m_all.as_dict(),
+        "in_sample_residuals_all": m_all.residuals(feats, lat), "samples": recs}}))
+
+
 def main():
     args = parse()
     if args.summarize_stats:
@@ -365,6 +443,12 @@ def main():
         torch.cuda.synchronize()
         print(f"# copy calibration: {n} bytes device-to-device", file=sys.stderr, flush=True)
         del src, dst
+    if args.chunk_sweep:
+        chunk_sweep(args, key, cfg, packed)
+        return
+    if args.predictor:
+        predictor_fit(args, key, cfg, packed)
+        return
     print(f"# bench: {key} ({cfg.name}) sweep P={sweep}, steps={args.steps}, warmup={args.warmup}",
           file=sys.stderr, flush=True)
 

@@ -488,14 +488,17 @@ def test_layer_step_aligned_value_runs(cfg):
     assert changed_slots(got["v0"], got["v"], True) <= written
 
 
-@pytest.mark.parametrize("key,P", [("c2", 512), ("c2", 0), ("c3", 1024), ("c4", 2048)])
-def test_layer_step_sampled(key, P):
+@pytest.mark.parametrize("key,P,ctx", [("c2", 512, 0), ("c2", 0, 0), ("c3", 1024, 0), ("c4", 2048, 0),
+                                       ("c4", 2048, 6144)])
+def test_layer_step_sampled(key, P, ctx):
     """Full-size layer iteration (the benchmark's launch configuration),
     checked on sampled rows: the oracle evaluates the requests that own them,
-    cut after their last sampled row."""
-    say(f"case: layer step {key} P={P} (sampled rows)")
+    cut after their last sampled row.  ctx > 0: the P-token chunk continues a
+    prompt with ctx tokens already cached (a later chunk of a chunked prefill,
+    as in the chunk-index sweep)."""
+    say(f"case: layer step {key} P={P} ctx={ctx} (sampled rows)")
     cfg = wl.CONFIGS[key]
-    b = wl.make_batch(key, P)
+    b = wl.make_batch(key, P, prefill_lens=[P], prefill_ctx=[ctx]) if ctx else wl.make_batch(key, P)
     w = wl.make_weights(cfg, key)
     x = wl.make_x(cfg, b.T, key)
     seed = wl.kv_seed(key)
