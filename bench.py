@@ -51,6 +51,12 @@ def parse():
                          "contexts, random chunk length and prior context), fit the linear "
                          "latency model on the even-numbered ones and report its residuals "
                          "on the odd-numbered ones; prints one JSON line")
+    ap.add_argument("--simulate", metavar="MODEL_JSON",
+                    help="CPU only: SLO attainment of colocated, disaggregated and SLO-aware "
+                         "multiplexing serving over a sweep of arrival rates, simulated with the "
+                         "latency model that `--predictor` printed (MODEL_JSON); prints one JSON line")
+    ap.add_argument("--rates", type=float, nargs="+", default=[4, 8, 16, 24, 32, 48])
+    ap.add_argument("--requests", type=int, default=800)
     ap.add_argument("--summarize-stats", nargs=3, metavar=("STATS_CSV", "COMMAND", "OUT_MD"),
                     help="write a markdown summary of a rocprofv3 --stats kernel_stats.csv "
                          "(no GPU needed)")
@@ -412,6 +418,21 @@ def main():
         return
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic)
+        return
+    if args.simulate:
+        from paper_2606_16264_amd.sched import LatencyModel, compare
+        import workload as wl
+        rec = json.load(open(args.simulate))["latency_model"]
+        cfg = wl.CONFIGS[args.config]
+        noise = rec["held_out_residuals"]["median_abs_rel"]
+        res = compare(LatencyModel.from_dict(rec["coef_us"]), args.rates, n=args.requests,
+                      kv_bytes_per_token=32.0 * cfg.kv_bytes_per_token, noise=noise)
+        res.update(latency_model=rec["workload"], noise=noise, layers=32,
+                   workers="4 (2 prefill + 2 decode/multiplexing; colocated: 4 mixed)",
+                   requests=args.requests,
+                   arrivals="Poisson; prompts lognormal(median 2048, sigma 1) in [32, 16384]; "
+                            "outputs lognormal(median 128, sigma 0.8) in [1, 1024]")
+        print(json.dumps(res))
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1 "

@@ -73,3 +73,114 @@ def test_fit_with_noise_has_small_residuals():
 def test_fit_needs_enough_samples():
     with pytest.raises(ValueError):
         LatencyModel.fit([np.ones(5)] * 3, [1.0, 2.0, 3.0])
+
+
+# ---------------------------------------------------------------- SLO and slack
+from paper_2606_16264_amd.sched import (SLO, Cluster, Request, Simulator, admits_chunk,  # noqa: E402
+                                        attainment, synthetic_requests)
+
+
+def done_request(rid, arrival, first, decode_time, output):
+    r = Request(rid, arrival, 10, output)
+    r.first_token, r.decode_time = first, decode_time
+    return r
+
+
+def test_attainment_eq1_to_3():
+    slo = SLO(ttft=100.0, tpot=10.0)
+    reqs = [done_request(0, 0.0, 100.0, 100.0, 10),    # TTFT = 100 ok, TPOT = 10 ok
+            done_request(1, 5.0, 106.0, 50.0, 10),     # TTFT 101 misses
+            done_request(2, 0.0, 50.0, 101.0, 10),     # TPOT 10.1 misses
+            done_request(3, 0.0, 20.0, 90.0, 10)]      # both ok
+    a = attainment(reqs, slo)
+    assert a["attainment"] == 0.5
+    assert a["ttft_attainment"] == 0.75 and a["tpot_attainment"] == 0.75
+
+
+def test_slack_accumulates_per_decode_step():
+    r = Request(0, 0.0, 10, 20)
+    for t in (60.0, 60.0, 80.0):
+        r.decode_time += t
+        r.decode_steps += 1
+    assert r.slack(100.0) == 300.0 - 200.0
+
+
+def test_admission_fig7():
+    """A decode iteration of 60 against a TPOT SLO of 100 leaves 40 of slack per
+    token; a prefill that makes the iteration 160 fits once the slack reaches
+    60, i.e. it is piggybacked on the iteration producing the third token, and
+    the decode request's running TPOT stays within the SLO."""
+    slo = SLO(ttft=1e9, tpot=100.0)
+    r0 = Request(0, 0.0, 10, 20)
+    admitted_at = None
+    for step in range(4):
+        if admitted_at is None and admits_chunk([r0], 60.0, 160.0, slo):
+            admitted_at = step
+            t = 160.0
+        else:
+            t = 60.0
+        r0.decode_time += t
+        r0.decode_steps += 1
+        assert r0.decode_time <= r0.decode_steps * slo.tpot
+    assert admitted_at == 2   # steps 0, 1 produce tokens 2 and 3; admission at the third decode step
+
+
+def test_admission_gates():
+    slo = SLO(ttft=1e9, tpot=100.0, busy_fraction=0.9, hbm_watermark=0.8)
+    r = Request(0, 0.0, 10, 20)
+    r.decode_steps, r.decode_time = 10, 100.0          # lots of slack
+    assert admits_chunk([r], 50.0, 150.0, slo)
+    assert not admits_chunk([r], 90.0, 150.0, slo)    # decode batch alone at 90% of the SLO
+    assert not admits_chunk([r], 50.0, 150.0, slo, kv_use=81.0, kv_capacity=100.0)
+    fresh = Request(1, 0.0, 10, 20)                    # no slack yet: one SLO of budget
+    assert admits_chunk([fresh], 50.0, 100.0, slo) and not admits_chunk([fresh], 50.0, 100.5, slo)
+
+
+# ---------------------------------------------------------------- simulator
+TOY = LatencyModel(coef=np.array([50.0, 10.0, 0.0, 0.0, 0.0]))   # 50 + 10 per token, per layer
+
+
+def test_simulator_fig7_scenario():
+    """One prefill worker and one multiplexing worker.  R0 is prefilled and
+    then decodes on the multiplexing worker at 60 per token (TPOT SLO 100); a
+    long prompt occupies the prefill worker; a short prompt that the prefill
+    worker cannot serve within its TTFT SLO waits until R0 has built up the
+    slack for it, and is then prefilled on the multiplexing worker without
+    pushing R0 over its TPOT SLO."""
+    slo = SLO(ttft=1000.0, tpot=100.0)
+    cl = Cluster("multiplexing", workers=2, prefill_workers=1, chunk=64, layers=1,
+                 kv_bytes_per_token=1.0, link_bytes_per_us=1e12, kv_capacity=1e12)
+    reqs = [Request(0, 0.0, 5, 10), Request(1, 1.0, 1000, 2), Request(2, 150.0, 10, 2)]
+    sim = Simulator(TOY, cl, slo, trace=True)
+    res = sim.run(reqs)
+    admits = [(t, w, rid) for t, w, kind, rid in sim.log if kind == "admit"]
+    assert admits == [(pytest.approx(220.0), 1, 2)]
+    r0 = next(r for r in sim.done if r.rid == 0)
+    assert r0.tpot <= slo.tpot
+    r2 = next(r for r in sim.done if r.rid == 2)
+    assert r2.ttft <= slo.ttft
+    assert res["requests"] == 3
+
+
+@pytest.mark.parametrize("policy", ["colocated", "disaggregated", "multiplexing"])
+def test_simulator_conserves_requests(policy):
+    reqs = synthetic_requests(rate_per_s=20.0, n=120, seed=5, prompt_median=512, output_median=32)
+    slo = SLO(ttft=2e6, tpot=4e4)
+    model = LatencyModel(coef=np.array([250.0, 0.5, 1.5e-3, 7e-5, 1.0]))
+    sim = Simulator(model, Cluster(policy, workers=4, prefill_workers=2, chunk=512), slo, seed=1)
+    res = sim.run(reqs)
+    assert res["requests"] == len(reqs)
+    for r in sim.done:
+        assert r.generated == r.output and r.first_token >= r.arrival
+        assert r.decode_steps == r.output - 1 and r.finish >= r.first_token
+
+
+def test_light_load_meets_every_slo():
+    model = LatencyModel(coef=np.array([250.0, 0.5, 1.5e-3, 7e-5, 1.0]))
+    from paper_2606_16264_amd.sched import light_load_slo
+    slo = light_load_slo(model, 32, 512, 512)
+    reqs = synthetic_requests(rate_per_s=0.2, n=30, seed=6, prompt_median=512, output_median=16,
+                              max_prompt=2048)
+    for policy in ("colocated", "disaggregated", "multiplexing"):
+        res = Simulator(model, Cluster(policy, workers=4, prefill_workers=2), slo).run(reqs)
+        assert res["attainment"] == 1.0, (policy, res)
