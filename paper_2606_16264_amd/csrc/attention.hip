@@ -18,7 +18,8 @@
 //                 partials (unnormalised O, running max, running sum) for the
 //                 merge kernel.
 //   prefill item: one q head, 64 query rows of a prefill chunk (16 per wave),
-//                 causal over the cached prefix plus the chunk.
+//                 causal over the cached prefix plus the chunk; the four waves
+//                 share each 32-key chunk through LDS (loaded once per tile).
 //
 // Masking is select-based: slots at or past the request's length are never
 // multiplied into a sum, so stale or NaN-filled slots cannot leak.
@@ -143,8 +144,33 @@ __device__ __forceinline__ void process_chunk(const Chunk<HD>& c, const bf16x8 (
   }
 }
 
+// Prefill tiles share every 32-key chunk through LDS: the four waves load it
+// once, a quarter each (waves 0 and 1 the keys of the chunk's two pages, waves
+// 2 and 3 their values), and every wave reads its matrix-core fragments from
+// there.  Keys are stored [32][HD] with the 16-byte chunk c of key row j at
+// c ^ ksw(j); values [HD][32 keys] with the 16-byte chunk c of dim row d at
+// c ^ ((d >> 2) & 3).  Both make the fragment reads (16 key rows, or 16 dim
+// rows, at one logical chunk) and the stores hit distinct bank groups.
+template <int HD>
+__device__ __forceinline__ int ksw(int key) {
+  if constexpr (HD == 128) return (key & 3) | ((key >> 3) << 2);
+  else return ((key >> 1) & 1) | ((key >> 3) << 1);
+}
+template <int HD>
+struct SharedChunk {
+  static constexpr int KBYTES = 32 * HD * 2;
+  static constexpr int BYTES = 2 * KBYTES;  // keys + values
+};
+template <int HD>
+constexpr int smem_bytes() {
+  constexpr int ring = 2 * SharedChunk<HD>::BYTES;
+  constexpr int combine = (4 * 16 * (HD + 4) + 2 * 4 * 16) * 4;
+  return ring > combine ? ring : combine;
+}
+
 template <int HD>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void paged_attn_kernel(AttnParams p) {
+  __shared__ __attribute__((aligned(16))) char smem[smem_bytes<HD>()];
   const AttnItem it = p.items[blockIdx.x];
   const ReqDev rq = p.reqs[it.req];
   const int lane = threadIdx.x & 63;
@@ -197,6 +223,99 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
     }
   }
 
+  if (it.kind == 1) {
+    // the tile's last row bounds the pages every wave helps to load
+    const int tile_last = min(it.start + 63, rq.n_new - 1);
+    const int item_pages = (rq.ctx_len + tile_last) / 16 + 1;
+    const int n_chunks = (item_pages + 1) / 2;
+    const int wave_chunks = (page_end + 1) / 2;  // 0 for a wave without valid rows
+    const int safe = p.pages[rq.page_start];
+    auto pid = [&](int pi) -> int {
+      const int v = p.pages[rq.page_start + min(pi, rq.n_pages - 1)];
+      return pi < item_pages ? v : -1;
+    };
+    constexpr int KB = SharedChunk<HD>::KBYTES, CB = SharedChunk<HD>::BYTES;
+    constexpr int NLD = HD / 32;  // 16-byte loads per lane for a quarter chunk
+    u32x4 st[NLD];
+    // waves 0 / 1: keys of the chunk's first / second page; 2 / 3: values
+    auto gload = [&](int pid0, int pid1) {
+      const int pg0 = (wave & 1) ? pid1 : pid0;
+      const int pg = pg0 >= 0 ? pg0 : safe;  // past the end: masked, like the decode path
+      const uint16_t* base = (wave < 2 ? p.k_pool : p.v_pool) + ((int64_t)pg * p.nkv + kvh) * (16 * HD);
+#pragma unroll
+      for (int i = 0; i < NLD; i++) st[i] = *reinterpret_cast<const u32x4*>(base + (i * 64 + lane) * 8);
+    };
+    auto swrite = [&](char* slot) {
+#pragma unroll
+      for (int i = 0; i < NLD; i++) {
+        const int c = i * 64 + lane;
+        char* dst;
+        if (wave < 2) {
+          const int key = 16 * (wave & 1) + c / (HD / 8), lc = c % (HD / 8);
+          dst = slot + key * (HD * 2) + ((lc ^ ksw<HD>(key)) << 4);
+        } else {
+          const int d = c >> 1, lc = 2 * (wave & 1) + (c & 1);
+          dst = slot + KB + d * 64 + ((lc ^ ((d >> 2) & 3)) << 4);
+        }
+        *reinterpret_cast<u32x4*>(dst) = st[i];
+      }
+    };
+    auto sread = [&](const char* slot, Chunk<HD>& c) {
+#pragma unroll
+      for (int b = 0; b < 2; b++)
+#pragma unroll
+        for (int ds = 0; ds < HD / 32; ds++) {
+          const int key = 16 * (col >> 3) + 8 * ((col >> 2) & 1) + (col & 3) + 4 * b;
+          c.k[b][ds] = *reinterpret_cast<const u32x4*>(slot + key * (HD * 2) +
+                                                       (((4 * ds + g4) ^ ksw<HD>(key)) << 4));
+        }
+#pragma unroll
+      for (int db = 0; db < HD / 16; db++) {
+        const int d = 16 * db + col;
+        c.v[db] = *reinterpret_cast<const u32x4*>(slot + KB + d * 64 + ((g4 ^ ((d >> 2) & 3)) << 4));
+      }
+    };
+    // one barrier per chunk: chunk kt + 1 is loaded into registers while chunk
+    // kt is processed, and stored into the other slot (read by everyone in the
+    // previous iteration, before its barrier) once the processing is done
+    int n0 = pid(2), n1 = pid(3);
+    gload(pid(0), pid(1));
+    swrite(smem);
+    __syncthreads();
+    for (int kt = 0; kt < n_chunks; kt++) {
+      const bool more = kt + 1 < n_chunks;
+      int nn0 = -1, nn1 = -1;
+      if (more) {
+        gload(n0, n1);
+        nn0 = pid(2 * kt + 4);
+        nn1 = pid(2 * kt + 5);
+      }
+      if (kt < wave_chunks) {
+        Chunk<HD> c;
+        sread(smem + (kt & 1) * CB, c);
+        process_chunk<HD>(c, qf, o, m, l, 2 * kt, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
+      }
+      if (more) {
+        swrite(smem + ((kt + 1) & 1) * CB);
+        n0 = nn0;
+        n1 = nn1;
+      }
+      __syncthreads();
+    }
+    if (row_valid) {
+      const float inv = 1.f / l;
+      uint16_t* op = p.out + qtok * p.out_tok_stride + (int64_t)qhead * HD + 4 * g4;
+#pragma unroll
+      for (int db = 0; db < HD / 16; db++) {
+        u32x2 w;
+        w[0] = pack_bf16x2(o[db][0] * inv, o[db][1] * inv);
+        w[1] = pack_bf16x2(o[db][2] * inv, o[db][3] * inv);
+        *reinterpret_cast<u32x2*>(op + db * 16) = w;
+      }
+    }
+    return;
+  }
+
   // Two chunk buffers used in turn: the loads of the next chunk are in flight
   // while the current one is processed.  The loop is unrolled by two so that
   // no buffer is ever copied (a register copy of a buffer whose loads are in
@@ -241,24 +360,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
     }
   }
 
-  if (it.kind == 1) {
-    if (row_valid) {
-      const float inv = 1.f / l;
-      uint16_t* op = p.out + qtok * p.out_tok_stride + (int64_t)qhead * HD + 4 * g4;
-#pragma unroll
-      for (int db = 0; db < HD / 16; db++) {
-        u32x2 w;
-        w[0] = pack_bf16x2(o[db][0] * inv, o[db][1] * inv);
-        w[1] = pack_bf16x2(o[db][2] * inv, o[db][3] * inv);
-        *reinterpret_cast<u32x2*>(op + db * 16) = w;
-      }
-    }
-    return;
-  }
-
   // decode: combine the four waves' partial softmax states through LDS
-  __shared__ float s_o[4][16][HD + 4];
-  __shared__ float s_m[4][16], s_l[4][16];
+  float(*s_o)[16][HD + 4] = reinterpret_cast<float(*)[16][HD + 4]>(smem);
+  float(*s_m)[16] = reinterpret_cast<float(*)[16]>(smem + 4 * 16 * (HD + 4) * 4);
+  float(*s_l)[16] = reinterpret_cast<float(*)[16]>(smem + 4 * 16 * (HD + 4) * 4 + 4 * 16 * 4);
 #pragma unroll
   for (int db = 0; db < HD / 16; db++)
 #pragma unroll
