@@ -75,7 +75,7 @@ def summarize_stats(csv_path, command, out_md):
     total = sum(float(r["TotalDurationNs"]) for r in rows)
     lines = ["# Kernel trace statistics: the layer step on the Llama-7B-shaped layer", "",
              "Workload: hidden 4096, 32 x 128 MHA, FFN 11008; 64 decodes (contexts uniform in "
-             "[512, 2048]) with 0 and with 512 mixed prefill tokens (the bench sweep), including "
+             "[512, 2048]) with 512 mixed prefill tokens (the benchmark point, T = 576), including "
              "setup (weight packing, pool fill) and the per-kernel timing steps.", "",
              "Command (one MI355X):", "", "```", command, "```", "",
              "Durations in microseconds (rocprofv3 kernel trace).  gemm_kernel<BM, BN, WM, WN, "
@@ -337,9 +337,16 @@ def cpu_baseline(key, cfg, w_host, budget_s):
         n_dec = int(min(len(dec), max(n_dec + 1, round(n_dec * grow))))
         n_pre = int(max(n_pre + 1, round(n_pre * grow)))
         dt, n = run(n_dec, n_pre)
-    return {"value": n / dt, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
+    # the whole batch fits the budget: repeat it until the budget is spent
+    reps, total = 1, dt
+    while total < budget_s / 2:
+        dt2, _ = run(n_dec, n_pre)
+        total += dt2
+        reps += 1
+    return {"value": n * reps / total, "unit": "tokens/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
             "sample": f"{n_dec} decode requests + first {n_pre} tokens of the prefill chunk "
-                      f"({n} rows, full layer, fp64), {dt:.1f} s"}
+                      f"({n} rows, full layer, fp64), {reps} evaluation(s) in {total:.1f} s"}
 
 
 def chunk_sweep(args, key, cfg, packed):
