@@ -76,7 +76,7 @@ __device__ __forceinline__ void load_chunk(Chunk<HD>& c, const AttnParams& p, in
 
 // One 32-key step of the online softmax for this lane's query row.  Lane group
 // g4 owns keys pi0 * 16 + 8 * g4 + i' (i' = 4 b + i for score block b, row i).
-template <int HD>
+template <int HD, bool MASK = true>
 __device__ __forceinline__ void process_chunk(const Chunk<HD>& c, const bf16x8 (&qf)[HD / 32],
                                               f32x4 (&o)[HD / 16], float& m, float& l,
                                               int pi0, int page_end, int row_pos, int kv_len,
@@ -98,7 +98,7 @@ __device__ __forceinline__ void process_chunk(const Chunk<HD>& c, const bf16x8 (
     for (int i = 0; i < 4; i++) {
       const int j = j0 + 4 * b + i;
       const float x = s[b][i] * scale_log2;
-      sv[b][i] = (pvalid && j <= row_pos) ? x : kNegBig;
+      sv[b][i] = (!MASK || (pvalid && j <= row_pos)) ? x : kNegBig;
       mx = fmaxf(mx, sv[b][i]);
     }
   mx = fmaxf(mx, __shfl_xor(mx, 16));
@@ -136,12 +136,21 @@ __device__ __forceinline__ void process_chunk(const Chunk<HD>& c, const bf16x8 (
   }
 #pragma unroll
   for (int db = 0; db < HD / 16; db++) {
-    u32x4 va;
+    u32x4 va = c.v[db];
+    if constexpr (MASK) {
 #pragma unroll
-    for (int h = 0; h < 4; h++) va[h] = c.v[db][h] & keep[h];
+      for (int h = 0; h < 4; h++) va[h] &= keep[h];
+    }
     o[db] = o[db] * alpha;
     o[db] = mfma16(as_bf16x8(va), pb, o[db]);
   }
+}
+
+// Keys pi0 * 16 .. pi0 * 16 + 31 all count for every row of the wave (both
+// pages inside the range, and the chunk's last key at or before the wave's
+// first row position, which is below kv_len): no mask is needed.
+__device__ __forceinline__ bool chunk_interior(int pi0, int page_end, int first_row_pos) {
+  return pi0 + 1 < page_end && pi0 * 16 + 31 <= first_row_pos;
 }
 
 // Prefill tiles share every 32-key chunk through LDS: the four waves load it
@@ -229,6 +238,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
     const int item_pages = (rq.ctx_len + tile_last) / 16 + 1;
     const int n_chunks = (item_pages + 1) / 2;
     const int wave_chunks = (page_end + 1) / 2;  // 0 for a wave without valid rows
+    const int wave_first_pos = rq.ctx_len + it.start + 16 * wave;  // the wave's first row
     const int safe = p.pages[rq.page_start];
     auto pid = [&](int pi) -> int {
       const int v = p.pages[rq.page_start + min(pi, rq.n_pages - 1)];
@@ -293,7 +303,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
       if (kt < wave_chunks) {
         Chunk<HD> c;
         sread(smem + (kt & 1) * CB, c);
-        process_chunk<HD>(c, qf, o, m, l, 2 * kt, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
+        if (chunk_interior(2 * kt, page_end, wave_first_pos))
+          process_chunk<HD, false>(c, qf, o, m, l, 2 * kt, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
+        else
+          process_chunk<HD>(c, qf, o, m, l, 2 * kt, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
       }
       if (more) {
         swrite(smem + ((kt + 1) & 1) * CB);
@@ -328,6 +341,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
     const int v = p.pages[rq.page_start + min(pi, rq.n_pages - 1)];
     return pi < page_end ? v : -1;
   };
+  auto proc = [&](const Chunk<HD>& c, int pi0) {
+    if (chunk_interior(pi0, page_end, row_pos))
+      process_chunk<HD, false>(c, qf, o, m, l, pi0, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
+    else
+      process_chunk<HD>(c, qf, o, m, l, pi0, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
+  };
   Chunk<HD> ca, cb;
   int pi = chunk_first;
   if (pi < page_end) {
@@ -336,24 +355,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
     while (true) {
       int pn = pi + chunk_step;
       if (pn >= page_end) {
-        process_chunk<HD>(ca, qf, o, m, l, pi, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
+        proc(ca, pi);
         break;
       }
       int nn0 = pid(pn + chunk_step), nn1 = pid(pn + chunk_step + 1);
       load_chunk<HD>(cb, p, kvh, n0, n1, safe, col, g4);
-      process_chunk<HD>(ca, qf, o, m, l, pi, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
+      proc(ca, pi);
       pi = pn;
       n0 = nn0;
       n1 = nn1;
       pn = pi + chunk_step;
       if (pn >= page_end) {
-        process_chunk<HD>(cb, qf, o, m, l, pi, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
+        proc(cb, pi);
         break;
       }
       nn0 = pid(pn + chunk_step);
       nn1 = pid(pn + chunk_step + 1);
       load_chunk<HD>(ca, p, kvh, n0, n1, safe, col, g4);
-      process_chunk<HD>(cb, qf, o, m, l, pi, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
+      proc(cb, pi);
       pi = pn;
       n0 = nn0;
       n1 = nn1;
