@@ -16,7 +16,9 @@ from typing import Optional, Sequence
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libmx.so")
+# MX_LIB_PATH selects another build of the same library (the host-sanitized
+# one); by default the in-tree libmx.so.
+LIB_PATH = os.environ.get("MX_LIB_PATH") or os.path.join(_HERE, "libmx.so")
 
 MX_OK, MX_ERR_INVALID, MX_ERR_NO_SPACE, MX_ERR_TOO_LARGE, MX_ERR_UNSUPPORTED, MX_ERR_NULL, \
     MX_ERR_HIP = range(7)

@@ -19,9 +19,14 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17", "-fvisibility=hi
          "-Wno-unused-command-line-argument", "-I", os.path.join(ROOT, "include"), "-I", CSRC]
 
 
-def _compile(src: str, verbose: bool) -> str:
-    obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC] + FLAGS + ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+# Host-side AddressSanitizer (the host code only: the flags reach the host
+# compilation pass alone, device code is built as usual).
+ASAN_HOST = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fno-omit-frame-pointer"]
+
+
+def _compile(src: str, verbose: bool, build_dir: str = BUILD, extra=()) -> str:
+    obj = os.path.join(build_dir, os.path.splitext(src)[0] + ".o")
+    cmd = [HIPCC] + FLAGS + list(extra) + ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -44,6 +49,25 @@ def build(verbose: bool = False) -> str:
     subprocess.run(cmd, check=True)
     os.replace(tmp, LIB)
     return LIB
+
+
+def build_asan_host(verbose: bool = False) -> str:
+    """A copy of the library whose host code (argument checks, planning,
+    metadata packing) runs under AddressSanitizer: _build/asan/libmx.so.
+    Load it with MX_LIB_PATH set to that file and the sanitizer runtime
+    preloaded (see the test notes)."""
+    build_dir = os.path.join(ROOT, "_build", "asan")
+    os.makedirs(build_dir, exist_ok=True)
+    with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
+        objs = list(ex.map(lambda s: _compile(s, verbose, build_dir,
+                                              ASAN_HOST if s.endswith(".cpp") else ()), SOURCES))
+    out = os.path.join(build_dir, "libmx.so")
+    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-Xarch_host",
+           "-fsanitize=address", "-shared-libasan", "-o", out] + objs
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    return out
 
 
 def device_asm(src: str, out: str) -> str:
@@ -71,5 +95,8 @@ def build_workload_gen(verbose: bool = False) -> str:
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
-    print(build_workload_gen(verbose="-v" in sys.argv))
+    if "--asan-host" in sys.argv:
+        print(build_asan_host(verbose="-v" in sys.argv))
+    else:
+        print(build(verbose="-v" in sys.argv))
+        print(build_workload_gen(verbose="-v" in sys.argv))
