@@ -31,8 +31,8 @@ MFMA_BF16_PEAK = 2.5e15  # flop/s, dense bf16
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=int(os.environ.get("WORLD_SIZE", "1")))
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="c2", help="layer shape c1..c5")
     ap.add_argument("--prefill", type=int, nargs="*", default=None,
                     help="mixed prefill tokens per point (default: the shape's sweep)")
@@ -228,15 +228,23 @@ class Point:
 
 def time_fn(fn, steps, warmup):
     """Mean ms per step over `steps` back-to-back steps (events bracketing the
-    whole run), plus the per-step distribution from events around each step."""
+    whole run), plus the per-step distribution from events around each step,
+    and the host's own time to plan and enqueue one step (taken over the first
+    calls after a synchronisation, before the library's ring of eight staging
+    buffers can make the host wait for the device)."""
+    import time
     import torch
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    n_host, host_ms = min(steps, 6), 0.0
     s.record()
-    for _ in range(steps):
+    t0 = time.perf_counter()
+    for i in range(steps):
         fn()
+        if i == n_host - 1:
+            host_ms = (time.perf_counter() - t0) * 1e3 / n_host
     e.record()
     torch.cuda.synchronize()
     mean = s.elapsed_time(e) / steps
@@ -250,7 +258,7 @@ def time_fn(fn, steps, warmup):
 
     def q(f):
         return per[min(len(per) - 1, int(round(f * (len(per) - 1))))]
-    return mean, {"median": q(0.5), "p10": q(0.1), "p90": q(0.9)}
+    return mean, {"median": q(0.5), "p10": q(0.1), "p90": q(0.9), "host": host_ms}
 
 
 def linear_fit(xs, ys, slope_name="slope_us_per_prefill_token"):
@@ -490,6 +498,7 @@ def main():
         us = ms * 1e3
         roof = t_roof(pt.parts) * 1e6
         rec = dict(P=int(P), T=pt.b.T, R=pt.b.R, us=round(us, 2),
+                   host_us=round(dist["host"] * 1e3, 1),
                    us_median=round(dist["median"] * 1e3, 2), us_p10=round(dist["p10"] * 1e3, 2),
                    us_p90=round(dist["p90"] * 1e3, 2),
                    tokens_per_s=pt.b.T / (us * 1e-6),
@@ -497,7 +506,8 @@ def main():
                    t_roof_us=round(roof, 2), roof_frac=roof / us)
         print(f"# P={P}: {us:.1f} us/step (median {rec['us_median']}, p10 {rec['us_p10']}, "
               f"p90 {rec['us_p90']}), {rec['tokens_per_s']:.0f} tok/s, "
-              f"roofline {roof:.1f} us ({rec['roof_frac']:.2f})", file=sys.stderr, flush=True)
+              f"roofline {roof:.1f} us ({rec['roof_frac']:.2f}), host {rec['host_us']} us/step",
+              file=sys.stderr, flush=True)
         if args.kernels:
             kernels = kernel_breakdown(pt, max(5, args.steps // 2), 2)
             rec["kernel_us"] = {k: round(v["us"], 2) for k, v in kernels.items()}

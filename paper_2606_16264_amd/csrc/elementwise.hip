@@ -1,5 +1,7 @@
 // elementwise.hip -- the memory-bound kernels of the layer step on gfx950:
 // token map + rotary table, RMSNorm, KV append, gather, weight packing.
+#include <algorithm>
+
 #include "mx_device.h"
 #include "mx_kernels.h"
 
@@ -163,7 +165,27 @@ __global__ __launch_bounds__(256) void interleave_kernel(const uint16_t* __restr
   for (int c = threadIdx.x; c < H / 8; c += blockDim.x) o[c] = s[c];
 }
 
+// Metadata upload: 16-byte words from the pinned host staging buffer (read
+// through its device mapping) into the workspace.
+__global__ __launch_bounds__(256) void upload_kernel(const u32x4* __restrict__ src,
+                                                     u32x4* __restrict__ dst, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    dst[i] = src[i];
+}
+
 }  // namespace
+
+hipError_t launch_upload(const void* host_mapped, void* dst, size_t bytes, hipStream_t stream) {
+  if (bytes == 0) return hipSuccess;
+  if (bytes % 16 != 0 || (size_t)host_mapped % 16 != 0 || (size_t)dst % 16 != 0)
+    return hipErrorInvalidValue;
+  const int64_t n = (int64_t)(bytes / 16);
+  const int blocks = (int)std::min<int64_t>((n + 255) / 256, 1024);
+  upload_kernel<<<blocks, 256, 0, stream>>>(static_cast<const u32x4*>(host_mapped),
+                                            static_cast<u32x4*>(dst), n);
+  return hipGetLastError();
+}
 
 hipError_t launch_token_map(const ReqDev* reqs, int R, int T, const int32_t* pages,
                             int32_t* tok_req, int32_t* tok_pos, int64_t* tok_slot,

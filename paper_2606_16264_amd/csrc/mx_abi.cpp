@@ -288,7 +288,8 @@ struct DeviceState {
   std::mutex mu;
   bool init = false;
   static constexpr int kRing = 8;
-  void* buf[kRing] = {};
+  void* buf[kRing] = {};   // pinned host staging buffers
+  void* dbuf[kRing] = {};  // the same buffers as the device reads them
   size_t cap[kRing] = {};
   hipEvent_t ev[kRing] = {};
   bool used[kRing] = {};
@@ -328,8 +329,9 @@ mx_status device_state(DeviceState** out) {
 }
 
 // Packs the plan's metadata into a pinned staging buffer and enqueues its copy
-// into the workspace.  A staging slot is reused only after its previous copy
-// has completed.
+// into the workspace (a kernel that reads the buffer through its device
+// mapping).  A staging slot is rewritten or freed only after the event
+// recorded behind its previous copy has completed.
 mx_status upload_meta(const Plan& p, const Layout& L, const mx_attn_shape* s, float theta,
                       void* ws, hipStream_t stream) {
   DeviceState* ds;
@@ -345,10 +347,17 @@ mx_status upload_meta(const Plan& p, const Layout& L, const mx_attn_shape* s, fl
   }
   if (ds->cap[i] < L.meta_end) {
     if (ds->buf[i]) hipHostFree(ds->buf[i]);
-    ds->buf[i] = nullptr;
+    ds->buf[i] = ds->dbuf[i] = nullptr;
     const size_t cap = std::max<size_t>(L.meta_end * 2, 1 << 16);
-    e = hipHostMalloc(&ds->buf[i], cap, hipHostMallocDefault);
-    if (e != hipSuccess) { ds->cap[i] = 0; return hip_fail(e, "hipHostMalloc"); }
+    e = hipHostMalloc(&ds->buf[i], cap, hipHostMallocMapped);
+    if (e != hipSuccess) { ds->buf[i] = nullptr; ds->cap[i] = 0; return hip_fail(e, "hipHostMalloc"); }
+    e = hipHostGetDevicePointer(&ds->dbuf[i], ds->buf[i], 0);
+    if (e != hipSuccess) {
+      hipHostFree(ds->buf[i]);
+      ds->buf[i] = ds->dbuf[i] = nullptr;
+      ds->cap[i] = 0;
+      return hip_fail(e, "hipHostGetDevicePointer");
+    }
     ds->cap[i] = cap;
   }
   char* h = (char*)ds->buf[i];
@@ -360,8 +369,8 @@ mx_status upload_meta(const Plan& p, const Layout& L, const mx_attn_shape* s, fl
   double* inv = (double*)(h + L.inv_freq);
   const int d = s->head_dim;
   for (int k = 0; k < d / 2; k++) inv[k] = std::pow((double)theta, -2.0 * k / d);
-  e = hipMemcpyAsync(ws, h, L.meta_end, hipMemcpyHostToDevice, stream);
-  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (metadata)");
+  e = launch_upload(ds->dbuf[i], ws, L.meta_end, stream);
+  if (e != hipSuccess) return hip_fail(e, "metadata upload launch");
   e = hipEventRecord(ds->ev[i], stream);
   if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
   ds->used[i] = true;

@@ -27,6 +27,12 @@ struct AttnParams {
 hipError_t launch_paged_attn(const AttnParams& p, int n_items, const MergeItem* merges,
                              int n_merges, int head_dim, hipStream_t stream);
 
+// Copies `bytes` (a multiple of 16, both ends 16-byte aligned) from pinned host
+// memory, given by its device mapping, into device memory.  A kernel on the
+// caller's stream rather than a copy-engine transfer, so that the first kernel
+// of the step does not wait on a cross-engine signal.
+hipError_t launch_upload(const void* host_mapped, void* dst, size_t bytes, hipStream_t stream);
+
 // Plan kernel: tok_req/tok_pos/tok_slot of every new token from the request
 // table and, when rope_cs is given, the RoPE (cos, sin) table [T][d/2] of the
 // tokens' positions (angle formed and reduced in double precision).
