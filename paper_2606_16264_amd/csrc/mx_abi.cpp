@@ -69,6 +69,9 @@ mx_status validate_batch(const mx_batch* b, const mx_attn_shape* s, int64_t* T_o
   if (b->num_reqs > 0 && !b->reqs) return fail(MX_ERR_NULL, "reqs is NULL");
   int64_t T = 0;
   std::vector<int64_t> slots;
+  for (int r = 0; r < b->num_reqs; r++) T += std::max(b->reqs[r].n_new, 0);
+  slots.reserve((size_t)std::min<int64_t>(T, INT32_MAX / 2));
+  T = 0;
   for (int r = 0; r < b->num_reqs; r++) {
     const mx_request& q = b->reqs[r];
     if (q.phase != MX_PREFILL && q.phase != MX_DECODE)
@@ -161,11 +164,14 @@ void build_plan(const mx_batch* b, const mx_attn_shape* s, bool with_items, Plan
     d.n_pages = (int)ceil_div(d.kv_len, 16);
     d.phase = q.phase;
     d.n_split = 1;
-    for (int i = 0; i < d.n_pages; i++) p.pages.push_back(q.pages[i]);
     tok += q.n_new;
     pg += d.n_pages;
   }
   p.T = tok;
+  p.pages.resize(pg);
+  for (int r = 0; r < p.R; r++)
+    std::copy(b->reqs[r].pages, b->reqs[r].pages + p.reqs[r].n_pages,
+              p.pages.begin() + p.reqs[r].page_start);
   if (!with_items) return;
   const int nq = s->n_q_heads;
   // prefill q tiles first (heaviest work first: later tiles see more keys)
@@ -188,12 +194,18 @@ void build_plan(const mx_batch* b, const mx_attn_shape* s, bool with_items, Plan
   // the hardware hands workgroups to free slots in list order, so the longest
   // items must not be left for the end: prefill tiles by the keys their last
   // rows scan, then the decode splits by page count, each longest first
-  std::stable_sort(p.items.begin(), p.items.end(), [&](const AttnItem& a, const AttnItem& b) {
+  auto longer = [&](const AttnItem& a, const AttnItem& b) {
     const ReqDev& ra = p.reqs[a.req];
     const ReqDev& rb = p.reqs[b.req];
     return ra.ctx_len + std::min(a.start + 64, ra.n_new) > rb.ctx_len + std::min(b.start + 64, rb.n_new);
-  });
-  const size_t first_decode = p.items.size();
+  };
+  // (one prompt's tiles are generated in this order already)
+  if (!std::is_sorted(p.items.begin(), p.items.end(), longer))
+    std::stable_sort(p.items.begin(), p.items.end(), longer);
+  // decode splits, longest first: a stable counting sort on the split's page
+  // count (1 .. split_pages), so equal lengths keep request, split and head order
+  std::vector<AttnItem> dec;
+  std::vector<int64_t> count(p.split_pages + 2, 0);
   for (int r = 0; r < p.R; r++) {
     ReqDev& d = p.reqs[r];
     if (d.phase != MX_DECODE) continue;
@@ -205,7 +217,8 @@ void build_plan(const mx_batch* b, const mx_attn_shape* s, bool with_items, Plan
       p.n_parts += (int64_t)nq * ns;
       p.merges.push_back(MergeItem{r, (int32_t)part_base});
     }
-    for (int sp = 0; sp < ns; sp++)
+    for (int sp = 0; sp < ns; sp++) {
+      const int len = std::min(p.split_pages, d.n_pages - sp * p.split_pages);
       for (int g = 0; g < s->n_kv_heads; g++)
         for (int h0 = 0; h0 < p.group; h0 += 16) {
           AttnItem it;
@@ -215,14 +228,18 @@ void build_plan(const mx_batch* b, const mx_attn_shape* s, bool with_items, Plan
           it.nrows = (int8_t)std::min(16, p.group - h0);
           it.start = sp * p.split_pages;
           it.part = (int32_t)(part_base + (int64_t)it.head * ns + sp);
-          p.items.push_back(it);
+          dec.push_back(it);
+          count[p.split_pages - len + 1]++;
         }
+    }
   }
-  auto pages_of = [&](const AttnItem& it) {
-    return std::min(p.split_pages, p.reqs[it.req].n_pages - it.start);
-  };
-  std::stable_sort(p.items.begin() + first_decode, p.items.end(),
-                   [&](const AttnItem& a, const AttnItem& b) { return pages_of(a) > pages_of(b); });
+  for (size_t i = 1; i < count.size(); i++) count[i] += count[i - 1];
+  const size_t first_decode = p.items.size();
+  p.items.resize(first_decode + dec.size());
+  for (const AttnItem& it : dec) {
+    const int len = std::min(p.split_pages, p.reqs[it.req].n_pages - it.start);
+    p.items[first_decode + count[p.split_pages - len]++] = it;
+  }
 }
 
 // ------------------------------------------------------------------ workspace layout
