@@ -237,7 +237,7 @@ int32_t mx_profile_read(const char** names, float* total_ms, int32_t* counts, in
 /* The projection GEMM of the layer on its own: C[M][N] = epi(A[M][K] B[N][K]^T),
  * bf16 in, fp32 accumulate; epilogue 0 = store, 1 = + R[M][N] (residual),
  * 2 = SwiGLU over B rows interleaved gate/up in 32-row blocks (C is [M][N/2]).
- * K must be a multiple of 64.  ws holds the K-split scratch
+ * R must not overlap C.  K must be a multiple of 64.  ws holds the K-split scratch
  * (mx_debug_gemm_ws_bytes).  For tests and microbenchmarks. */
 size_t mx_debug_gemm_ws_bytes(int32_t M, int32_t N, int32_t K);
 mx_status mx_debug_gemm(int32_t M, int32_t N, int32_t K, const uint16_t* A, const uint16_t* B,

@@ -81,103 +81,241 @@ __device__ __forceinline__ void tile_coords(int bid, int tiles_m, int tiles_n, i
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
 
+// Pointers of the fused QKV epilogue, passed to the epilogue functions as
+// separate __restrict__ parameters: the table reads (rotary cos/sin, KV slots)
+// then cannot alias the stores, so the reads of a whole row block are issued
+// before its first store.  (A wait on a load also waits for every store issued
+// before it: interleaved, each store would put a full memory round trip in
+// front of the next load.)
+struct QkvPtrs {
+  const float2* rope_cs;
+  const int64_t* tok_slot;
+  uint16_t* q_out;
+  uint16_t* k_pool;
+  uint16_t* v_pool;
+};
+
 // Fused QKV epilogue for one rotary pair: packed columns c and c + 32 (c in the
-// low 32-column block of a 64-column group) of token row t, fp32 values lo, hi.
-// q and k heads are rotated (rotate-half pairing, dims d_lo and d_lo + hd/2)
-// and rounded once; q goes to q_out, k and v to their slots in the pools.
-__device__ __forceinline__ void qkv_pair_store(const GemmArgs& a, int t, int c, float lo, float hi) {
-  const QkvEpilogue& e = a.qkv;
-  const int hd = e.head_dim;
+// low 32-column block of a 64-column group) of token row t, fp32 values lo,
+// hi, with the token's KV slot and the pair's (cos, sin) already read.  q and k
+// heads are rotated (rotate-half pairing, dims d_lo and d_lo + hd/2) and
+// rounded once; q goes to q_out, k and v to their slots in the pools.
+__device__ __forceinline__ void qkv_pair_store(uint16_t* __restrict__ q_out,
+                                               uint16_t* __restrict__ k_pool,
+                                               uint16_t* __restrict__ v_pool, int nq, int nkv,
+                                               int hd, int t, int c, float lo, float hi,
+                                               int64_t slot, float2 cs) {
   const int head = c / hd, within = c % hd;
-  const int64_t slot = (head >= e.nq) ? e.tok_slot[t] : 0;
-  if (head < e.nq + e.nkv) {
+  if (head < nq + nkv) {
     const int d_lo = 32 * (within / 64) + (within % 32);
-    const float2 cs = e.rope_cs[(int64_t)t * (hd / 2) + d_lo];
     const float rlo = lo * cs.x - hi * cs.y;
     const float rhi = hi * cs.x + lo * cs.y;
     uint16_t* dst;
-    if (head < e.nq) {
-      dst = e.q_out + ((int64_t)t * e.nq + head) * hd;
+    if (head < nq) {
+      dst = q_out + ((int64_t)t * nq + head) * hd;
     } else {
       const int64_t page = slot / 16;
-      dst = e.k_pool + ((page * e.nkv + (head - e.nq)) * 16 + slot % 16) * hd;
+      dst = k_pool + ((page * nkv + (head - nq)) * 16 + slot % 16) * hd;
     }
     dst[d_lo] = f32_to_bf16(rlo);
     dst[d_lo + hd / 2] = f32_to_bf16(rhi);
   } else {
     const int64_t page = slot / 16;
-    uint16_t* dst = e.v_pool + ((page * e.nkv + (head - e.nq - e.nkv)) * hd) * 16 + slot % 16;
+    uint16_t* dst = v_pool + ((page * nkv + (head - nq - nkv)) * hd) * 16 + slot % 16;
     dst[(int64_t)within * 16] = f32_to_bf16(lo);
     dst[(int64_t)(within + 32) * 16] = f32_to_bf16(hi);
   }
 }
 
+// The (cos, sin) of packed column c (any column of a 64-column group) of
+// token t; in bounds for every c (v heads read a row of the table too).
+__device__ __forceinline__ int rope_index(int t, int c, int hd) {
+  const int within = c % hd;
+  return t * (hd / 2) + 32 * (within / 64) + (within % 32);
+}
+
 // QKV epilogue of one wave's block (rows r0.., columns c0..).  q and k heads
-// go through qkv_pair_store.  A v head goes to the transposed value pages
-// [page][kv head][dim][16 slots], where one dim of consecutive slots is a
-// contiguous run: when rows 8 jj .. 8 jj + 7 of a 32-row block hold tokens in
-// eight consecutive slots starting at a multiple of 8, the lane pair
-// (l, l ^ 32) trades halves so that each lane holds the eight tokens of one dim
-// and writes them with a single 16-byte store; otherwise every value is stored
-// on its own.
+// are rotated and rounded once; q goes to q_out, k to its pool slot.  A v head
+// goes to the transposed value pages [page][kv head][dim][16 slots], where one
+// dim of consecutive slots is a contiguous run: when rows 8 jj .. 8 jj + 7 of a
+// 32-row block hold tokens in eight consecutive slots starting at a multiple
+// of 8, the lane pair (l, l ^ 32) trades halves so that each lane holds the
+// eight tokens of one dim and writes them with a single 16-byte store;
+// otherwise every value is stored on its own.
+// Per 32-row block, in three phases: every read (KV slots, rotary cos/sin;
+// unconditional, indices clamped into range), then all arithmetic (rotated
+// values, destination offsets, the traded value runs) in straight-line code,
+// then the stores, which use no register a load is still filling.  (A wait on
+// a load also waits for every store issued before it, so loads and stores
+// interleaved would cost one memory round trip per element.)
 template <int MB, int NB>
-__device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&acc)[MB][NB],
-                                             int r0, int c0, int lane) {
-  const QkvEpilogue& e = a.qkv;
-  const int hd = e.head_dim;
+__device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MB][NB], int M, int N, int r0,
+                                             int c0, int lane, const float2* __restrict__ rope_cs,
+                                             const int64_t* __restrict__ tok_slot,
+                                             uint16_t* __restrict__ q_out,
+                                             uint16_t* __restrict__ k_pool,
+                                             uint16_t* __restrict__ v_pool, int nq, int nkv,
+                                             int hd) {
+  constexpr int NP = NB / 2;  // 64-column groups (rotary pairs) per lane
   const int ccol = lane & 31, crow = 4 * (lane >> 5);
   const bool upper = lane >= 32;
-  const int first_v_col = (e.nq + e.nkv) * hd;
-  const bool has_v = c0 + NB * 32 > first_v_col;  // the same for the whole wave
 #pragma unroll
   for (int i = 0; i < MB; i++) {
+    // 1. reads: the KV slots of this lane's rows, the (cos, sin) of its pairs
+    int64_t slot[4][4];
+    float2 cs[4][NP][4];
+#pragma unroll
+    for (int jj = 0; jj < 4; jj++)
+#pragma unroll
+      for (int ii = 0; ii < 4; ii++) {
+        const int row = min(r0 + i * 32 + 8 * jj + crow + ii, M - 1);
+        slot[jj][ii] = tok_slot[row];
+#pragma unroll
+        for (int jp = 0; jp < NP; jp++)
+          cs[jj][jp][ii] = rope_cs[rope_index(row, c0 + jp * 64 + ccol, hd)];
+      }
+    __builtin_amdgcn_sched_barrier(0);
+    // 2. arithmetic: what goes where
+    uint32_t val[4][NP][4];  // bf16 pair (low: dim d_lo or c, high: d_lo + hd/2 or c + 32)
+    int64_t dst[4][NP][4];   // element offset of the low value in its buffer
+    u32x4 run[4][NP];        // the traded value run of a v head (when run8)
+    bool run8[4];
+    int64_t run_slot[4];     // slot of row 8 jj (where a run starts)
 #pragma unroll
     for (int jj = 0; jj < 4; jj++) {
       const int rbase = r0 + i * 32 + 8 * jj;
-      if (rbase >= a.M) continue;
-      bool run8 = false;
-      int64_t s0 = 0;
-      if (has_v && rbase + 7 < a.M) {
-        s0 = e.tok_slot[rbase];
-        run8 = (s0 & 7) == 0;
+      bool own = true;
 #pragma unroll
-        for (int k = 1; k < 8; k++) run8 = run8 && e.tok_slot[rbase + k] == s0 + k;
-      }
+      for (int ii = 1; ii < 4; ii++) own = own && slot[jj][ii] == slot[jj][0] + ii;
+      const int64_t other = __shfl_xor(slot[jj][0], 32);
+      const bool other_own = __shfl_xor((int)own, 32) != 0;
+      const int64_t s_lo = upper ? other : slot[jj][0], s_hi = upper ? slot[jj][0] : other;
+      run8[jj] = rbase + 7 < M && own && other_own && (s_lo & 7) == 0 && s_hi == s_lo + 4;
+      run_slot[jj] = s_lo;
 #pragma unroll
-      for (int jp = 0; jp < NB / 2; jp++) {
-        const int cb = c0 + jp * 64;
-        if (cb >= a.N) continue;
-        const int colg = cb + ccol;
+      for (int jp = 0; jp < NP; jp++) {
+        const int colg = c0 + jp * 64 + ccol;
+        const int head = colg / hd, within = colg % hd;
+        const int d_lo = 32 * (within / 64) + (within % 32);
         float lo[4], hi[4];
 #pragma unroll
         for (int ii = 0; ii < 4; ii++) {
           lo[ii] = acc[i][2 * jp][4 * jj + ii];
           hi[ii] = acc[i][2 * jp + 1][4 * jj + ii];
         }
-        if (cb >= first_v_col && run8) {
-          // lower lane: dim c, tokens 0..3 (own) + 4..7 (partner);
-          // upper lane: dim c + 32, tokens 0..3 (partner) + 4..7 (own)
-          float tok[8];
+        // lower lane: dim c, tokens 0..3 (own) + 4..7 (partner);
+        // upper lane: dim c + 32, tokens 0..3 (partner) + 4..7 (own)
+        float tok[8];
 #pragma unroll
-          for (int ii = 0; ii < 4; ii++) {
-            const float got = __shfl_xor(upper ? lo[ii] : hi[ii], 32);
-            tok[ii] = upper ? got : lo[ii];
-            tok[4 + ii] = upper ? hi[ii] : got;
+        for (int ii = 0; ii < 4; ii++) {
+          const float got = __shfl_xor(upper ? lo[ii] : hi[ii], 32);
+          tok[ii] = upper ? got : lo[ii];
+          tok[4 + ii] = upper ? hi[ii] : got;
+        }
+#pragma unroll
+        for (int h = 0; h < 4; h++) run[jj][jp][h] = pack_bf16x2(tok[2 * h], tok[2 * h + 1]);
+        asm volatile("" : "+v"(run[jj][jp]));
+#pragma unroll
+        for (int ii = 0; ii < 4; ii++) {
+          const int t = rbase + crow + ii;
+          const int64_t sl = slot[jj][ii];
+          if (head < nq + nkv) {
+            const float2 c = cs[jj][jp][ii];
+            val[jj][jp][ii] = pack_bf16x2(lo[ii] * c.x - hi[ii] * c.y, hi[ii] * c.x + lo[ii] * c.y);
+            dst[jj][jp][ii] = head < nq ? ((int64_t)t * nq + head) * hd + d_lo
+                                        : (((sl >> 4) * nkv + (head - nq)) * 16 + (sl & 15)) * hd + d_lo;
+          } else {
+            val[jj][jp][ii] = pack_bf16x2(lo[ii], hi[ii]);
+            dst[jj][jp][ii] = (((sl >> 4) * nkv + (head - nq - nkv)) * hd + within) * 16 + (sl & 15);
           }
-          const int within = colg % hd + (upper ? 32 : 0);
-          const int vh = cb / hd - e.nq - e.nkv;
-          u32x4 w;
+          // (pinned: otherwise this sinks into the bounds-checked store blocks)
+          asm volatile("" : "+v"(val[jj][jp][ii]), "+v"(dst[jj][jp][ii]));
+        }
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // 3. stores
 #pragma unroll
-          for (int h = 0; h < 4; h++) w[h] = pack_bf16x2(tok[2 * h], tok[2 * h + 1]);
-          *reinterpret_cast<u32x4*>(e.v_pool + (((s0 >> 4) * e.nkv + vh) * hd + within) * 16 +
-                                    (s0 & 15)) = w;
-        } else {
+    for (int jj = 0; jj < 4; jj++) {
+      const int rbase = r0 + i * 32 + 8 * jj;
+      if (rbase >= M) continue;
 #pragma unroll
-          for (int ii = 0; ii < 4; ii++) {
-            const int row = rbase + crow + ii;
-            if (row < a.M) qkv_pair_store(a, row, colg, lo[ii], hi[ii]);
+      for (int jp = 0; jp < NP; jp++) {
+        const int cb = c0 + jp * 64;
+        if (cb >= N) continue;
+        const int head = (cb + ccol) / hd;
+        if (head >= nq + nkv && run8[jj]) {
+          // (every cross-lane exchange happens above, with all lanes active)
+          const int64_t s0 = run_slot[jj];
+          const int within = (cb + ccol) % hd + (upper ? 32 : 0);
+          *reinterpret_cast<u32x4*>(v_pool + (((s0 >> 4) * nkv + (head - nq - nkv)) * hd + within) * 16 +
+                                    (s0 & 15)) = run[jj][jp];
+          continue;
+        }
+#pragma unroll
+        for (int ii = 0; ii < 4; ii++) {
+          if (rbase + crow + ii >= M) continue;
+          const uint16_t vlo = (uint16_t)(val[jj][jp][ii] & 0xFFFFu);
+          const uint16_t vhi = (uint16_t)(val[jj][jp][ii] >> 16);
+          if (head < nq) {
+            q_out[dst[jj][jp][ii]] = vlo;
+            q_out[dst[jj][jp][ii] + hd / 2] = vhi;
+          } else if (head < nq + nkv) {
+            k_pool[dst[jj][jp][ii]] = vlo;
+            k_pool[dst[jj][jp][ii] + hd / 2] = vhi;
+          } else {
+            v_pool[dst[jj][jp][ii]] = vlo;
+            v_pool[dst[jj][jp][ii] + 32 * 16] = vhi;
           }
         }
+      }
+    }
+  }
+}
+
+// Plain or residual epilogue of one wave's block (rows r0.., columns c0..),
+// per 32-row block in three phases like the QKV epilogue: every residual read
+// (unconditional, indices clamped into range), the sums rounded to bf16, then
+// the stores.  R must not overlap C.
+template <int MB, int NB, bool RESIDUAL>
+__device__ __forceinline__ void store_epilogue(const f32x16 (&acc)[MB][NB], int M, int N, int r0,
+                                               int c0, int lane, const uint16_t* __restrict__ R,
+                                               int ldr, uint16_t* __restrict__ C, int ldc) {
+  const int ccol = lane & 31, crow = 4 * (lane >> 5);
+#pragma unroll
+  for (int i = 0; i < MB; i++) {
+    float res[16][NB];
+#pragma unroll
+    for (int r = 0; r < 16; r++)
+#pragma unroll
+      for (int j = 0; j < NB; j++) {
+        res[r][j] = 0.f;
+        if constexpr (RESIDUAL) {
+          const int row = min(r0 + i * 32 + 8 * (r >> 2) + crow + (r & 3), M - 1);
+          const int colg = min(c0 + j * 32 + ccol, N - 1);
+          res[r][j] = bf16_to_f32(R[(int64_t)row * ldr + colg]);
+        }
+      }
+    __builtin_amdgcn_sched_barrier(0);
+    // (pinned: otherwise the sums sink into the bounds-checked store blocks,
+    // behind earlier stores)
+    uint32_t out[16][NB];
+#pragma unroll
+    for (int r = 0; r < 16; r++)
+#pragma unroll
+      for (int j = 0; j < NB; j++) {
+        out[r][j] = f32_to_bf16(acc[i][j][r] + res[r][j]);
+        asm volatile("" : "+v"(out[r][j]));
+      }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int r = 0; r < 16; r++) {
+      const int row = r0 + i * 32 + 8 * (r >> 2) + crow + (r & 3);
+      if (row >= M) continue;
+#pragma unroll
+      for (int j = 0; j < NB; j++) {
+        const int colg = c0 + j * 32 + ccol;
+        if (colg < N) C[(int64_t)row * ldc + colg] = (uint16_t)out[r][j];
       }
     }
   }
@@ -308,7 +446,14 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
 
   // epilogue
   if constexpr (EPI == EPI_QKV && !SPLIT) {
-    qkv_epilogue<MB, NB>(a, acc, m0 + wave_m * WM, n0 + wave_n * WN, lane);
+    const QkvEpilogue& e = a.qkv;
+    qkv_epilogue<MB, NB>(acc, a.M, a.N, m0 + wave_m * WM, n0 + wave_n * WN, lane, e.rope_cs,
+                         e.tok_slot, e.q_out, e.k_pool, e.v_pool, e.nq, e.nkv, e.head_dim);
+    return;
+  }
+  if constexpr (!SPLIT && (EPI == EPI_STORE || EPI == EPI_RESIDUAL)) {
+    store_epilogue<MB, NB, EPI == EPI_RESIDUAL>(acc, a.M, a.N, m0 + wave_m * WM, n0 + wave_n * WN,
+                                                lane, a.R, a.ldr, a.C, a.ldc);
     return;
   }
   const int ccol = lane & 31, crow = 4 * (lane >> 5);
@@ -332,15 +477,6 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
           const float gt = acc[i][2 * jp][r], up = acc[i][2 * jp + 1][r];
           a.C[(int64_t)row * a.ldc + colg / 2 + ccol] = f32_to_bf16(silu(gt) * up);
         }
-      } else {
-#pragma unroll
-        for (int j = 0; j < NB; j++) {
-          const int colg = n0 + wave_n * WN + j * 32 + ccol;
-          if (colg >= a.N) continue;
-          float v = acc[i][j][r];
-          if constexpr (EPI == EPI_RESIDUAL) v += bf16_to_f32(a.R[(int64_t)row * a.ldr + colg]);
-          a.C[(int64_t)row * a.ldc + colg] = f32_to_bf16(v);
-        }
       }
     }
   }
@@ -363,7 +499,9 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int kspl
         lo += a.partial[z * plane + li];
         hv += a.partial[z * plane + hi];
       }
-      qkv_pair_store(a, row, c, lo, hv);
+      const QkvEpilogue& e = a.qkv;
+      qkv_pair_store(e.q_out, e.k_pool, e.v_pool, e.nq, e.nkv, e.head_dim, row, c, lo, hv,
+                     e.tok_slot[row], e.rope_cs[rope_index(row, c, e.head_dim)]);
     } else if constexpr (EPI == EPI_SWIGLU) {
       const int fb = col / 32, w = col % 32;
       const int64_t gi = (int64_t)row * a.N + fb * 64 + w, ui = gi + 32;

@@ -845,6 +845,11 @@ MX_EXPORT mx_status mx_debug_gemm_config(int32_t M, int32_t N, int32_t K, const 
   if (M == 0) return MX_OK;
   if (!A || !B || !C || (epilogue == EPI_RESIDUAL && !R)) return fail(MX_ERR_NULL, "NULL operand");
   if (mx_status sa = check_aligned({A, B, C, R, ws}); sa != MX_OK) return sa;
+  if (epilogue == EPI_RESIDUAL) {
+    const size_t bytes = (size_t)M * N * 2;  // C and R are both [M][N]
+    const char *c0 = (const char*)C, *r0 = (const char*)R;
+    if (c0 < r0 + bytes && r0 < c0 + bytes) return fail(MX_ERR_INVALID, "R overlaps C");
+  }
   const size_t need = tile_cfg >= 0 ? (ksplit > 1 ? (size_t)ksplit * M * N : 0)
                                     : gemm_scratch_floats(M, N, K);
   if (need && (!ws || ws_bytes < need * 4))

@@ -146,6 +146,7 @@ def test_workspace_bound_covers_batch(key, P):
     ((64, 96, 256, 2, 0, 1), "MX_ERR_UNSUPPORTED"),    # SwiGLU needs N % 64 == 0
     ((64, 256, 256, 3, 0, 1), "MX_ERR_INVALID"),       # the QKV epilogue is not exposed here
     ((64, 256, 512, 0, 0, 2), "MX_ERR_TOO_LARGE"),     # split scratch larger than ws
+    ((64, 256, 256, 1, 0, 1), "MX_ERR_INVALID"),       # residual R overlapping C (0x4000 in [0x3000, +32K))
 ])
 def test_debug_gemm_config_errors(args, status):
     M, N, K, epi, cfg, ks = args
