@@ -294,9 +294,8 @@ def kernel_breakdown(pt, steps, warmup):
     parts = pt.parts
     algo = {"gemm_qkv": parts["qkv"], "gemm_o": parts["o"], "gemm_gate_up": parts["gate_up"],
             "gemm_down": parts["down"], "paged_attn": parts["attention"],
-            "rmsnorm_1": {"flops": 0.0, "bytes": parts["rmsnorm"]["bytes"] / 2},
-            "rmsnorm_2": {"flops": 0.0, "bytes": parts["rmsnorm"]["bytes"] / 2},
-            "token_map": {"flops": 0.0, "bytes": 0.0}}
+            "token_map+rmsnorm_1": {"flops": 0.0, "bytes": parts["rmsnorm"]["bytes"] / 2},
+            "rmsnorm_2": {"flops": 0.0, "bytes": parts["rmsnorm"]["bytes"] / 2}}
     res = {}
     for tag, (ms, n) in times.items():
         us = ms / max(n, 1) * 1e3

@@ -11,40 +11,63 @@ namespace {
 
 // ---------------------------------------------------------------- token map
 // One thread per (token, rotary pair).  The token's request is found by binary
-// search over the requests' first rows; token t = tok_start + i of request r
-// sits at position ctx_len + i and writes slot page * 16 + pos % 16.  The
-// rotary angle pos * theta^(-2i/d) is formed and reduced modulo 2 pi in double
-// precision; its cosine and sine are then taken in single precision.
-__global__ __launch_bounds__(256) void token_map_kernel(const ReqDev* __restrict__ reqs, int R,
-                                                        int T, const int32_t* __restrict__ pages,
-                                                        int32_t* tok_req, int32_t* tok_pos,
-                                                        int64_t* tok_slot,
-                                                        const double* __restrict__ inv_freq,
-                                                        float2* rope_cs, int half) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int t = (int)(idx / half), i = (int)(idx % half);
-  if (t >= T) return;
-  int lo = 0, hi = R - 1;
+// search over the requests' first rows (copied to LDS first when they fit, so
+// that the search does not chain global-memory round trips); token
+// t = tok_start + i of request r sits at position ctx_len + i and writes slot
+// page * 16 + pos % 16.  The rotary angle pos * theta^(-2i/d) is formed and
+// reduced modulo 2 pi in double precision; its cosine and sine are then taken
+// in single precision.
+constexpr int kLdsReqs = 4096;
+
+struct TokenMapArgs {
+  const ReqDev* reqs;
+  int R, T;
+  const int32_t* pages;
+  int32_t* tok_req;
+  int32_t* tok_pos;
+  int64_t* tok_slot;
+  const double* inv_freq;
+  float2* rope_cs;
+  int half;
+};
+
+// Block-uniform: every thread of the block calls it (it synchronises the block).
+__device__ __forceinline__ void token_map_block(const TokenMapArgs& a, int block, int* s_start) {
+  const bool in_lds = a.R <= kLdsReqs;
+  if (in_lds) {
+    for (int r = threadIdx.x; r < a.R; r += blockDim.x) s_start[r] = a.reqs[r].tok_start;
+    __syncthreads();
+  }
+  const int64_t idx = (int64_t)block * blockDim.x + threadIdx.x;
+  const int t = (int)(idx / a.half), i = (int)(idx % a.half);
+  if (t >= a.T) return;
+  int lo = 0, hi = a.R - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    if (reqs[mid].tok_start <= t) lo = mid; else hi = mid - 1;
+    const int start = in_lds ? s_start[mid] : a.reqs[mid].tok_start;
+    if (start <= t) lo = mid; else hi = mid - 1;
   }
-  const ReqDev rq = reqs[lo];
+  const ReqDev rq = a.reqs[lo];
   const int pos = rq.ctx_len + (t - rq.tok_start);
   if (i == 0) {
-    const int64_t page = pages[rq.page_start + pos / 16];
-    tok_req[t] = lo;
-    tok_pos[t] = pos;
-    tok_slot[t] = page * 16 + pos % 16;
+    const int64_t page = a.pages[rq.page_start + pos / 16];
+    a.tok_req[t] = lo;
+    a.tok_pos[t] = pos;
+    a.tok_slot[t] = page * 16 + pos % 16;
   }
-  if (rope_cs) {
-    const double a = (double)pos * inv_freq[i];
+  if (a.rope_cs) {
+    const double ang = (double)pos * a.inv_freq[i];
     const double two_pi = 6.283185307179586476925286766559;
-    const double r = a - rint(a / two_pi) * two_pi;
+    const double r = ang - rint(ang / two_pi) * two_pi;
     float sn, cs;
     sincosf((float)r, &sn, &cs);
-    rope_cs[(int64_t)t * half + i] = make_float2(cs, sn);
+    a.rope_cs[(int64_t)t * a.half + i] = make_float2(cs, sn);
   }
+}
+
+__global__ __launch_bounds__(256) void token_map_kernel(TokenMapArgs a) {
+  __shared__ int s_start[kLdsReqs];
+  token_map_block(a, blockIdx.x, s_start);
 }
 
 // ---------------------------------------------------------------- RMSNorm
@@ -57,12 +80,11 @@ __device__ __forceinline__ float block_sum_256(float v, float* red) {
   return red[0] + red[1] + red[2] + red[3];
 }
 
-__global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict__ x,
-                                                      const uint16_t* __restrict__ g,
-                                                      uint16_t* __restrict__ out, int H,
-                                                      float eps) {
-  __shared__ float red[4];
-  const int64_t row = blockIdx.x;
+// One row per block of 256 threads.
+__device__ __forceinline__ void rmsnorm_row(const uint16_t* __restrict__ x,
+                                            const uint16_t* __restrict__ g,
+                                            uint16_t* __restrict__ out, int H, float eps,
+                                            int64_t row, float* red) {
   const u32x4* xr = reinterpret_cast<const u32x4*>(x + row * H);
   const u32x4* gr = reinterpret_cast<const u32x4*>(g);
   u32x4* outr = reinterpret_cast<u32x4*>(out + row * H);
@@ -88,6 +110,30 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict
     }
     outr[c] = w;
   }
+}
+
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict__ x,
+                                                      const uint16_t* __restrict__ g,
+                                                      uint16_t* __restrict__ out, int H,
+                                                      float eps) {
+  __shared__ float red[4];
+  rmsnorm_row(x, g, out, H, eps, blockIdx.x, red);
+}
+
+// The first kernel of a layer step: the token map (blocks 0 .. map_blocks - 1)
+// and the first RMSNorm (one block per row after them), which do not depend on
+// each other, in one launch.
+__global__ __launch_bounds__(256) void prologue_kernel(TokenMapArgs a, int map_blocks,
+                                                       const uint16_t* __restrict__ x,
+                                                       const uint16_t* __restrict__ g,
+                                                       uint16_t* __restrict__ out, int H,
+                                                       float eps) {
+  __shared__ int s_start[kLdsReqs];
+  if ((int)blockIdx.x < map_blocks)
+    token_map_block(a, blockIdx.x, s_start);
+  else
+    rmsnorm_row(x, g, out, H, eps, (int64_t)blockIdx.x - map_blocks,
+                reinterpret_cast<float*>(s_start));
 }
 
 // ---------------------------------------------------------------- KV append
@@ -194,8 +240,21 @@ hipError_t launch_token_map(const ReqDev* reqs, int R, int T, const int32_t* pag
   if (R == 0 || T == 0) return hipSuccess;
   if (!rope_cs) half = 1;
   const int64_t n = (int64_t)T * half;
-  token_map_kernel<<<(unsigned)((n + 255) / 256), 256, 0, stream>>>(
-      reqs, R, T, pages, tok_req, tok_pos, tok_slot, inv_freq, rope_cs, half);
+  const TokenMapArgs a{reqs, R, T, pages, tok_req, tok_pos, tok_slot, inv_freq, rope_cs, half};
+  token_map_kernel<<<(unsigned)((n + 255) / 256), 256, 0, stream>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_prologue(const ReqDev* reqs, int R, int T, const int32_t* pages,
+                           int32_t* tok_req, int32_t* tok_pos, int64_t* tok_slot,
+                           const double* inv_freq, float2* rope_cs, int half,
+                           const uint16_t* x, const uint16_t* g, uint16_t* out, int H, float eps,
+                           hipStream_t stream) {
+  if (R == 0 || T == 0) return hipSuccess;
+  const int64_t map_blocks = ((int64_t)T * half + 255) / 256;
+  const TokenMapArgs a{reqs, R, T, pages, tok_req, tok_pos, tok_slot, inv_freq, rope_cs, half};
+  prologue_kernel<<<(unsigned)(map_blocks + T), 256, 0, stream>>>(a, (int)map_blocks, x, g, out, H,
+                                                                  eps);
   return hipGetLastError();
 }
 

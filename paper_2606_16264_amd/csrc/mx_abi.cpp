@@ -700,17 +700,14 @@ MX_EXPORT mx_status mx_layer_step(const mx_batch* batch, const mx_layer_cfg* cfg
   hipError_t e;
 #define MX_CK(call, what) \
   if ((e = (call)) != hipSuccess) return hip_fail(e, what);
-  // a1: token map and rotary table
-  MX_CK(timed("token_map", stream, [&] {
-          return launch_token_map(at<ReqDev>(ws, L.reqs), p.R, p.T, at<int32_t>(ws, L.pages),
-                                  at<int32_t>(ws, L.tok_req), at<int32_t>(ws, L.tok_pos),
-                                  at<int64_t>(ws, L.tok_slot), at<double>(ws, L.inv_freq),
-                                  rope_cs, d / 2, stream);
-        }), "token map launch")
-  // a2: RMSNorm 1
-  MX_CK(timed("rmsnorm_1", stream, [&] {
-          return launch_rmsnorm(x, (const uint16_t*)(P + W.g1), h, M, H, cfg->rms_eps, stream);
-        }), "rmsnorm launch")
+  // a1 + a2: token map and rotary table, and RMSNorm 1, in one launch
+  MX_CK(timed("token_map+rmsnorm_1", stream, [&] {
+          return launch_prologue(at<ReqDev>(ws, L.reqs), p.R, p.T, at<int32_t>(ws, L.pages),
+                                 at<int32_t>(ws, L.tok_req), at<int32_t>(ws, L.tok_pos),
+                                 at<int64_t>(ws, L.tok_slot), at<double>(ws, L.inv_freq),
+                                 rope_cs, d / 2, x, (const uint16_t*)(P + W.g1), h, H,
+                                 cfg->rms_eps, stream);
+        }), "prologue launch")
   // a3-a5: QKV projection with RoPE and the KV append fused into its epilogue
   {
     GemmArgs g{h, (const uint16_t*)(P + W.qkv), nullptr, nullptr, scratch, M, Nqkv, H, H, H, 0, 0, EPI_QKV,

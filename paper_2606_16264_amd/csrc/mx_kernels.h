@@ -41,6 +41,14 @@ hipError_t launch_token_map(const ReqDev* reqs, int R, int T, const int32_t* pag
                             const double* inv_freq, float2* rope_cs, int half,
                             hipStream_t stream);
 
+// The token map with its rotary table and the first RMSNorm (below) in one
+// launch: the first kernel of a layer step.
+hipError_t launch_prologue(const ReqDev* reqs, int R, int T, const int32_t* pages,
+                           int32_t* tok_req, int32_t* tok_pos, int64_t* tok_slot,
+                           const double* inv_freq, float2* rope_cs, int half,
+                           const uint16_t* x, const uint16_t* g, uint16_t* out, int H, float eps,
+                           hipStream_t stream);
+
 // RMSNorm: out[t] = x[t] / sqrt(mean(x[t]^2) + eps) * g, bf16 in/out, fp32 math.
 hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* g, uint16_t* out, int T, int H,
                           float eps, hipStream_t stream);
