@@ -482,6 +482,36 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   }
 }
 
+// Plain or residual reduce, four columns per thread (N, ldc and ldr multiples
+// of 4): 16-byte partial loads, 8-byte residual loads and stores, and every
+// load of a thread's iteration issued before its store.
+template <bool RESIDUAL>
+__global__ __launch_bounds__(256) void splitk_reduce4_kernel(GemmArgs a, int ksplit) {
+  const int nq4 = a.N / 4;
+  const int64_t total = (int64_t)a.M * nq4;
+  const f32x4* part = reinterpret_cast<const f32x4*>(a.partial);
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int row = (int)(idx / nq4), col = (int)(idx % nq4) * 4;
+    f32x4 v = part[idx];
+    for (int z = 1; z < ksplit; z++) {
+      const f32x4 pz = part[z * total + idx];
+      v[0] += pz[0]; v[1] += pz[1]; v[2] += pz[2]; v[3] += pz[3];
+    }
+    if constexpr (RESIDUAL) {
+      const u32x2 r = *reinterpret_cast<const u32x2*>(a.R + (int64_t)row * a.ldr + col);
+      v[0] += __uint_as_float(r[0] << 16);
+      v[1] += __uint_as_float(r[0] & 0xFFFF0000u);
+      v[2] += __uint_as_float(r[1] << 16);
+      v[3] += __uint_as_float(r[1] & 0xFFFF0000u);
+    }
+    u32x2 w;
+    w[0] = pack_bf16x2(v[0], v[1]);
+    w[1] = pack_bf16x2(v[2], v[3]);
+    *reinterpret_cast<u32x2*>(a.C + (int64_t)row * a.ldc + col) = w;
+  }
+}
+
 // Sum of the K splits in fixed order, then the epilogue.
 template <int EPI>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int ksplit) {
@@ -588,6 +618,16 @@ hipError_t run_shape(const GemmArgs& a, int ksplit, hipStream_t stream) {
     const bool paired = a.epilogue == EPI_SWIGLU || a.epilogue == EPI_QKV;
     const int64_t total = (int64_t)a.M * (paired ? a.N / 2 : a.N);
     const int blocks = (int)std::min<int64_t>((total + 255) / 256, 4096);
+    const bool by4 = !paired && a.N % 4 == 0 && a.ldc % 4 == 0 &&
+                     (a.epilogue != EPI_RESIDUAL || a.ldr % 4 == 0);
+    if (by4) {
+      const int blocks4 = (int)std::min<int64_t>((total / 4 + 255) / 256, 4096);
+      if (a.epilogue == EPI_RESIDUAL)
+        splitk_reduce4_kernel<true><<<blocks4, 256, 0, stream>>>(a, ksplit);
+      else
+        splitk_reduce4_kernel<false><<<blocks4, 256, 0, stream>>>(a, ksplit);
+      return hipGetLastError();
+    }
     if (a.epilogue == EPI_QKV)
       splitk_reduce_kernel<EPI_QKV><<<blocks, 256, 0, stream>>>(a, ksplit);
     else if (a.epilogue == EPI_SWIGLU)

@@ -250,16 +250,18 @@ def gemm_case(M, N, K, epi, tile_cfg=-1, ksplit=0):
     w = wl.f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * 0.02)
     r = wl.f32_to_bf16_bits(rng.standard_normal((M, N), dtype=np.float32))
     ncol = N // 2 if epi == 2 else N
-    # filled and checked through the int16 view: few device ops exist for uint16
-    buf16 = torch.full(((M + 4) * ncol,), CANARY, dtype=torch.int16, device="cuda")
-    C = buf16.view(torch.uint16)[2 * ncol:(M + 2) * ncol].view(M, ncol)
+    # filled and checked through the int16 view: few device ops exist for uint16;
+    # C starts 16-byte aligned after at least two canary rows
+    lead = -(-2 * ncol // 8) * 8
+    buf16 = torch.full((lead + (M + 2) * ncol,), CANARY, dtype=torch.int16, device="cuda")
+    C = buf16.view(torch.uint16)[lead:lead + M * ncol].view(M, ncol)
     need = mx.mx_debug_gemm_ws_bytes(M, N, K) if tile_cfg < 0 else \
         (ksplit * M * N * 4 if ksplit > 1 else 0)
     ws = ws_tensor(max(need, 256))
     mx.mx_debug_gemm(dev(a), dev(w), C, dev(r) if epi == 1 else None, epi, ws,
                      tile_cfg=tile_cfg, ksplit=ksplit)
     sync()
-    guard = torch.cat([buf16[:2 * ncol], buf16[(M + 2) * ncol:]]).cpu().numpy()
+    guard = torch.cat([buf16[:lead], buf16[lead + M * ncol:]]).cpu().numpy()
     assert (guard == CANARY).all(), "GEMM wrote outside C"
     # every row at small shapes, sampled rows keep the fp64 reference cheap at large ones
     if M * N * K <= (1 << 31):
@@ -295,6 +297,13 @@ def test_gemm_matches_oracle(M, N, K, epi):
     (97, 640, 1024, 2, 2), (33, 384, 2048, 1, 4), (257, 320, 256, 0, 2),
 ])
 def test_gemm_forced_tile_shapes(tile_cfg, M, N, K, epi, ksplit):
+    gemm_case(M, N, K, epi, tile_cfg=tile_cfg, ksplit=ksplit)
+
+
+# N not a multiple of 4: the element-wise split-K reduce (plain and residual)
+@pytest.mark.parametrize("tile_cfg", [0, 3])
+@pytest.mark.parametrize("M,N,K,epi,ksplit", [(131, 1090, 512, 1, 2), (70, 775, 1024, 0, 4)])
+def test_gemm_ragged_n_split(tile_cfg, M, N, K, epi, ksplit):
     gemm_case(M, N, K, epi, tile_cfg=tile_cfg, ksplit=ksplit)
 
 
