@@ -80,7 +80,33 @@ __device__ __forceinline__ float block_sum_256(float v, float* red) {
   return red[0] + red[1] + red[2] + red[3];
 }
 
-// One row per block of 256 threads.
+// One row per block of 256 threads.  Rows of up to 8192 elements are held in
+// registers between the sum of squares and the scaling (with the gains, read
+// in the same first pass), so the row is read from memory once; longer rows
+// are read twice.
+constexpr int kRowChunks = 4;  // 16-byte chunks per thread held in registers
+
+__device__ __forceinline__ void rms_scale_store(u32x4 v, u32x4 gv, float inv, u32x4* dst) {
+  u32x4 w;
+#pragma unroll
+  for (int j = 0; j < 4; j++) {
+    const float a = __uint_as_float(v[j] << 16) * inv * __uint_as_float(gv[j] << 16);
+    const float b = __uint_as_float(v[j] & 0xFFFF0000u) * inv * __uint_as_float(gv[j] & 0xFFFF0000u);
+    w[j] = pack_bf16x2(a, b);
+  }
+  *dst = w;
+}
+
+__device__ __forceinline__ float sum_squares(u32x4 v) {
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; j++) {
+    const float a = __uint_as_float(v[j] << 16), b = __uint_as_float(v[j] & 0xFFFF0000u);
+    ss += a * a + b * b;
+  }
+  return ss;
+}
+
 __device__ __forceinline__ void rmsnorm_row(const uint16_t* __restrict__ x,
                                             const uint16_t* __restrict__ g,
                                             uint16_t* __restrict__ out, int H, float eps,
@@ -89,27 +115,29 @@ __device__ __forceinline__ void rmsnorm_row(const uint16_t* __restrict__ x,
   const u32x4* gr = reinterpret_cast<const u32x4*>(g);
   u32x4* outr = reinterpret_cast<u32x4*>(out + row * H);
   const int nchunk = H / 8;
+  if (nchunk <= kRowChunks * 256) {
+    u32x4 v[kRowChunks], gv[kRowChunks];
+    float ss = 0.f;
+#pragma unroll
+    for (int k = 0; k < kRowChunks; k++) {
+      const int c = threadIdx.x + k * 256;
+      const bool in = c < nchunk;
+      v[k] = in ? xr[c] : u32x4{0, 0, 0, 0};
+      gv[k] = in ? gr[c] : u32x4{0, 0, 0, 0};
+      ss += sum_squares(v[k]);
+    }
+    const float inv = 1.0f / sqrtf(block_sum_256(ss, red) / (float)H + eps);
+#pragma unroll
+    for (int k = 0; k < kRowChunks; k++) {
+      const int c = threadIdx.x + k * 256;
+      if (c < nchunk) rms_scale_store(v[k], gv[k], inv, outr + c);
+    }
+    return;
+  }
   float ss = 0.f;
-  for (int c = threadIdx.x; c < nchunk; c += 256) {
-    u32x4 v = xr[c];
-#pragma unroll
-    for (int j = 0; j < 4; j++) {
-      const float a = __uint_as_float(v[j] << 16), b = __uint_as_float(v[j] & 0xFFFF0000u);
-      ss += a * a + b * b;
-    }
-  }
-  const float total = block_sum_256(ss, red);
-  const float inv = 1.0f / sqrtf(total / (float)H + eps);
-  for (int c = threadIdx.x; c < nchunk; c += 256) {
-    u32x4 v = xr[c], gv = gr[c], w;
-#pragma unroll
-    for (int j = 0; j < 4; j++) {
-      const float a = __uint_as_float(v[j] << 16) * inv * __uint_as_float(gv[j] << 16);
-      const float b = __uint_as_float(v[j] & 0xFFFF0000u) * inv * __uint_as_float(gv[j] & 0xFFFF0000u);
-      w[j] = pack_bf16x2(a, b);
-    }
-    outr[c] = w;
-  }
+  for (int c = threadIdx.x; c < nchunk; c += 256) ss += sum_squares(xr[c]);
+  const float inv = 1.0f / sqrtf(block_sum_256(ss, red) / (float)H + eps);
+  for (int c = threadIdx.x; c < nchunk; c += 256) rms_scale_store(xr[c], gr[c], inv, outr + c);
 }
 
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict__ x,
