@@ -243,7 +243,8 @@ size_t mx_debug_gemm_ws_bytes(int32_t M, int32_t N, int32_t K);
 mx_status mx_debug_gemm(int32_t M, int32_t N, int32_t K, const uint16_t* A, const uint16_t* B,
                         uint16_t* C, const uint16_t* R, int32_t epilogue, void* ws, size_t ws_bytes,
                         hipStream_t stream);
-/* The same with a forced tile shape (0: 256x256, 1: 128x256, 2: 128x128, 3: 64x128;
+/* The same with a forced tile shape (0: 256x256, 1: 128x256, 2: 128x128, 3: 64x128,
+ * 4: 128x256 with a shallower LDS ring, two workgroups per CU;
  * -1: the library's own choice) and K split (ws must hold ksplit * M * N floats
  * when ksplit > 1).  For tuning sweeps. */
 mx_status mx_debug_gemm_config(int32_t M, int32_t N, int32_t K, const uint16_t* A, const uint16_t* B,

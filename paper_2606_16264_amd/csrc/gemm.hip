@@ -30,7 +30,6 @@ namespace {
 
 constexpr int BK = 64;    // K granularity of a split (and of the problem)
 constexpr int BKS = 32;   // K per LDS stage
-constexpr int NS = 4;     // LDS ring depth: NS - 1 stages in flight
 constexpr int kGroupM = 8;
 
 // LDS ring discipline.  The K slices are copied global -> LDS by the DMA path
@@ -321,7 +320,7 @@ __device__ __forceinline__ void store_epilogue(const f32x16 (&acc)[MB][NB], int 
   }
 }
 
-template <int BM, int BN, int WM, int WN, int EPI, bool SPLIT>
+template <int BM, int BN, int WM, int WN, int NS, int EPI, bool SPLIT>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmArgs a, int tiles_m,
                                                                            int tiles_n,
                                                                            int k_per_split) {
@@ -558,18 +557,24 @@ struct Plan {
 
 struct Shape {
   int BM, BN;
-  // time of one tile-unit on one CU: a + b * (K slice length), microseconds
-  // (least-squares fit over measured layer-shape GEMMs, all tile shapes and
-  // K splits; the main loop is bound by its global->LDS feed, so a unit's
-  // time grows with the bytes it streams)
+  // time of one round of tile-units on the chip: a + b * (K slice length),
+  // microseconds (least-squares fit over measured layer-shape GEMMs, all tile
+  // shapes and K splits; the main loop is bound by its global->LDS feed, so a
+  // unit's time grows with the bytes it streams)
   double a_us, b_us_per_k;
+  int per_cu;  // tile-units one round holds per CU
 };
 // 256x256 and 128x256 run eight waves (2 per SIMD), the smaller shapes four.
-constexpr Shape kShapes[] = {{256, 256, 3.471, 0.02443},
-                             {128, 256, 0.978, 0.01544},
-                             {128, 128, 0.615, 0.01019},
-                             {64, 128, 0.0, 0.00729}};
-constexpr int kNumShapes = 4;
+// The last shape is 128x256 with a three-stage ring (72 KB of LDS), so that
+// two workgroups share a CU: problems of more than 256 such tiles then run in
+// one round instead of two.  A round holds two tiles per CU, each running
+// 1.86 times as long as alone (measured in the layer step), hence b.
+constexpr Shape kShapes[] = {{256, 256, 3.471, 0.02443, 1},
+                             {128, 256, 0.978, 0.01544, 1},
+                             {128, 128, 0.615, 0.01019, 1},
+                             {64, 128, 0.0, 0.00729, 1},
+                             {128, 256, 0.978, 0.0287, 2}};
+constexpr int kNumShapes = 5;
 
 // Estimated time of each (tile shape, K split) choice: the busiest CU runs
 // ceil(units / 256) tile-units; nothing beats streaming the operands from HBM
@@ -584,7 +589,7 @@ Plan choose(int M, int N, int K) {
     for (int ks = 1; ks <= 8; ks *= 2) {
       if (K % (BK * ks) != 0 || K / ks < 4 * BK) break;
       if (ks > 1 && (double)ks * M * N > (double)kMaxSplitFloats) break;
-      const double rounds = std::ceil(tiles * ks / cus);
+      const double rounds = std::ceil(tiles * ks / (cus * kShapes[c].per_cu));
       const double t_units = rounds * (kShapes[c].a_us + kShapes[c].b_us_per_k * (double)(K / ks));
       const double t_mem = 2.0 * ((double)N * K + (double)M * K) / hbm * 1e6;
       const double t_red =
@@ -599,21 +604,21 @@ Plan choose(int M, int N, int K) {
   return best;
 }
 
-template <int BM, int BN, int WM, int WN, int EPI, bool SPLIT>
+template <int BM, int BN, int WM, int WN, int NS, int EPI, bool SPLIT>
 hipError_t run(const GemmArgs& a, int ksplit, hipStream_t stream) {
   const int tiles_m = (a.M + BM - 1) / BM, tiles_n = (a.N + BN - 1) / BN;
   const int threads = (BM / WM) * (BN / WN) * 64;
   const size_t lds = (size_t)NS * (BM + BN) * BKS * 2;
   dim3 grid(tiles_m * tiles_n, ksplit);
-  gemm_kernel<BM, BN, WM, WN, EPI, SPLIT><<<grid, threads, lds, stream>>>(a, tiles_m, tiles_n,
+  gemm_kernel<BM, BN, WM, WN, NS, EPI, SPLIT><<<grid, threads, lds, stream>>>(a, tiles_m, tiles_n,
                                                                           a.K / ksplit);
   return hipGetLastError();
 }
 
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN, int WM, int WN, int NS>
 hipError_t run_shape(const GemmArgs& a, int ksplit, hipStream_t stream) {
   if (ksplit > 1) {
-    hipError_t e = run<BM, BN, WM, WN, EPI_STORE, true>(a, ksplit, stream);
+    hipError_t e = run<BM, BN, WM, WN, NS, EPI_STORE, true>(a, ksplit, stream);
     if (e != hipSuccess) return e;
     const bool paired = a.epilogue == EPI_SWIGLU || a.epilogue == EPI_QKV;
     const int64_t total = (int64_t)a.M * (paired ? a.N / 2 : a.N);
@@ -639,19 +644,19 @@ hipError_t run_shape(const GemmArgs& a, int ksplit, hipStream_t stream) {
     return hipGetLastError();
   }
   switch (a.epilogue) {
-    case EPI_QKV: return run<BM, BN, WM, WN, EPI_QKV, false>(a, 1, stream);
-    case EPI_SWIGLU: return run<BM, BN, WM, WN, EPI_SWIGLU, false>(a, 1, stream);
-    case EPI_RESIDUAL: return run<BM, BN, WM, WN, EPI_RESIDUAL, false>(a, 1, stream);
-    default: return run<BM, BN, WM, WN, EPI_STORE, false>(a, 1, stream);
+    case EPI_QKV: return run<BM, BN, WM, WN, NS, EPI_QKV, false>(a, 1, stream);
+    case EPI_SWIGLU: return run<BM, BN, WM, WN, NS, EPI_SWIGLU, false>(a, 1, stream);
+    case EPI_RESIDUAL: return run<BM, BN, WM, WN, NS, EPI_RESIDUAL, false>(a, 1, stream);
+    default: return run<BM, BN, WM, WN, NS, EPI_STORE, false>(a, 1, stream);
   }
 }
 
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN, int WM, int WN, int NS>
 hipError_t set_lds_attr() {
   const int lds = NS * (BM + BN) * BKS * 2;
   hipError_t e;
 #define MX_SET(EPI, SPLIT)                                                                  \
-  e = hipFuncSetAttribute((const void*)gemm_kernel<BM, BN, WM, WN, EPI, SPLIT>,             \
+  e = hipFuncSetAttribute((const void*)gemm_kernel<BM, BN, WM, WN, NS, EPI, SPLIT>,             \
                           hipFuncAttributeMaxDynamicSharedMemorySize, lds);                 \
   if (e != hipSuccess) return e;
   MX_SET(EPI_STORE, false)
@@ -666,13 +671,15 @@ hipError_t set_lds_attr() {
 }  // namespace
 
 hipError_t gemm_init() {
-  hipError_t e = set_lds_attr<256, 256, 128, 64>();
+  hipError_t e = set_lds_attr<256, 256, 128, 64, 4>();
   if (e != hipSuccess) return e;
-  e = set_lds_attr<128, 256, 64, 64>();
+  e = set_lds_attr<128, 256, 64, 64, 4>();
   if (e != hipSuccess) return e;
-  e = set_lds_attr<128, 128, 64, 64>();
+  e = set_lds_attr<128, 128, 64, 64, 4>();
   if (e != hipSuccess) return e;
-  return set_lds_attr<64, 128, 32, 64>();
+  e = set_lds_attr<64, 128, 32, 64, 4>();
+  if (e != hipSuccess) return e;
+  return set_lds_attr<128, 256, 64, 64, 3>();
 }
 
 size_t gemm_scratch_floats(int M, int N, int K) {
@@ -697,10 +704,11 @@ hipError_t launch_gemm_config(const GemmArgs& a, size_t ws_floats, int cfg, int 
   }
   if (p.ksplit > 1 && (size_t)p.ksplit * a.M * a.N > ws_floats) p.ksplit = 1;
   switch (p.cfg) {
-    case 0: return run_shape<256, 256, 128, 64>(a, p.ksplit, stream);
-    case 1: return run_shape<128, 256, 64, 64>(a, p.ksplit, stream);
-    case 2: return run_shape<128, 128, 64, 64>(a, p.ksplit, stream);
-    default: return run_shape<64, 128, 32, 64>(a, p.ksplit, stream);
+    case 0: return run_shape<256, 256, 128, 64, 4>(a, p.ksplit, stream);
+    case 1: return run_shape<128, 256, 64, 64, 4>(a, p.ksplit, stream);
+    case 2: return run_shape<128, 128, 64, 64, 4>(a, p.ksplit, stream);
+    case 3: return run_shape<64, 128, 32, 64, 4>(a, p.ksplit, stream);
+    default: return run_shape<128, 256, 64, 64, 3>(a, p.ksplit, stream);
   }
 }
 

@@ -137,7 +137,7 @@ def test_workspace_bound_covers_batch(key, P):
 
 
 @pytest.mark.parametrize("args,status", [
-    ((64, 256, 256, 0, 4, 1), "MX_ERR_INVALID"),       # tile shape out of range
+    ((64, 256, 256, 0, 5, 1), "MX_ERR_INVALID"),       # tile shape out of range
     ((64, 256, 256, 0, -2, 1), "MX_ERR_INVALID"),
     ((64, 256, 256, 0, 0, 0), "MX_ERR_INVALID"),       # forced shape without a split count
     ((64, 256, 256, 0, 0, 3), "MX_ERR_INVALID"),       # split not dividing K into 64s

@@ -291,7 +291,7 @@ def test_gemm_matches_oracle(M, N, K, epi):
 
 
 # every tile shape with every epilogue, ragged M and N edges, with and without a K split
-@pytest.mark.parametrize("tile_cfg", [0, 1, 2, 3])
+@pytest.mark.parametrize("tile_cfg", [0, 1, 2, 3, 4])
 @pytest.mark.parametrize("M,N,K,epi,ksplit", [
     (577, 2048, 512, 2, 1), (300, 1344, 768, 0, 1), (131, 1088, 512, 1, 1),
     (97, 640, 1024, 2, 2), (33, 384, 2048, 1, 4), (257, 320, 256, 0, 2),
