@@ -208,35 +208,42 @@ __global__ __launch_bounds__(256) void gather_kernel(const uint16_t* __restrict_
 }
 
 // ---------------------------------------------------------------- weight packing
-// Packed row p of w_qkv: rows of q and k heads with head_dim 128 are permuted
-// within the head so that packed rows 64 g + w and 64 g + 32 + w hold dims
-// 32 g + w and 64 + 32 g + w (the two halves of a rotary pair); v rows and
-// head_dim 64 keep their order.
-__global__ __launch_bounds__(256) void pack_qkv_kernel(const uint16_t* __restrict__ src,
-                                                       uint16_t* __restrict__ dst, int nq, int nkv,
-                                                       int d, int H) {
-  const int p = blockIdx.x;
-  const int head = p / d, within = p % d;
-  int sw = within;
-  if (head < nq + nkv && d == 128) {
-    const int g = within / 64, blk = (within % 64) / 32, w = within % 32;
-    sw = blk * 64 + g * 32 + w;
+// Packed row n of a weight matrix -> its source row.  kind 1 (w_qkv): rows
+// of q and k heads with head_dim 128 are permuted within the head so that
+// packed rows 64 g + w and 64 g + 32 + w hold dims 32 g + w and 64 + 32 g + w
+// (the two halves of a rotary pair); v rows and head_dim 64 keep their order.
+// kind 2 (w_gate_up): block b = n / 32; even blocks are gate rows, odd blocks
+// the up rows of the same 32 features.  kind 0: identity.
+__device__ __forceinline__ int packed_source_row(int n, int kind, int nq, int nkv, int d, int F) {
+  if (kind == 1) {
+    const int head = n / d, within = n % d;
+    int sw = within;
+    if (head < nq + nkv && d == 128) {
+      const int g = within / 64, blk = (within % 64) / 32, w = within % 32;
+      sw = blk * 64 + g * 32 + w;
+    }
+    return head * d + sw;
   }
-  const u32x4* s = reinterpret_cast<const u32x4*>(src + ((int64_t)head * d + sw) * H);
-  u32x4* o = reinterpret_cast<u32x4*>(dst + (int64_t)p * H);
-  for (int c = threadIdx.x; c < H / 8; c += blockDim.x) o[c] = s[c];
+  if (kind == 2) {
+    const int b = n / 32, w = n % 32, fb = b / 2;
+    return (b % 2 == 0) ? fb * 32 + w : F + fb * 32 + w;
+  }
+  return n;
 }
 
-// Packed row p of w_gate_up: block b = p / 32; even blocks are gate rows, odd
-// blocks the up rows of the same 32 features.
-__global__ __launch_bounds__(256) void interleave_kernel(const uint16_t* __restrict__ src,
-                                                         uint16_t* __restrict__ dst, int F, int H) {
-  const int p = blockIdx.x;
-  const int b = p / 32, w = p % 32, fb = b / 2;
-  const int srow = (b % 2 == 0) ? fb * 32 + w : F + fb * 32 + w;
-  const u32x4* s = reinterpret_cast<const u32x4*>(src + (int64_t)srow * H);
-  u32x4* o = reinterpret_cast<u32x4*>(dst + (int64_t)p * H);
-  for (int c = threadIdx.x; c < H / 8; c += blockDim.x) o[c] = s[c];
+// One workgroup per 16-row block: 16-byte pieces in destination order (piece
+// q of row r of k-chunk kc), so that the stores are contiguous.
+__global__ __launch_bounds__(256) void pack_tiled_kernel(const uint16_t* __restrict__ src,
+                                                         uint16_t* __restrict__ dst, int K,
+                                                         int kind, int nq, int nkv, int d, int F) {
+  const int nb = blockIdx.x;
+  const int pieces = (K / 32) * 16 * 4;
+  u32x4* o = reinterpret_cast<u32x4*>(dst + (int64_t)nb * 16 * K);
+  for (int p = threadIdx.x; p < pieces; p += blockDim.x) {
+    const int q = p & 3, r = (p >> 2) & 15, kc = p >> 6;
+    const int srow = packed_source_row(nb * 16 + r, kind, nq, nkv, d, F);
+    o[p] = *reinterpret_cast<const u32x4*>(src + (int64_t)srow * K + kc * 32 + q * 8);
+  }
 }
 
 // Metadata upload: 16-byte words from the pinned host staging buffer (read
@@ -301,23 +308,18 @@ hipError_t launch_kv_append(const uint16_t* k_new, const uint16_t* v_new, uint16
   return hipGetLastError();
 }
 
+hipError_t launch_pack_tiled(const uint16_t* src, uint16_t* dst, int N, int K, int kind, int nq,
+                             int nkv, int d, int F, hipStream_t stream) {
+  if (N % 16 != 0 || K % 32 != 0) return hipErrorInvalidValue;
+  pack_tiled_kernel<<<N / 16, 256, 0, stream>>>(src, dst, K, kind, nq, nkv, d, F);
+  return hipGetLastError();
+}
+
 hipError_t launch_gather(const uint16_t* k_pool, const uint16_t* v_pool, const int32_t* pages,
                          int len, int nkv, int d, uint16_t* k_out, uint16_t* v_out,
                          hipStream_t stream) {
   if (len == 0) return hipSuccess;
   gather_kernel<<<len, 256, 0, stream>>>(k_pool, v_pool, pages, nkv, d, k_out, v_out);
-  return hipGetLastError();
-}
-
-hipError_t launch_pack_qkv(const uint16_t* src, uint16_t* dst, int nq, int nkv, int d, int H,
-                           hipStream_t stream) {
-  pack_qkv_kernel<<<(nq + 2 * nkv) * d, 256, 0, stream>>>(src, dst, nq, nkv, d, H);
-  return hipGetLastError();
-}
-
-hipError_t launch_interleave_gate_up(const uint16_t* src, uint16_t* dst, int F, int H,
-                                     hipStream_t stream) {
-  interleave_kernel<<<2 * F, 256, 0, stream>>>(src, dst, F, H);
   return hipGetLastError();
 }
 

@@ -352,19 +352,28 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   // 16 j .. 16 j + 15 of the stacked A|B tile; lane l lands at row 16 j + l / 4,
   // stored chunk l % 4, which holds logical chunk (l % 4) ^ ((row >> 1) & 3).
   // That XOR makes the fragment reads of 8 consecutive rows conflict-free.
+  // (an instruction's 16 rows are all A or all B: BM is a multiple of 16)
   const uint16_t* src[L];
+  int64_t kstep[L];
 #pragma unroll
   for (int i = 0; i < L; i++) {
     const int row = (wave * L + i) * 16 + (lane >> 2);
     const int c = (lane & 3) ^ ((row >> 1) & 3);
-    src[i] = (row < BM) ? a.A + (int64_t)min(m0 + row, a.M - 1) * a.lda + kbeg + c * 8
-                        : a.B + (int64_t)min(n0 + row - BM, a.N - 1) * a.ldb + kbeg + c * 8;
+    if (row < BM) {
+      src[i] = a.A + (int64_t)min(m0 + row, a.M - 1) * a.lda + kbeg + c * 8;
+      kstep[i] = BKS;
+    } else {
+      const int n = min(n0 + row - BM, a.N - 1);
+      src[i] = a.B + (int64_t)(n >> 4) * a.b_blk + (int64_t)(n & 15) * a.b_row +
+               (int64_t)(kbeg >> 5) * a.b_kstep + c * 8;
+      kstep[i] = a.b_kstep;
+    }
   }
   auto issue = [&](int st) {
     const int kk = min(st, nk - 1);  // past the end: re-fetch the last slice (never read)
     const unsigned slot = sbase + (unsigned)((st % NS) * STAGE);
 #pragma unroll
-    for (int i = 0; i < L; i++) dma16(src[i] + kk * BKS, slot + (wave * L + i) * 1024);
+    for (int i = 0; i < L; i++) dma16(src[i] + kk * kstep[i], slot + (wave * L + i) * 1024);
   };
 
   f32x16 acc[MB][NB];

@@ -596,14 +596,18 @@ MX_EXPORT mx_status mx_pack_weights(const mx_layer_cfg* cfg, const mx_layer_weig
   e = hipMemcpyAsync(P + (off), (src), (bytes), hipMemcpyDeviceToDevice, stream);    \
   if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (pack)");
   MX_CP(L.g1, w->ln1_g, H * 2)
-  MX_CP(L.o, w->w_o, H * nq * d * 2)
   MX_CP(L.g2, w->ln2_g, H * 2)
-  MX_CP(L.down, w->w_down, H * F * 2)
 #undef MX_CP
-  e = launch_interleave_gate_up(w->w_gate_up, (uint16_t*)(P + L.gu), (int)F, (int)H, stream);
-  if (e != hipSuccess) return hip_fail(e, "interleave launch");
-  e = launch_pack_qkv(w->w_qkv, (uint16_t*)(P + L.qkv), (int)nq, (int)nkv, (int)d, (int)H, stream);
-  if (e != hipSuccess) return hip_fail(e, "qkv packing launch");
+  // the four matrices in the GEMMs' tiled layout (row permutation applied on the way)
+#define MX_TILE(off, src, N, K, kind, what)                                                      \
+  e = launch_pack_tiled((src), (uint16_t*)(P + (off)), (int)(N), (int)(K), (kind), (int)nq,      \
+                        (int)nkv, (int)d, (int)F, stream);                                       \
+  if (e != hipSuccess) return hip_fail(e, what);
+  MX_TILE(L.qkv, w->w_qkv, (nq + 2 * nkv) * d, H, 1, "qkv packing launch")
+  MX_TILE(L.o, w->w_o, H, nq * d, 0, "o packing launch")
+  MX_TILE(L.gu, w->w_gate_up, 2 * F, H, 2, "gate/up packing launch")
+  MX_TILE(L.down, w->w_down, H, F, 0, "down packing launch")
+#undef MX_TILE
   return MX_OK;
 }
 
@@ -712,6 +716,7 @@ MX_EXPORT mx_status mx_layer_step(const mx_batch* batch, const mx_layer_cfg* cfg
   {
     GemmArgs g{h, (const uint16_t*)(P + W.qkv), nullptr, nullptr, scratch, M, Nqkv, H, H, H, 0, 0, EPI_QKV,
                QkvEpilogue{rope_cs, at<int64_t>(ws, L.tok_slot), q, k_pool, v_pool, nq, nkv, d}};
+    set_b_tiled(g);
     MX_CK(timed("gemm_qkv", stream, [&] { return launch_gemm(g, L.scratch_floats, stream); }),
           "qkv gemm launch")
   }
@@ -726,6 +731,7 @@ MX_EXPORT mx_status mx_layer_step(const mx_batch* batch, const mx_layer_cfg* cfg
   // a7: output projection + residual
   {
     GemmArgs g{o, (const uint16_t*)(P + W.o), x1, x, scratch, M, H, nq * d, nq * d, nq * d, H, H, EPI_RESIDUAL, {}};
+    set_b_tiled(g);
     MX_CK(timed("gemm_o", stream, [&] { return launch_gemm(g, L.scratch_floats, stream); }),
           "o gemm launch")
   }
@@ -736,12 +742,14 @@ MX_EXPORT mx_status mx_layer_step(const mx_batch* batch, const mx_layer_cfg* cfg
   // a9: gate/up projection + SwiGLU
   {
     GemmArgs g{h, (const uint16_t*)(P + W.gu), act, nullptr, scratch, M, 2 * F, H, H, H, F, 0, EPI_SWIGLU, {}};
+    set_b_tiled(g);
     MX_CK(timed("gemm_gate_up", stream, [&] { return launch_gemm(g, L.scratch_floats, stream); }),
           "gate/up gemm launch")
   }
   // a10: down projection + residual
   {
     GemmArgs g{act, (const uint16_t*)(P + W.down), y, x1, scratch, M, H, F, F, F, H, H, EPI_RESIDUAL, {}};
+    set_b_tiled(g);
     MX_CK(timed("gemm_down", stream, [&] { return launch_gemm(g, L.scratch_floats, stream); }),
           "down gemm launch")
   }
@@ -856,6 +864,7 @@ MX_EXPORT mx_status mx_debug_gemm_config(int32_t M, int32_t N, int32_t K, const 
   if (st != MX_OK) return st;
   const int ldc = epilogue == EPI_SWIGLU ? N / 2 : N;
   GemmArgs g{A, B, C, R, (float*)ws, M, N, K, K, K, ldc, N, epilogue, {}};
+  set_b_row_major(g);
   hipError_t e = launch_gemm_config(g, ws ? ws_bytes / 4 : 0, tile_cfg, ksplit, stream);
   if (e != hipSuccess) return hip_fail(e, "gemm launch");
   return MX_OK;

@@ -94,7 +94,24 @@ struct GemmArgs {
   int lda, ldb, ldc, ldr;
   int epilogue;
   QkvEpilogue qkv;
+  // B element (n, k) sits at B + (n / 16) b_blk + (n % 16) b_row + (k / 32) b_kstep
+  // + k % 32: row-major B is (16 ldb, ldb, 32) (set_b_row_major), the packed
+  // weights are 16 x 32 tiles of 1 KB, [N / 16][K / 32][16][32] (set_b_tiled),
+  // so that each DMA instruction reads one contiguous kilobyte
+  int64_t b_blk, b_kstep;
+  int b_row;
 };
+
+inline void set_b_row_major(GemmArgs& g) {
+  g.b_blk = 16 * (int64_t)g.ldb;
+  g.b_row = g.ldb;
+  g.b_kstep = 32;
+}
+inline void set_b_tiled(GemmArgs& g) {
+  g.b_blk = 16 * (int64_t)g.K;
+  g.b_row = 32;
+  g.b_kstep = 512;
+}
 
 // Chooses a tile shape and split for the problem; ws_floats is the fp32
 // scratch available at args.partial.  A K split never needs more than
@@ -109,11 +126,11 @@ int gemm_num_configs();
 size_t gemm_scratch_floats(int M, int N, int K);
 hipError_t gemm_init();
 
-// Weight packing: row permutation copies for the gate/up interleave and for
-// the RoPE pair layout of the q/k rows of w_qkv.
-hipError_t launch_interleave_gate_up(const uint16_t* src, uint16_t* dst, int F, int H,
-                                     hipStream_t stream);
-hipError_t launch_pack_qkv(const uint16_t* src, uint16_t* dst, int nq, int nkv, int d, int H,
-                           hipStream_t stream);
+// Weight packing: copies a [N][K] bf16 matrix into the GEMMs' tiled layout
+// [N / 16][K / 32][16][32] (N % 16 == 0, K % 32 == 0), taking packed row n
+// from source row perm(n): kind 0 identity, 1 the RoPE pair layout of the
+// q/k rows of w_qkv, 2 the gate/up interleave.
+hipError_t launch_pack_tiled(const uint16_t* src, uint16_t* dst, int N, int K, int kind, int nq,
+                             int nkv, int d, int F, hipStream_t stream);
 
 }  // namespace mx
