@@ -363,14 +363,18 @@ mx_status upload_meta(const Plan& p, const Layout& L, const mx_attn_shape* s, fl
     if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
   }
   if (ds->cap[i] < L.meta_end) {
-    if (ds->buf[i]) hipHostFree(ds->buf[i]);
-    ds->buf[i] = ds->dbuf[i] = nullptr;
+    if (ds->buf[i]) {
+      e = hipHostFree(ds->buf[i]);
+      ds->buf[i] = ds->dbuf[i] = nullptr;
+      ds->cap[i] = 0;
+      if (e != hipSuccess) return hip_fail(e, "hipHostFree");
+    }
     const size_t cap = std::max<size_t>(L.meta_end * 2, 1 << 16);
     e = hipHostMalloc(&ds->buf[i], cap, hipHostMallocMapped);
     if (e != hipSuccess) { ds->buf[i] = nullptr; ds->cap[i] = 0; return hip_fail(e, "hipHostMalloc"); }
     e = hipHostGetDevicePointer(&ds->dbuf[i], ds->buf[i], 0);
     if (e != hipSuccess) {
-      hipHostFree(ds->buf[i]);
+      (void)hipHostFree(ds->buf[i]);  // the lookup's error is the one reported
       ds->buf[i] = ds->dbuf[i] = nullptr;
       ds->cap[i] = 0;
       return hip_fail(e, "hipHostGetDevicePointer");
