@@ -78,7 +78,7 @@ def summarize_stats(csv_path, command, out_md):
              "[512, 2048]) with 512 mixed prefill tokens (the benchmark point, T = 576), including "
              "setup (weight packing, pool fill) and the per-kernel timing steps.", "",
              "Command (one MI355X):", "", "```", command, "```", "",
-             "Durations in microseconds (rocprofv3 kernel trace).  gemm_kernel<BM, BN, WM, WN, "
+             "Durations in microseconds (rocprofv3 kernel trace).  gemm_kernel<BM, BN, WM, WN, LDS stages, "
              "epilogue, split>: epilogue 0 store, 1 residual, 2 SwiGLU, 3 QKV.", "",
              "| kernel | calls | average us | min us | max us | share % |",
              "|---|---:|---:|---:|---:|---:|"]
