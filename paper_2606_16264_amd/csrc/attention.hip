@@ -17,12 +17,17 @@
 //                 through LDS.  Requests with several splits leave fp32
 //                 partials (unnormalised O, running max, running sum) for the
 //                 merge kernel.
-//   prefill item: one q head, 64 query rows of a prefill chunk (16 per wave),
-//                 causal over the cached prefix plus the chunk; the four waves
-//                 share each 32-key chunk through LDS (loaded once per tile).
+//   prefill item: one q head, 128 query rows of a prefill chunk (two blocks
+//                 of 16 per wave), causal over the cached prefix plus the
+//                 chunk; the four waves share each 32-key chunk through LDS
+//                 (loaded once per tile), and each wave applies the chunk's
+//                 key and value fragments, read from LDS once, to both of its
+//                 row blocks.
 //
 // Masking is select-based: slots at or past the request's length are never
 // multiplied into a sum, so stale or NaN-filled slots cannot leak.
+#include <type_traits>
+
 #include "mx_device.h"
 #include "mx_kernels.h"
 
@@ -74,20 +79,28 @@ __device__ __forceinline__ void load_chunk(Chunk<HD>& c, const AttnParams& p, in
   }
 }
 
-// One 32-key step of the online softmax for this lane's query row.  Lane group
-// g4 owns keys pi0 * 16 + 8 * g4 + i' (i' = 4 b + i for score block b, row i).
-template <int HD, bool MASK = true>
-__device__ __forceinline__ void process_chunk(const Chunk<HD>& c, const bf16x8 (&qf)[HD / 32],
-                                              f32x4 (&o)[HD / 16], float& m, float& l,
-                                              int pi0, int page_end, int row_pos, int kv_len,
-                                              float scale_log2, int g4) {
-  f32x4 s[2];
+// One 32-key step of the online softmax for this lane's query row, in two
+// parts: the scores and the softmax update from the key fragments, then the
+// value product.  Lane group g4 owns keys pi0 * 16 + 8 * g4 + i' (i' = 4 b + i
+// for score block b, row i).
+struct StepP {
+  bf16x8 pb;     // P^T as the B operand: k index i' = 4 b + i <-> key j0 + i'
+  float alpha;   // rescale of the running output
+};
+
+// Score block b of S^T = K Q^T (16 keys x 16 rows).
+template <int HD>
+__device__ __forceinline__ f32x4 score_block(const u32x4 (&kf)[HD / 32], const bf16x8 (&qf)[HD / 32]) {
+  f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int b = 0; b < 2; b++) {
-    s[b] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ds = 0; ds < HD / 32; ds++) s[b] = mfma16(as_bf16x8(c.k[b][ds]), qf[ds], s[b]);
-  }
+  for (int ds = 0; ds < HD / 32; ds++) s = mfma16(as_bf16x8(kf[ds]), qf[ds], s);
+  return s;
+}
+
+// Online-softmax update of this lane's row from its two score blocks.
+template <bool MASK>
+__device__ __forceinline__ StepP softmax_step(const f32x4 (&s)[2], float& m, float& l, int pi0,
+                                              int page_end, int row_pos, float scale_log2, int g4) {
   const bool pvalid = (pi0 + (g4 >> 1)) < page_end;
   const int j0 = pi0 * 16 + 8 * g4;
   float sv[2][4];
@@ -118,32 +131,59 @@ __device__ __forceinline__ void process_chunk(const Chunk<HD>& c, const bf16x8 (
   ps += __shfl_xor(ps, 32);
   l = l * alpha + ps;
   m = m_new;
-  // P^T as the B operand: k index i' = 4 b + i <-> key j0 + i'
   u32x4 pb_bits;
   pb_bits[0] = pack_bf16x2(pv[0][0], pv[0][1]);
   pb_bits[1] = pack_bf16x2(pv[0][2], pv[0][3]);
   pb_bits[2] = pack_bf16x2(pv[1][0], pv[1][1]);
   pb_bits[3] = pack_bf16x2(pv[1][2], pv[1][3]);
-  const bf16x8 pb = as_bf16x8(pb_bits);
-  // V^T as the A operand; values of keys past the request's length are zeroed
-  // (select, not multiply) so that NaN-filled slots stay out of the sum.
-  uint32_t keep[4];
+  return StepP{as_bf16x8(pb_bits), alpha};
+}
+
+// Which of this lane group's eight keys hold values (bf16 lanes of each
+// 32-bit word): keys past the request's length are zeroed by select, not
+// multiplied, so that NaN-filled slots stay out of the sum.  Depends on the
+// keys only, not on the row.
+__device__ __forceinline__ void value_keep(int pi0, int page_end, int kv_len, int g4,
+                                           uint32_t (&keep)[4]) {
+  const bool pvalid = (pi0 + (g4 >> 1)) < page_end;
+  const int j0 = pi0 * 16 + 8 * g4;
 #pragma unroll
   for (int h = 0; h < 4; h++) {
     const bool k0 = pvalid && (j0 + 2 * h) < kv_len;
     const bool k1 = pvalid && (j0 + 2 * h + 1) < kv_len;
     keep[h] = (k0 ? 0x0000FFFFu : 0u) | (k1 ? 0xFFFF0000u : 0u);
   }
+}
+
+// O^T = alpha O^T + V^T P^T over the output blocks DB0 .. DB0 + NDB - 1 (16
+// head dims each), V^T as the A operand.
+template <int HD, int DB0, int NDB, bool MASK>
+__device__ __forceinline__ void values_part(const u32x4 (&vf)[NDB], f32x4 (&o)[HD / 16], StepP sp,
+                                            const uint32_t (&keep)[4]) {
 #pragma unroll
-  for (int db = 0; db < HD / 16; db++) {
-    u32x4 va = c.v[db];
+  for (int e = 0; e < NDB; e++) {
+    u32x4 va = vf[e];
     if constexpr (MASK) {
 #pragma unroll
       for (int h = 0; h < 4; h++) va[h] &= keep[h];
     }
-    o[db] = o[db] * alpha;
-    o[db] = mfma16(as_bf16x8(va), pb, o[db]);
+    o[DB0 + e] = o[DB0 + e] * sp.alpha;
+    o[DB0 + e] = mfma16(as_bf16x8(va), sp.pb, o[DB0 + e]);
   }
+}
+
+// One 32-key step of the online softmax for this lane's query row.  Lane group
+// g4 owns keys pi0 * 16 + 8 * g4 + i' (i' = 4 b + i for score block b, row i).
+template <int HD, bool MASK = true>
+__device__ __forceinline__ void process_chunk(const Chunk<HD>& c, const bf16x8 (&qf)[HD / 32],
+                                              f32x4 (&o)[HD / 16], float& m, float& l,
+                                              int pi0, int page_end, int row_pos, int kv_len,
+                                              float scale_log2, int g4) {
+  const f32x4 s[2] = {score_block<HD>(c.k[0], qf), score_block<HD>(c.k[1], qf)};
+  const StepP sp = softmax_step<MASK>(s, m, l, pi0, page_end, row_pos, scale_log2, g4);
+  uint32_t keep[4];
+  value_keep(pi0, page_end, kv_len, g4, keep);
+  values_part<HD, 0, HD / 16, MASK>(c.v, o, sp, keep);
 }
 
 // Keys pi0 * 16 .. pi0 * 16 + 31 all count for every row of the wave (both
@@ -177,52 +217,207 @@ constexpr int smem_bytes() {
   return ring > combine ? ring : combine;
 }
 
+// Prefill item: one q head, rows it.start .. it.start + 127 of the chunk; wave
+// w owns two blocks of 16 consecutive rows, it.start + 32 w + (0 | 16) + col.
+static_assert(kPrefillTileRows == 4 * 32, "four waves of two 16-row blocks");
 template <int HD>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void paged_attn_kernel(AttnParams p) {
-  __shared__ __attribute__((aligned(16))) char smem[smem_bytes<HD>()];
-  const AttnItem it = p.items[blockIdx.x];
-  const ReqDev rq = p.reqs[it.req];
+__device__ __forceinline__ void prefill_item(const AttnParams& p, const AttnItem& it,
+                                             const ReqDev& rq, char* smem) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int col = lane & 15;  // query row of this lane
+  const int col = lane & 15;  // query row of this lane within each block
   const int g4 = lane >> 4;   // lane group
+  const int qhead = it.head;
+  const int kvh = qhead / p.group;
+  const int row0 = it.start + 32 * wave;
+  const int row = row0 + col, row2 = row0 + 16 + col;
+  const bool row_valid = row < rq.n_new, row_valid2 = row2 < rq.n_new;
+  const int rowc = row_valid ? row : rq.n_new - 1;
+  const int rowc2 = row_valid2 ? row2 : rq.n_new - 1;
+  const int64_t qtok = rq.tok_start + rowc, qtok2 = rq.tok_start + rowc2;
+  const int row_pos = rq.ctx_len + rowc, row_pos2 = rq.ctx_len + rowc2;
+  const int last_row = min(row0 + 31, rq.n_new - 1);
+  const int page_end = row0 < rq.n_new ? (rq.ctx_len + last_row) / 16 + 1 : 0;
+
+  float m = kNegBig, l = 0.f, m2 = kNegBig, l2 = 0.f;
+  f32x4 o[HD / 16], o2[HD / 16];
+#pragma unroll
+  for (int db = 0; db < HD / 16; db++) o[db] = o2[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  bf16x8 qf[HD / 32], qf2[HD / 32];
+  {
+    const uint16_t* qp = p.q + qtok * p.q_tok_stride + (int64_t)qhead * HD + 8 * g4;
+    const uint16_t* qp2 = p.q + qtok2 * p.q_tok_stride + (int64_t)qhead * HD + 8 * g4;
+#pragma unroll
+    for (int ds = 0; ds < HD / 32; ds++) {
+      u32x4 v = row_valid ? *reinterpret_cast<const u32x4*>(qp + ds * 32) : u32x4{0, 0, 0, 0};
+      u32x4 v2 = row_valid2 ? *reinterpret_cast<const u32x4*>(qp2 + ds * 32) : u32x4{0, 0, 0, 0};
+      qf[ds] = as_bf16x8(v);
+      qf2[ds] = as_bf16x8(v2);
+    }
+  }
+
+  // the tile's last row bounds the pages every wave helps to load
+  const int tile_last = min(it.start + kPrefillTileRows - 1, rq.n_new - 1);
+  const int item_pages = (rq.ctx_len + tile_last) / 16 + 1;
+  const int n_chunks = (item_pages + 1) / 2;
+  const int wave_chunks = (page_end + 1) / 2;  // 0 for a wave without valid rows
+  const int wave_first_pos = rq.ctx_len + it.start + 32 * wave;  // the wave's first row
+  const int safe = p.pages[rq.page_start];
+  auto pid = [&](int pi) -> int {
+    const int v = p.pages[rq.page_start + min(pi, rq.n_pages - 1)];
+    return pi < item_pages ? v : -1;
+  };
+  constexpr int KB = SharedChunk<HD>::KBYTES, CB = SharedChunk<HD>::BYTES;
+  constexpr int NLD = HD / 32;  // 16-byte loads per lane for a quarter chunk
+  u32x4 st[NLD];
+  // waves 0 / 1: keys of the chunk's first / second page; 2 / 3: values
+  auto gload = [&](int pid0, int pid1) {
+    const int pg0 = (wave & 1) ? pid1 : pid0;
+    const int pg = pg0 >= 0 ? pg0 : safe;  // past the end: masked, like the decode path
+    const uint16_t* base = (wave < 2 ? p.k_pool : p.v_pool) + ((int64_t)pg * p.nkv + kvh) * (16 * HD);
+#pragma unroll
+    for (int i = 0; i < NLD; i++) st[i] = *reinterpret_cast<const u32x4*>(base + (i * 64 + lane) * 8);
+  };
+  auto swrite = [&](char* slot) {
+#pragma unroll
+    for (int i = 0; i < NLD; i++) {
+      const int c = i * 64 + lane;
+      char* dst;
+      if (wave < 2) {
+        const int key = 16 * (wave & 1) + c / (HD / 8), lc = c % (HD / 8);
+        dst = slot + key * (HD * 2) + ((lc ^ ksw<HD>(key)) << 4);
+      } else {
+        const int d = c >> 1, lc = 2 * (wave & 1) + (c & 1);
+        dst = slot + KB + d * 64 + ((lc ^ ((d >> 2) & 3)) << 4);
+      }
+      *reinterpret_cast<u32x4*>(dst) = st[i];
+    }
+  };
+  // fragments of score block b (keys), or of output blocks DB0 .. (values)
+  auto kread = [&](const char* slot, int b, u32x4 (&kf)[HD / 32]) {
+#pragma unroll
+    for (int ds = 0; ds < HD / 32; ds++) {
+      const int key = 16 * (col >> 3) + 8 * ((col >> 2) & 1) + (col & 3) + 4 * b;
+      kf[ds] = *reinterpret_cast<const u32x4*>(slot + key * (HD * 2) +
+                                               (((4 * ds + g4) ^ ksw<HD>(key)) << 4));
+    }
+  };
+  auto vread = [&](const char* slot, int db0, u32x4 (&vf)[HD / 32]) {
+#pragma unroll
+    for (int e = 0; e < HD / 32; e++) {
+      const int d = 16 * (db0 + e) + col;
+      vf[e] = *reinterpret_cast<const u32x4*>(slot + KB + d * 64 + ((g4 ^ ((d >> 2) & 3)) << 4));
+    }
+  };
+  // one barrier per chunk: chunk kt + 1 is loaded into registers while chunk
+  // kt is processed, and stored into the other slot (read by everyone in the
+  // previous iteration, before its barrier) once the processing is done
+  int n0 = pid(2), n1 = pid(3);
+  gload(pid(0), pid(1));
+  swrite(smem);
+  __syncthreads();
+  for (int kt = 0; kt < n_chunks; kt++) {
+    const bool more = kt + 1 < n_chunks;
+    int nn0 = -1, nn1 = -1;
+    if (more) {
+      gload(n0, n1);
+      nn0 = pid(2 * kt + 4);
+      nn1 = pid(2 * kt + 5);
+    }
+    if (kt < wave_chunks) {
+      // both row blocks from one read of the chunk's fragments, half a
+      // chunk's keys (or values) at a time, each half applied to both
+      // blocks before the next is read.  The wave's first row bounds both
+      // blocks: the second block's rows come later.
+      const char* slot = smem + (kt & 1) * CB;
+      const int pi0 = 2 * kt;
+      auto both = [&](auto mask) {
+        constexpr bool MASK = decltype(mask)::value;
+        f32x4 s1[2], s2[2];
+#pragma unroll
+        for (int b = 0; b < 2; b++) {
+          u32x4 kf[HD / 32];
+          kread(slot, b, kf);
+          s1[b] = score_block<HD>(kf, qf);
+          s2[b] = score_block<HD>(kf, qf2);
+        }
+        const StepP sp1 = softmax_step<MASK>(s1, m, l, pi0, page_end, row_pos, p.scale_log2, g4);
+        const StepP sp2 = softmax_step<MASK>(s2, m2, l2, pi0, page_end, row_pos2, p.scale_log2, g4);
+        uint32_t keep[4];
+        value_keep(pi0, page_end, rq.kv_len, g4, keep);
+        {
+          u32x4 vf[HD / 32];
+          vread(slot, 0, vf);
+          values_part<HD, 0, HD / 32, MASK>(vf, o, sp1, keep);
+          values_part<HD, 0, HD / 32, MASK>(vf, o2, sp2, keep);
+        }
+        {
+          u32x4 vf[HD / 32];
+          vread(slot, HD / 32, vf);
+          values_part<HD, HD / 32, HD / 32, MASK>(vf, o, sp1, keep);
+          values_part<HD, HD / 32, HD / 32, MASK>(vf, o2, sp2, keep);
+        }
+      };
+      if (chunk_interior(pi0, page_end, wave_first_pos))
+        both(std::integral_constant<bool, false>{});
+      else
+        both(std::integral_constant<bool, true>{});
+    }
+    if (more) {
+      swrite(smem + ((kt + 1) & 1) * CB);
+      n0 = nn0;
+      n1 = nn1;
+    }
+    __syncthreads();
+  }
+  if (row_valid) {
+    const float inv = 1.f / l;
+    uint16_t* op = p.out + qtok * p.out_tok_stride + (int64_t)qhead * HD + 4 * g4;
+#pragma unroll
+    for (int db = 0; db < HD / 16; db++) {
+      u32x2 w;
+      w[0] = pack_bf16x2(o[db][0] * inv, o[db][1] * inv);
+      w[1] = pack_bf16x2(o[db][2] * inv, o[db][3] * inv);
+      *reinterpret_cast<u32x2*>(op + db * 16) = w;
+    }
+  }
+  if (row_valid2) {
+    const float inv = 1.f / l2;
+    uint16_t* op = p.out + qtok2 * p.out_tok_stride + (int64_t)qhead * HD + 4 * g4;
+#pragma unroll
+    for (int db = 0; db < HD / 16; db++) {
+      u32x2 w;
+      w[0] = pack_bf16x2(o2[db][0] * inv, o2[db][1] * inv);
+      w[1] = pack_bf16x2(o2[db][2] * inv, o2[db][3] * inv);
+      *reinterpret_cast<u32x2*>(op + db * 16) = w;
+    }
+  }
+}
+
+// Decode item: the q heads it.head .. it.head + nrows - 1 (one per lane row)
+// of the request's single token, over pages it.start .. of its table; the four
+// waves stride over the split's 32-key chunks and combine through LDS.
+template <int HD>
+__device__ __forceinline__ void decode_item(const AttnParams& p, const AttnItem& it,
+                                            const ReqDev& rq, char* smem) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int col = lane & 15;  // q head of this lane (relative to it.head)
+  const int g4 = lane >> 4;   // lane group
+  const int qhead = it.head + col;
+  const bool row_valid = col < it.nrows;
+  const int kvh = it.head / p.group;
+  const int64_t qtok = rq.tok_start;
+  const int row_pos = rq.kv_len - 1;
+  const int page_end = min(it.start + p.split_pages, rq.n_pages);
+  const int chunk_first = it.start + 2 * wave;
+  constexpr int chunk_step = 8;
 
   float m = kNegBig, l = 0.f;
   f32x4 o[HD / 16];
 #pragma unroll
   for (int db = 0; db < HD / 16; db++) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
   bf16x8 qf[HD / 32];
-
-  int kvh, qhead, row_pos, page_first, page_end, chunk_first, chunk_step;
-  bool row_valid;
-  int64_t qtok;
-  if (it.kind == 0) {
-    // decode: rows are q heads it.head .. it.head + nrows - 1 of the request's token
-    qhead = it.head + col;
-    row_valid = col < it.nrows;
-    kvh = it.head / p.group;
-    qtok = rq.tok_start;
-    row_pos = rq.kv_len - 1;
-    page_first = it.start;
-    page_end = min(it.start + p.split_pages, rq.n_pages);
-    chunk_first = page_first + 2 * wave;
-    chunk_step = 8;
-  } else {
-    // prefill: rows are 16 consecutive tokens of the chunk, one q head
-    qhead = it.head;
-    kvh = qhead / p.group;
-    const int row0 = it.start + 16 * wave;
-    const int row = row0 + col;
-    row_valid = row < rq.n_new;
-    const int rowc = row_valid ? row : rq.n_new - 1;
-    qtok = rq.tok_start + rowc;
-    row_pos = rq.ctx_len + rowc;
-    const int last_row = min(row0 + 15, rq.n_new - 1);
-    page_first = 0;
-    page_end = row0 < rq.n_new ? (rq.ctx_len + last_row) / 16 + 1 : 0;
-    chunk_first = 0;
-    chunk_step = 2;
-  }
   {
     const uint16_t* qp = p.q + qtok * p.q_tok_stride + (int64_t)qhead * HD + 8 * g4;
 #pragma unroll
@@ -230,103 +425,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
       u32x4 v = row_valid ? *reinterpret_cast<const u32x4*>(qp + ds * 32) : u32x4{0, 0, 0, 0};
       qf[ds] = as_bf16x8(v);
     }
-  }
-
-  if (it.kind == 1) {
-    // the tile's last row bounds the pages every wave helps to load
-    const int tile_last = min(it.start + 63, rq.n_new - 1);
-    const int item_pages = (rq.ctx_len + tile_last) / 16 + 1;
-    const int n_chunks = (item_pages + 1) / 2;
-    const int wave_chunks = (page_end + 1) / 2;  // 0 for a wave without valid rows
-    const int wave_first_pos = rq.ctx_len + it.start + 16 * wave;  // the wave's first row
-    const int safe = p.pages[rq.page_start];
-    auto pid = [&](int pi) -> int {
-      const int v = p.pages[rq.page_start + min(pi, rq.n_pages - 1)];
-      return pi < item_pages ? v : -1;
-    };
-    constexpr int KB = SharedChunk<HD>::KBYTES, CB = SharedChunk<HD>::BYTES;
-    constexpr int NLD = HD / 32;  // 16-byte loads per lane for a quarter chunk
-    u32x4 st[NLD];
-    // waves 0 / 1: keys of the chunk's first / second page; 2 / 3: values
-    auto gload = [&](int pid0, int pid1) {
-      const int pg0 = (wave & 1) ? pid1 : pid0;
-      const int pg = pg0 >= 0 ? pg0 : safe;  // past the end: masked, like the decode path
-      const uint16_t* base = (wave < 2 ? p.k_pool : p.v_pool) + ((int64_t)pg * p.nkv + kvh) * (16 * HD);
-#pragma unroll
-      for (int i = 0; i < NLD; i++) st[i] = *reinterpret_cast<const u32x4*>(base + (i * 64 + lane) * 8);
-    };
-    auto swrite = [&](char* slot) {
-#pragma unroll
-      for (int i = 0; i < NLD; i++) {
-        const int c = i * 64 + lane;
-        char* dst;
-        if (wave < 2) {
-          const int key = 16 * (wave & 1) + c / (HD / 8), lc = c % (HD / 8);
-          dst = slot + key * (HD * 2) + ((lc ^ ksw<HD>(key)) << 4);
-        } else {
-          const int d = c >> 1, lc = 2 * (wave & 1) + (c & 1);
-          dst = slot + KB + d * 64 + ((lc ^ ((d >> 2) & 3)) << 4);
-        }
-        *reinterpret_cast<u32x4*>(dst) = st[i];
-      }
-    };
-    auto sread = [&](const char* slot, Chunk<HD>& c) {
-#pragma unroll
-      for (int b = 0; b < 2; b++)
-#pragma unroll
-        for (int ds = 0; ds < HD / 32; ds++) {
-          const int key = 16 * (col >> 3) + 8 * ((col >> 2) & 1) + (col & 3) + 4 * b;
-          c.k[b][ds] = *reinterpret_cast<const u32x4*>(slot + key * (HD * 2) +
-                                                       (((4 * ds + g4) ^ ksw<HD>(key)) << 4));
-        }
-#pragma unroll
-      for (int db = 0; db < HD / 16; db++) {
-        const int d = 16 * db + col;
-        c.v[db] = *reinterpret_cast<const u32x4*>(slot + KB + d * 64 + ((g4 ^ ((d >> 2) & 3)) << 4));
-      }
-    };
-    // one barrier per chunk: chunk kt + 1 is loaded into registers while chunk
-    // kt is processed, and stored into the other slot (read by everyone in the
-    // previous iteration, before its barrier) once the processing is done
-    int n0 = pid(2), n1 = pid(3);
-    gload(pid(0), pid(1));
-    swrite(smem);
-    __syncthreads();
-    for (int kt = 0; kt < n_chunks; kt++) {
-      const bool more = kt + 1 < n_chunks;
-      int nn0 = -1, nn1 = -1;
-      if (more) {
-        gload(n0, n1);
-        nn0 = pid(2 * kt + 4);
-        nn1 = pid(2 * kt + 5);
-      }
-      if (kt < wave_chunks) {
-        Chunk<HD> c;
-        sread(smem + (kt & 1) * CB, c);
-        if (chunk_interior(2 * kt, page_end, wave_first_pos))
-          process_chunk<HD, false>(c, qf, o, m, l, 2 * kt, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
-        else
-          process_chunk<HD>(c, qf, o, m, l, 2 * kt, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
-      }
-      if (more) {
-        swrite(smem + ((kt + 1) & 1) * CB);
-        n0 = nn0;
-        n1 = nn1;
-      }
-      __syncthreads();
-    }
-    if (row_valid) {
-      const float inv = 1.f / l;
-      uint16_t* op = p.out + qtok * p.out_tok_stride + (int64_t)qhead * HD + 4 * g4;
-#pragma unroll
-      for (int db = 0; db < HD / 16; db++) {
-        u32x2 w;
-        w[0] = pack_bf16x2(o[db][0] * inv, o[db][1] * inv);
-        w[1] = pack_bf16x2(o[db][2] * inv, o[db][3] * inv);
-        *reinterpret_cast<u32x2*>(op + db * 16) = w;
-      }
-    }
-    return;
   }
 
   // Two chunk buffers used in turn: the loads of the next chunk are in flight
@@ -430,6 +528,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
       p.part_ml[part * 2 + 1] = L;
     }
   }
+}
+
+template <int HD>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void paged_attn_kernel(AttnParams p) {
+  __shared__ __attribute__((aligned(16))) char smem[smem_bytes<HD>()];
+  const AttnItem it = p.items[blockIdx.x];
+  const ReqDev rq = p.reqs[it.req];
+  if (it.kind == 1)
+    prefill_item<HD>(p, it, rq, smem);
+  else
+    decode_item<HD>(p, it, rq, smem);
 }
 
 // Deterministic merge of the key splits of one (decode request, q head).

@@ -178,7 +178,7 @@ void build_plan(const mx_batch* b, const mx_attn_shape* s, bool with_items, Plan
   for (int r = 0; r < p.R; r++) {
     const ReqDev& d = p.reqs[r];
     if (d.phase != MX_PREFILL) continue;
-    const int tiles = (int)ceil_div(d.n_new, 64);
+    const int tiles = (int)ceil_div(d.n_new, kPrefillTileRows);
     for (int qt = tiles - 1; qt >= 0; qt--)
       for (int h = 0; h < nq; h++) {
         AttnItem it;
@@ -186,7 +186,7 @@ void build_plan(const mx_batch* b, const mx_attn_shape* s, bool with_items, Plan
         it.head = (int16_t)h;
         it.kind = 1;
         it.nrows = 16;
-        it.start = qt * 64;
+        it.start = qt * kPrefillTileRows;
         it.part = 0;
         p.items.push_back(it);
       }
@@ -197,7 +197,8 @@ void build_plan(const mx_batch* b, const mx_attn_shape* s, bool with_items, Plan
   auto longer = [&](const AttnItem& a, const AttnItem& b) {
     const ReqDev& ra = p.reqs[a.req];
     const ReqDev& rb = p.reqs[b.req];
-    return ra.ctx_len + std::min(a.start + 64, ra.n_new) > rb.ctx_len + std::min(b.start + 64, rb.n_new);
+    return ra.ctx_len + std::min(a.start + kPrefillTileRows, ra.n_new) >
+           rb.ctx_len + std::min(b.start + kPrefillTileRows, rb.n_new);
   };
   // (one prompt's tiles are generated in this order already)
   if (!std::is_sorted(p.items.begin(), p.items.end(), longer))
@@ -563,7 +564,8 @@ MX_EXPORT size_t mx_workspace_bytes(const mx_layer_cfg* cfg, const mx_attn_shape
   const int64_t nq = shape->n_q_heads, nkv = shape->n_kv_heads, group = nq / nkv;
   // every split has at least 8 pages, so splits <= pages / 8 + requests
   const int64_t splits = max_pages / 8 + max_reqs;
-  const int64_t items = splits * nkv * ceil_div(group, 16) + (max_tokens / 64 + max_reqs) * nq;
+  const int64_t items =
+      splits * nkv * ceil_div(group, 16) + (max_tokens / kPrefillTileRows + max_reqs) * nq;
   const int64_t parts = splits * nq;
   const size_t scratch = cfg ? kMaxSplitFloats : 0;
   return make_layout(max_reqs, max_tokens, max_pages, items, max_reqs, parts, shape, cfg, scratch)

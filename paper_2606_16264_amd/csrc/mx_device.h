@@ -62,7 +62,9 @@ struct ReqDev {
 //   kind 0 (decode): q heads [head, head + nrows) of the request's single token,
 //                    pages [start, start + split_pages) of its table; part =
 //                    split index (ignored when the request has one split).
-//   kind 1 (prefill): q head `head`, query rows [start, start + 64) of the request.
+//   kind 1 (prefill): q head `head`, query rows [start, start + kPrefillTileRows)
+//                     of the request.
+constexpr int kPrefillTileRows = 128;  // four waves x two blocks of 16 rows
 struct AttnItem {
   int32_t req;
   int16_t head;

@@ -202,6 +202,24 @@ def test_paged_attn_boundaries(nq, nkv, d):
     say(f"  max row rel err {err:.2e}")
 
 
+# Prefill tiles of 128 query rows (two blocks of 16 per wave): chunks that
+# fill a tile exactly, spill one row into the next, end inside a wave's second
+# block, and continue a cached prefix
+@pytest.mark.parametrize("nq,nkv,d", [(8, 8, 128), (32, 8, 128), (4, 4, 64)])
+def test_paged_attn_prefill_tiles(nq, nkv, d):
+    say(f"case: paged attn prefill tiles nq={nq} nkv={nkv} d={d}")
+    rng = np.random.default_rng(200 + nq + nkv + d)
+    cfg = wl.LayerConfig("t", 256, 256, nq, nkv, d)
+    b = wl.custom_batch(rng, [5, 600], [(128, 0), (129, 40), (256, 7), (383, 300), (17, 0), (48, 1)])
+    c = attention_case(cfg, b, 14, rng)
+    out = torch.empty((b.T, nq, d), dtype=torch.uint16, device="cuda")
+    mx.mx_paged_attn(c["mb"], c["shape"], c["q"], c["k"], c["v"], out, c["ws"])
+    sync()
+    err = assert_rows_close(bits_to_f64(out).reshape(b.T * nq, d), c["exp"].reshape(b.T * nq, d),
+                            what="attention")
+    say(f"  max row rel err {err:.2e}")
+
+
 @pytest.mark.parametrize("key", ["c2", "c4"])
 def test_paged_attn_long_contexts_split(key):
     """Long decode contexts (several key splits and the merge) at a real shape."""
@@ -491,6 +509,39 @@ def test_layer_step_aligned_value_runs(cfg):
     exp = oracle.layer_step(cfg.as_dict(), b.n_new, b.ctx_len, x, w, kp, vp)
     rows = np.arange(b.T)
     check_layer(cfg, b, got, exp, rows, cfg.name, staged_attention(cfg, b, x, w, kp, vp, rows))
+    check_pool_rows(cfg, b, got, exp.k_new, exp.v_new, rows)
+    written = set(oracle.token_map(b.n_new, b.ctx_len, b.page_tables, 16).tok_slot.tolist())
+    assert changed_slots(got["k0"], got["k"], False) <= written
+    assert changed_slots(got["v0"], got["v"], True) <= written
+
+
+# Degenerate batches: a lone decode (T = 1), one-token prefills with and
+# without a cached prefix, a prefill-only batch, a chunk of exactly one tile,
+# and a batch whose only decode sits on a page boundary
+DEGENERATE = {
+    "lone-decode": ([37], []),
+    "one-token-prefill": ([], [(1, 0)]),
+    "one-token-chunk-after-cache": ([], [(1, 300)]),
+    "prefill-only": ([], [(33, 0), (64, 16), (2, 31)]),
+    "one-tile-chunk": ([], [(64, 0)]),
+    "decode-at-page-edge": ([16], [(15, 0)]),
+}
+
+
+@pytest.mark.parametrize("case", list(DEGENERATE))
+def test_layer_step_degenerate_batches(case):
+    say(f"case: layer step degenerate batch {case}")
+    cfg = SMALL_GQA
+    rng = np.random.default_rng(sum(map(ord, case)))
+    dec, pre = DEGENERATE[case]
+    b = wl.custom_batch(rng, dec, pre)
+    w = small_weights(rng, cfg)
+    x = wl.f32_to_bf16_bits(rng.standard_normal((b.T, cfg.hidden), dtype=np.float32))
+    got = run_layer(cfg, b, w, x, 515, keep_before=True)
+    kp, vp = wl.prior_kv_concat(cfg, b, 515)
+    exp = oracle.layer_step(cfg.as_dict(), b.n_new, b.ctx_len, x, w, kp, vp)
+    rows = np.arange(b.T)
+    check_layer(cfg, b, got, exp, rows, case, staged_attention(cfg, b, x, w, kp, vp, rows))
     check_pool_rows(cfg, b, got, exp.k_new, exp.v_new, rows)
     written = set(oracle.token_map(b.n_new, b.ctx_len, b.page_tables, 16).tok_slot.tolist())
     assert changed_slots(got["k0"], got["k"], False) <= written
