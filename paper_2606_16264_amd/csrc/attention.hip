@@ -85,8 +85,17 @@ __device__ __forceinline__ void load_chunk(Chunk<HD>& c, const AttnParams& p, in
 // for score block b, row i).
 struct StepP {
   bf16x8 pb;     // P^T as the B operand: k index i' = 4 b + i <-> key j0 + i'
-  float alpha;   // rescale of the running output
+  float alpha;   // rescale of the running output (1 where the max was kept)
+  bool rescale;  // some row of the wave raised its max (wave-uniform)
 };
+
+// A row's running max m (log2 units) is raised only when a score exceeds it by
+// more than this: the probabilities exp2(x - m) then stay below 2^8, which bf16
+// and fp32 hold at full relative precision, and the output is rescaled only on
+// the steps where some row of the wave raised its max (rarely, past the first
+// keys).  Output and sum always refer to the same m, so the normalised result
+// is the softmax itself.
+constexpr float kLazyMax = 8.0f;
 
 // Score block b of S^T = K Q^T (16 keys x 16 rows).
 template <int HD>
@@ -97,7 +106,8 @@ __device__ __forceinline__ f32x4 score_block(const u32x4 (&kf)[HD / 32], const b
   return s;
 }
 
-// Online-softmax update of this lane's row from its two score blocks.
+// Online-softmax update of this lane's row from its two score blocks (raw
+// scores; the softmax scale, in log2 units, is applied inside the exponent).
 template <bool MASK>
 __device__ __forceinline__ StepP softmax_step(const f32x4 (&s)[2], float& m, float& l, int pi0,
                                               int page_end, int row_pos, float scale_log2, int g4) {
@@ -110,21 +120,22 @@ __device__ __forceinline__ StepP softmax_step(const f32x4 (&s)[2], float& m, flo
 #pragma unroll
     for (int i = 0; i < 4; i++) {
       const int j = j0 + 4 * b + i;
-      const float x = s[b][i] * scale_log2;
-      sv[b][i] = (!MASK || (pvalid && j <= row_pos)) ? x : kNegBig;
+      sv[b][i] = (!MASK || (pvalid && j <= row_pos)) ? s[b][i] : kNegBig;
       mx = fmaxf(mx, sv[b][i]);
     }
   mx = fmaxf(mx, __shfl_xor(mx, 16));
   mx = fmaxf(mx, __shfl_xor(mx, 32));
-  const float m_new = fmaxf(m, mx);
-  const float alpha = exp2f(m - m_new);
+  mx *= scale_log2;  // scale > 0: the max of the scaled scores
+  const bool raise = mx > m + kLazyMax;
+  const float m_new = raise ? mx : m;
+  const float alpha = raise ? exp2f(m - mx) : 1.f;
   float ps = 0.f;
   float pv[2][4];
 #pragma unroll
   for (int b = 0; b < 2; b++)
 #pragma unroll
     for (int i = 0; i < 4; i++) {
-      pv[b][i] = exp2f(sv[b][i] - m_new);
+      pv[b][i] = exp2f(fmaf(sv[b][i], scale_log2, -m_new));
       ps += pv[b][i];
     }
   ps += __shfl_xor(ps, 16);
@@ -136,7 +147,7 @@ __device__ __forceinline__ StepP softmax_step(const f32x4 (&s)[2], float& m, flo
   pb_bits[1] = pack_bf16x2(pv[0][2], pv[0][3]);
   pb_bits[2] = pack_bf16x2(pv[1][0], pv[1][1]);
   pb_bits[3] = pack_bf16x2(pv[1][2], pv[1][3]);
-  return StepP{as_bf16x8(pb_bits), alpha};
+  return StepP{as_bf16x8(pb_bits), alpha, __any(raise) != 0};
 }
 
 // Which of this lane group's eight keys hold values (bf16 lanes of each
@@ -160,6 +171,10 @@ __device__ __forceinline__ void value_keep(int pi0, int page_end, int kv_len, in
 template <int HD, int DB0, int NDB, bool MASK>
 __device__ __forceinline__ void values_part(const u32x4 (&vf)[NDB], f32x4 (&o)[HD / 16], StepP sp,
                                             const uint32_t (&keep)[4]) {
+  if (sp.rescale) {
+#pragma unroll
+    for (int e = 0; e < NDB; e++) o[DB0 + e] = o[DB0 + e] * sp.alpha;
+  }
 #pragma unroll
   for (int e = 0; e < NDB; e++) {
     u32x4 va = vf[e];
@@ -167,7 +182,6 @@ __device__ __forceinline__ void values_part(const u32x4 (&vf)[NDB], f32x4 (&o)[H
 #pragma unroll
       for (int h = 0; h < 4; h++) va[h] &= keep[h];
     }
-    o[DB0 + e] = o[DB0 + e] * sp.alpha;
     o[DB0 + e] = mfma16(as_bf16x8(va), sp.pb, o[DB0 + e]);
   }
 }
