@@ -283,16 +283,15 @@ __device__ __forceinline__ void prefill_item(const AttnParams& p, const AttnItem
   };
   constexpr int KB = SharedChunk<HD>::KBYTES, CB = SharedChunk<HD>::BYTES;
   constexpr int NLD = HD / 32;  // 16-byte loads per lane for a quarter chunk
-  u32x4 st[NLD];
   // waves 0 / 1: keys of the chunk's first / second page; 2 / 3: values
-  auto gload = [&](int pid0, int pid1) {
+  auto gload = [&](u32x4 (&st)[NLD], int pid0, int pid1) {
     const int pg0 = (wave & 1) ? pid1 : pid0;
     const int pg = pg0 >= 0 ? pg0 : safe;  // past the end: masked, like the decode path
     const uint16_t* base = (wave < 2 ? p.k_pool : p.v_pool) + ((int64_t)pg * p.nkv + kvh) * (16 * HD);
 #pragma unroll
     for (int i = 0; i < NLD; i++) st[i] = *reinterpret_cast<const u32x4*>(base + (i * 64 + lane) * 8);
   };
-  auto swrite = [&](char* slot) {
+  auto swrite = [&](char* slot, const u32x4 (&st)[NLD]) {
 #pragma unroll
     for (int i = 0; i < NLD; i++) {
       const int c = i * 64 + lane;
@@ -323,21 +322,18 @@ __device__ __forceinline__ void prefill_item(const AttnParams& p, const AttnItem
       vf[e] = *reinterpret_cast<const u32x4*>(slot + KB + d * 64 + ((g4 ^ ((d >> 2) & 3)) << 4));
     }
   };
-  // one barrier per chunk: chunk kt + 1 is loaded into registers while chunk
-  // kt is processed, and stored into the other slot (read by everyone in the
-  // previous iteration, before its barrier) once the processing is done
-  int n0 = pid(2), n1 = pid(3);
-  gload(pid(0), pid(1));
-  swrite(smem);
-  __syncthreads();
-  for (int kt = 0; kt < n_chunks; kt++) {
-    const bool more = kt + 1 < n_chunks;
-    int nn0 = -1, nn1 = -1;
-    if (more) {
-      gload(n0, n1);
-      nn0 = pid(2 * kt + 4);
-      nn1 = pid(2 * kt + 5);
-    }
+  // Two register stagings used in turn: the loads of chunk kt + 2 are issued
+  // while chunk kt is processed, and chunk kt + 1 (loaded during the previous
+  // step) is then stored into the other LDS slot, which everyone finished
+  // reading before the previous step's barrier; one barrier per chunk.  Page
+  // ids are read one step ahead of their loads and issued before the step's
+  // chunk loads: one counter tracks both, in order, so a wait for a page id
+  // never waits for a chunk in flight.  Chunks past the tile's last one read
+  // the request's first page and are never processed, so every step issues
+  // the same loads.
+  u32x4 sta[NLD], stb[NLD];
+  int f0 = pid(4), f1 = pid(5);  // pages of the chunk the next step loads
+  auto process = [&](int kt) {
     if (kt < wave_chunks) {
       // both row blocks from one read of the chunk's fragments, half a
       // chunk's keys (or values) at a time, each half applied to both
@@ -377,12 +373,29 @@ __device__ __forceinline__ void prefill_item(const AttnParams& p, const AttnItem
       else
         both(std::integral_constant<bool, true>{});
     }
-    if (more) {
-      swrite(smem + ((kt + 1) & 1) * CB);
-      n0 = nn0;
-      n1 = nn1;
-    }
+  };
+  auto step = [&](int kt, u32x4 (&fill)[NLD], const u32x4 (&store)[NLD]) {
+    const int g0 = pid(2 * kt + 6), g1 = pid(2 * kt + 7);  // for the next step
+    __builtin_amdgcn_sched_barrier(0);
+    gload(fill, f0, f1);  // chunk kt + 2
+    __builtin_amdgcn_sched_barrier(0);
+    f0 = g0;
+    f1 = g1;
+    process(kt);
+    swrite(smem + ((kt + 1) & 1) * CB, store);  // chunk kt + 1
     __syncthreads();
+  };
+  {
+    const int a0 = pid(0), a1 = pid(1), b0 = pid(2), b1 = pid(3);
+    gload(sta, a0, a1);
+    gload(stb, b0, b1);
+  }
+  swrite(smem, sta);
+  __syncthreads();
+  for (int kt = 0; kt < n_chunks; kt += 2) {
+    step(kt, sta, stb);
+    if (kt + 1 >= n_chunks) break;
+    step(kt + 1, stb, sta);
   }
   if (row_valid) {
     const float inv = 1.f / l;
