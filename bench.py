@@ -449,8 +449,8 @@ def main():
         print(json.dumps(res))
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1 "
-                                   "(multi-GPU sharding is described in DESIGN.md, not run)"}))
+        print(json.dumps({"error": "the layer step runs on one GPU; --gpus must be 1 "
+                                   "(there is no multi-GPU path)"}))
         sys.exit(2)
     import numpy as np
     import torch
