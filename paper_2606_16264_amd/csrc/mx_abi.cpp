@@ -306,16 +306,28 @@ Layout layout_for(const Plan& p, const mx_attn_shape* s, const mx_layer_cfg* c) 
 }
 
 // ------------------------------------------------------------------ per-device state
+// Metadata staging: kRing pinned host buffers used in turn.  A buffer may be
+// rewritten once the upload that read it has run.  A completion event costs
+// the stream a few microseconds, so one is recorded per group of up to kEvery
+// consecutive uploads on one stream, after the group's last upload, and covers
+// the whole group: a group ends after kEvery uploads, at the last buffer of the
+// ring, or when the next upload is on another stream.  A group never wraps
+// around the ring, so the event that covers buffer i was recorded into a
+// buffer at or after i, which is not reused (and so not re-recorded) before i.
 struct DeviceState {
   std::mutex mu;
   bool init = false;
   static constexpr int kRing = 8;
+  static constexpr int kEvery = 4;
   void* buf[kRing] = {};   // pinned host staging buffers
   void* dbuf[kRing] = {};  // the same buffers as the device reads them
   size_t cap[kRing] = {};
   hipEvent_t ev[kRing] = {};
   bool used[kRing] = {};
+  int cover[kRing] = {};   // buffer whose event covers this buffer's last upload
   int next = 0;
+  int group_first = -1;    // first buffer of the open group (-1: none)
+  hipStream_t group_stream = nullptr;
 };
 
 std::mutex g_dev_mu;
@@ -354,6 +366,19 @@ mx_status device_state(DeviceState** out) {
 // into the workspace (a kernel that reads the buffer through its device
 // mapping).  A staging slot is rewritten or freed only after the event
 // recorded behind its previous copy has completed.
+// Records the open group's event after its last upload (buffer `last`) on the
+// group's stream; every buffer of the group is then covered by it.
+hipError_t close_group(DeviceState* ds, int last) {
+  hipError_t e = hipEventRecord(ds->ev[last], ds->group_stream);
+  if (e != hipSuccess) return e;
+  for (int j = ds->group_first;; j = (j + 1) % DeviceState::kRing) {
+    ds->cover[j] = last;
+    if (j == last) break;
+  }
+  ds->group_first = -1;
+  return hipSuccess;
+}
+
 mx_status upload_meta(const Plan& p, const Layout& L, const mx_attn_shape* s, float theta,
                       void* ws, hipStream_t stream) {
   DeviceState* ds;
@@ -363,8 +388,13 @@ mx_status upload_meta(const Plan& p, const Layout& L, const mx_attn_shape* s, fl
   const int i = ds->next;
   ds->next = (ds->next + 1) % DeviceState::kRing;
   hipError_t e;
+  // the open group is on another stream: close it there first
+  if (ds->group_first >= 0 && ds->group_stream != stream) {
+    if ((e = close_group(ds, (i + DeviceState::kRing - 1) % DeviceState::kRing)) != hipSuccess)
+      return hip_fail(e, "hipEventRecord");
+  }
   if (ds->used[i]) {
-    e = hipEventSynchronize(ds->ev[i]);
+    e = hipEventSynchronize(ds->ev[ds->cover[i]]);
     if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
   }
   if (ds->cap[i] < L.meta_end) {
@@ -397,9 +427,15 @@ mx_status upload_meta(const Plan& p, const Layout& L, const mx_attn_shape* s, fl
   for (int k = 0; k < d / 2; k++) inv[k] = std::pow((double)theta, -2.0 * k / d);
   e = launch_upload(ds->dbuf[i], ws, L.meta_end, stream);
   if (e != hipSuccess) return hip_fail(e, "metadata upload launch");
-  e = hipEventRecord(ds->ev[i], stream);
-  if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
   ds->used[i] = true;
+  if (ds->group_first < 0) {
+    ds->group_first = i;
+    ds->group_stream = stream;
+  }
+  const int size = i - ds->group_first + 1;
+  if (size == DeviceState::kEvery || i == DeviceState::kRing - 1) {
+    if ((e = close_group(ds, i)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  }
   return MX_OK;
 }
 
