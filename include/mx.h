@@ -250,6 +250,14 @@ mx_status mx_debug_gemm(int32_t M, int32_t N, int32_t K, const uint16_t* A, cons
 mx_status mx_debug_gemm_config(int32_t M, int32_t N, int32_t K, const uint16_t* A, const uint16_t* B,
                                uint16_t* C, const uint16_t* R, int32_t epilogue, int32_t tile_cfg,
                                int32_t ksplit, void* ws, size_t ws_bytes, hipStream_t stream);
+/* The same with B in the layer step's packed-weight tile layout: element (n, k) at
+ * ((n / 16) * (K / 32) + k / 32) * 512 + (n % 16) * 32 + k % 32, i.e. 16 x 32 tiles of
+ * 1 KB ordered [N / 16][K / 32].  N % 16 == 0 and K % 32 == 0 (else MX_ERR_UNSUPPORTED).
+ * For tests and tuning sweeps of the layer's own operand layout. */
+mx_status mx_debug_gemm_tiled(int32_t M, int32_t N, int32_t K, const uint16_t* A,
+                              const uint16_t* B_tiled, uint16_t* C, const uint16_t* R,
+                              int32_t epilogue, int32_t tile_cfg, int32_t ksplit, void* ws,
+                              size_t ws_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -29,6 +29,7 @@ EXPORTED = [
     "mx_workspace_bytes", "mx_packed_weights_bytes", "mx_pack_weights", "mx_kv_append",
     "mx_paged_attn", "mx_layer_step", "mx_layer_workspace_offsets", "mx_debug_token_map",
     "mx_debug_gather", "mx_debug_gemm_ws_bytes", "mx_debug_gemm", "mx_debug_gemm_config",
+    "mx_debug_gemm_tiled",
     "mx_profile_enable", "mx_profile_read",
 ]
 
@@ -96,6 +97,7 @@ def _load() -> ctypes.CDLL:
         "mx_debug_gemm_ws_bytes": ([I32, I32, I32], SZ),
         "mx_debug_gemm": ([I32, I32, I32, P, P, P, P, I32, P, SZ, P], ctypes.c_int),
         "mx_debug_gemm_config": ([I32, I32, I32, P, P, P, P, I32, I32, I32, P, SZ, P], ctypes.c_int),
+        "mx_debug_gemm_tiled": ([I32, I32, I32, P, P, P, P, I32, I32, I32, P, SZ, P], ctypes.c_int),
         "mx_profile_enable": ([I32], ctypes.c_int),
         "mx_profile_read": ([ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float),
                              ctypes.POINTER(ctypes.c_int32), I32], I32),
@@ -261,14 +263,20 @@ def mx_debug_gemm_ws_bytes(M: int, N: int, K: int) -> int:
 
 
 def mx_debug_gemm(A, B, C, R=None, epilogue: int = EPI_STORE, ws=None, stream=None,
-                  tile_cfg: int = -1, ksplit: int = 0) -> None:
+                  tile_cfg: int = -1, ksplit: int = 0, b_tiled: bool = False, N: int = None) -> None:
     """C = epi(A B^T); A [M][K], B [N][K], C [M][N] (or [M][N/2] for SwiGLU).
-    tile_cfg >= 0 forces a tile shape and K split (tuning)."""
+    tile_cfg >= 0 forces a tile shape and K split (tuning).  b_tiled: B holds
+    the N x K weights in the packed 16 x 32 tile layout (any shape; pass N)."""
     M, K = A.shape
-    N = B.shape[0]
-    _check(_lib.mx_debug_gemm_config(M, N, K, _ptr(A), _ptr(B), _ptr(C), _ptr(R), epilogue,
-                                     tile_cfg, ksplit, _ptr(ws), 0 if ws is None else ws.numel(),
-                                     _stream(stream)))
+    if b_tiled:
+        if N is None:
+            raise ValueError("b_tiled needs N")
+        fn = _lib.mx_debug_gemm_tiled
+    else:
+        N = B.shape[0]
+        fn = _lib.mx_debug_gemm_config
+    _check(fn(M, N, K, _ptr(A), _ptr(B), _ptr(C), _ptr(R), epilogue, tile_cfg, ksplit, _ptr(ws),
+              0 if ws is None else ws.numel(), _stream(stream)))
 
 
 def mx_profile_enable(on: bool = True) -> None:

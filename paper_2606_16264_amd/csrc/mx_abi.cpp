@@ -880,11 +880,14 @@ MX_EXPORT mx_status mx_debug_gemm(int32_t M, int32_t N, int32_t K, const uint16_
   return mx_debug_gemm_config(M, N, K, A, B, C, R, epilogue, -1, 0, ws, ws_bytes, stream);
 }
 
-MX_EXPORT mx_status mx_debug_gemm_config(int32_t M, int32_t N, int32_t K, const uint16_t* A,
-                                         const uint16_t* B, uint16_t* C, const uint16_t* R,
-                                         int32_t epilogue, int32_t tile_cfg, int32_t ksplit,
-                                         void* ws, size_t ws_bytes, hipStream_t stream) {
+namespace {
+mx_status debug_gemm(int32_t M, int32_t N, int32_t K, const uint16_t* A, const uint16_t* B,
+                     bool b_tiled, uint16_t* C, const uint16_t* R, int32_t epilogue,
+                     int32_t tile_cfg, int32_t ksplit, void* ws, size_t ws_bytes,
+                     hipStream_t stream) {
   g_err.clear();
+  if (b_tiled && (N % 16 || K % 32))
+    return fail(MX_ERR_UNSUPPORTED, "tiled weights need N %% 16 == 0 and K %% 32 == 0");
   if (M < 0 || N <= 0 || K <= 0) return fail(MX_ERR_INVALID, "bad GEMM shape %d x %d x %d", M, N, K);
   if (K % 64) return fail(MX_ERR_UNSUPPORTED, "K %d is not a multiple of 64", K);
   if (tile_cfg < -1 || tile_cfg >= gemm_num_configs())
@@ -910,10 +913,29 @@ MX_EXPORT mx_status mx_debug_gemm_config(int32_t M, int32_t N, int32_t K, const 
   if (st != MX_OK) return st;
   const int ldc = epilogue == EPI_SWIGLU ? N / 2 : N;
   GemmArgs g{A, B, C, R, (float*)ws, M, N, K, K, K, ldc, N, epilogue, {}};
-  set_b_row_major(g);
+  if (b_tiled)
+    set_b_tiled(g);
+  else
+    set_b_row_major(g);
   hipError_t e = launch_gemm_config(g, ws ? ws_bytes / 4 : 0, tile_cfg, ksplit, stream);
   if (e != hipSuccess) return hip_fail(e, "gemm launch");
   return MX_OK;
+}
+}  // namespace
+
+MX_EXPORT mx_status mx_debug_gemm_config(int32_t M, int32_t N, int32_t K, const uint16_t* A,
+                                         const uint16_t* B, uint16_t* C, const uint16_t* R,
+                                         int32_t epilogue, int32_t tile_cfg, int32_t ksplit,
+                                         void* ws, size_t ws_bytes, hipStream_t stream) {
+  return debug_gemm(M, N, K, A, B, false, C, R, epilogue, tile_cfg, ksplit, ws, ws_bytes, stream);
+}
+
+MX_EXPORT mx_status mx_debug_gemm_tiled(int32_t M, int32_t N, int32_t K, const uint16_t* A,
+                                        const uint16_t* B_tiled, uint16_t* C, const uint16_t* R,
+                                        int32_t epilogue, int32_t tile_cfg, int32_t ksplit,
+                                        void* ws, size_t ws_bytes, hipStream_t stream) {
+  return debug_gemm(M, N, K, A, B_tiled, true, C, R, epilogue, tile_cfg, ksplit, ws, ws_bytes,
+                    stream);
 }
 
 MX_EXPORT mx_status mx_profile_enable(int32_t on) {

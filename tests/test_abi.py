@@ -155,6 +155,18 @@ def test_debug_gemm_config_errors(args, status):
     assert st == getattr(mx, status), st
 
 
+@pytest.mark.parametrize("args,status", [
+    ((64, 264, 256, 0, 0, 1), "MX_ERR_UNSUPPORTED"),   # tiled weights need N % 16 == 0
+    ((64, 256, 160, 0, 0, 1), "MX_ERR_UNSUPPORTED"),   # K not a multiple of 64
+    ((64, 256, 256, 0, 5, 1), "MX_ERR_INVALID"),       # tile shape out of range
+])
+def test_debug_gemm_tiled_errors(args, status):
+    M, N, K, epi, cfg, ks = args
+    st = mx.lib().mx_debug_gemm_tiled(M, N, K, 0x1000, 0x2000, 0x3000, 0x4000, epi, cfg, ks,
+                                      0x5000, 16, None)
+    assert st == getattr(mx, status), st
+
+
 def test_misaligned_pointers_rejected_before_device_work():
     cfg = wl.CONFIGS["c1"]
     c = mx_cfg(mx, cfg, 64)

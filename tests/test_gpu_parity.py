@@ -259,10 +259,11 @@ def test_paged_attn_needle():
 CANARY = 0x7FC1  # a NaN pattern no GEMM output takes
 
 
-def gemm_case(M, N, K, epi, tile_cfg=-1, ksplit=0):
+def gemm_case(M, N, K, epi, tile_cfg=-1, ksplit=0, b_tiled=False):
     """C = epi(A B^T) through the C-ABI against the oracle; C sits between two
-    canary rows on each side, which must come back untouched."""
-    say(f"case: gemm M={M} N={N} K={K} epi={epi} cfg={tile_cfg} ksplit={ksplit}")
+    canary rows on each side, which must come back untouched.  b_tiled: the
+    weights go in as the layer step's packed 16 x 32 tiles."""
+    say(f"case: gemm M={M} N={N} K={K} epi={epi} cfg={tile_cfg} ksplit={ksplit} tiled={b_tiled}")
     rng = np.random.default_rng(M + N + K + epi)
     a = wl.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
     w = wl.f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * 0.02)
@@ -276,8 +277,13 @@ def gemm_case(M, N, K, epi, tile_cfg=-1, ksplit=0):
     need = mx.mx_debug_gemm_ws_bytes(M, N, K) if tile_cfg < 0 else \
         (ksplit * M * N * 4 if ksplit > 1 else 0)
     ws = ws_tensor(max(need, 256))
-    mx.mx_debug_gemm(dev(a), dev(w), C, dev(r) if epi == 1 else None, epi, ws,
-                     tile_cfg=tile_cfg, ksplit=ksplit)
+    if b_tiled:
+        wt = np.ascontiguousarray(w.reshape(N // 16, 16, K // 32, 32).transpose(0, 2, 1, 3))
+        mx.mx_debug_gemm(dev(a), dev(wt.reshape(-1)), C, dev(r) if epi == 1 else None, epi, ws,
+                         tile_cfg=tile_cfg, ksplit=ksplit, b_tiled=True, N=N)
+    else:
+        mx.mx_debug_gemm(dev(a), dev(w), C, dev(r) if epi == 1 else None, epi, ws,
+                         tile_cfg=tile_cfg, ksplit=ksplit)
     sync()
     guard = torch.cat([buf16[:lead], buf16[lead + M * ncol:]]).cpu().numpy()
     assert (guard == CANARY).all(), "GEMM wrote outside C"
@@ -316,6 +322,16 @@ def test_gemm_matches_oracle(M, N, K, epi):
 ])
 def test_gemm_forced_tile_shapes(tile_cfg, M, N, K, epi, ksplit):
     gemm_case(M, N, K, epi, tile_cfg=tile_cfg, ksplit=ksplit)
+
+
+# The packed 16 x 32 weight tiles the layer step reads, through every tile shape:
+# ragged M and N (N a multiple of 16 only), every epilogue, with and without a K split
+@pytest.mark.parametrize("tile_cfg", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("M,N,K,epi,ksplit", [
+    (577, 1040, 512, 0, 1), (131, 2048, 1024, 2, 2), (64, 4096, 2048, 1, 4), (300, 784, 768, 1, 1),
+])
+def test_gemm_tiled_weights(tile_cfg, M, N, K, epi, ksplit):
+    gemm_case(M, N, K, epi, tile_cfg=tile_cfg, ksplit=ksplit, b_tiled=True)
 
 
 # N not a multiple of 4: the element-wise split-K reduce (plain and residual)
