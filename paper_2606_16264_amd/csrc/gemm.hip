@@ -5,9 +5,13 @@
 // Design:
 //  - workgroup tile BM x BN, K step 64; waves of 64 lanes each own a WM x WN
 //    sub-tile computed with v_mfma_f32_32x32x16_bf16;
-//  - K is consumed in 32-wide slices through a 4-deep LDS ring filled by the
-//    DMA path (global_load_lds): three slices are in flight while the matrix
-//    cores work on the fourth, and no registers are spent on staging;
+//  - K is consumed in 32-wide slices through an LDS ring (4 stages; 3 for the
+//    shape that puts two workgroups on a CU) filled by the DMA path
+//    (global_load_lds): the other slices are in flight while the matrix cores
+//    work on one, and no registers are spent on staging;
+//  - B is addressed through block, row and K-slice strides: row-major, or the
+//    packed weights' 16 x 32 tiles of 1 KB, where each DMA instruction reads
+//    one contiguous kilobyte;
 //  - fragment reads of the next k-step are issued before the MFMAs of the
 //    current one; one barrier per slice;
 //  - LDS rows are 64 bytes (32 bf16 of K); the 16-byte chunk c of row r is
@@ -16,8 +20,10 @@
 //  - tile order is XCD-aware: workgroup b runs on XCD b % 8, and each XCD is
 //    handed a contiguous run of tiles taken in M-grouped order, so that the
 //    tiles sharing an L2 also share A and B panels;
-//  - small-M problems (weight streaming) split K over a second grid dimension
-//    and finish in a deterministic reduce-and-epilogue kernel.
+//  - a K split runs over a second grid dimension and finishes in a
+//    deterministic reduce-and-epilogue kernel;
+//  - a cost model picks tile shape and K split per problem (a per-CU feed
+//    estimate for few rows, rounds of tile-units for more).
 #include <algorithm>
 #include <cmath>
 
