@@ -31,12 +31,9 @@
  *    with MX_ERR_INVALID.
  *  - Ownership: the caller allocates and owns every device buffer (weights,
  *    pools, activations, workspace) and the stream.  The library keeps no
- *    pointer after a call returns except for work already enqueued, and one
- *    stream handle: the staging ring may record a completion event on the
- *    stream of an earlier call when a later call on this device comes on
- *    another stream, so a stream passed to a call must stay valid until a
- *    later call on the same device uses a different stream (or the process
- *    ends).  Host
+ *    pointer after a call returns except for work already enqueued (a later
+ *    call may record a completion event on the null stream for earlier calls
+ *    made on it; never on another stream).  Host
  *    arrays (the batch) are read during the call only.  The library allocates
  *    nothing per call; on its first call on a device it allocates a small ring
  *    of pinned host staging buffers (grown, rarely, if a batch needs more) that

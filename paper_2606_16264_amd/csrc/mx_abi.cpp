@@ -308,12 +308,15 @@ Layout layout_for(const Plan& p, const mx_attn_shape* s, const mx_layer_cfg* c) 
 // ------------------------------------------------------------------ per-device state
 // Metadata staging: kRing pinned host buffers used in turn.  A buffer may be
 // rewritten once the upload that read it has run.  A completion event costs
-// the stream a few microseconds, so one is recorded per group of up to kEvery
-// consecutive uploads on one stream, after the group's last upload, and covers
-// the whole group: a group ends after kEvery uploads, at the last buffer of the
-// ring, or when the next upload is on another stream.  A group never wraps
-// around the ring, so the event that covers buffer i was recorded into a
-// buffer at or after i, which is not reused (and so not re-recorded) before i.
+// the stream a few microseconds, so on the null stream one is recorded per
+// group of up to kEvery consecutive uploads, after the group's last upload,
+// and covers the whole group: a group ends after kEvery uploads, at the last
+// buffer of the ring, or when the next upload is on another stream.  On any
+// other stream every upload closes its own group in the same call: an event is
+// never recorded on a stream the caller may have destroyed since (the null
+// stream cannot be).  A group never wraps around the ring, so the event that
+// covers buffer i was recorded into a buffer at or after i, which is not
+// reused (and so not re-recorded) before i.
 struct DeviceState {
   std::mutex mu;
   bool init = false;
@@ -433,7 +436,7 @@ mx_status upload_meta(const Plan& p, const Layout& L, const mx_attn_shape* s, fl
     ds->group_stream = stream;
   }
   const int size = i - ds->group_first + 1;
-  if (size == DeviceState::kEvery || i == DeviceState::kRing - 1) {
+  if (stream != nullptr || size == DeviceState::kEvery || i == DeviceState::kRing - 1) {
     if ((e = close_group(ds, i)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   }
   return MX_OK;

@@ -531,6 +531,40 @@ def test_layer_step_aligned_value_runs(cfg):
     assert changed_slots(got["v0"], got["v"], True) <= written
 
 
+def test_layer_step_streams_and_ring():
+    """Twelve layer steps (more than the eight pinned staging buffers), on the
+    null stream and on torch streams that are dropped between calls: every
+    output equals the first null-stream step bit for bit (the step is
+    deterministic and appends the same keys to the same slots)."""
+    say("case: layer step across streams and the staging ring")
+    cfg = wl.CONFIGS["c1"]
+    b = wl.make_batch("c1")
+    w = wl.make_weights(cfg, "c1")
+    x = wl.make_x(cfg, b.T, "c1")
+    c, packed = pack_layer(cfg, b, w)
+    k, v = wdev.alloc_pools(cfg, b.pool_pages)
+    wdev.fill_pools(k, v, cfg, b, wl.kv_seed("c1"), poison=True)
+    mb = mx_batch(mx, b)
+    ws = ws_tensor(mx.mx_workspace_bytes_for(mb, cfg=c))
+    xd = dev(x)
+    ref = torch.empty_like(xd)
+    mx.mx_layer_step(mb, c, packed, xd, ref, k, v, ws)
+    sync()
+    for i, kind in enumerate(["null", "null", "side", "null", "side", "side", "null", "null",
+                              "null", "side", "null", "null"]):
+        y = torch.empty_like(xd)
+        if kind == "null":
+            mx.mx_layer_step(mb, c, packed, xd, y, k, v, ws)
+            sync()
+        else:
+            s = torch.cuda.Stream()
+            s.wait_stream(torch.cuda.current_stream())
+            mx.mx_layer_step(mb, c, packed, xd, y, k, v, ws, stream=s)
+            s.synchronize()
+            del s
+        assert torch.equal(y.view(torch.int16), ref.view(torch.int16)), f"step {i} ({kind})"
+
+
 # Degenerate batches: a lone decode (T = 1), one-token prefills with and
 # without a cached prefix, a prefill-only batch, a chunk of exactly one tile,
 # and a batch whose only decode sits on a page boundary
