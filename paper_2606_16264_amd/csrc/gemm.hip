@@ -15,8 +15,9 @@
 //  - fragment reads of the next k-step are issued before the MFMAs of the
 //    current one; one barrier per slice;
 //  - LDS rows are 64 bytes (32 bf16 of K); the 16-byte chunk c of row r is
-//    stored at c ^ ((r >> 1) & 3), which makes the fragment reads of 8
-//    consecutive rows hit 8 distinct bank groups;
+//    stored at c ^ swz(r), which makes the fragment reads of 16 consecutive
+//    rows hit 16 distinct bank groups (the LDS serves a 16-byte read for 16
+//    lanes at a time from 64 banks);
 //  - tile order is XCD-aware: workgroup b runs on XCD b % 8, and each XCD is
 //    handed a contiguous run of tiles taken in M-grouped order, so that the
 //    tiles sharing an L2 also share A and B panels;
@@ -69,6 +70,13 @@ __device__ __forceinline__ u32x4 lds_read16(unsigned addr) {
 __device__ __forceinline__ void dma16(const void* g, unsigned lds_addr) {
   __builtin_amdgcn_global_load_lds(g, (MX_LDS void*)(size_t)lds_addr, 16, 0, 0);
 }
+
+// Chunk swizzle of LDS row r: 16-byte chunk c is stored at c ^ swz(r).  A
+// 16-lane phase of a fragment read (rows r0 .. r0 + 15, one logical chunk)
+// then touches 16 distinct bank groups of 16 bytes: row r sits in group
+// 4 (r % 4) + chunk of its 256 bytes, and swz takes all four values over
+// r >> 2 for each r % 4.  (The same holds for 8-row phases over 32 banks.)
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) & 3) ^ ((r >> 3) & 1); }
 
 __device__ __forceinline__ void tile_coords(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
   const int nt = tiles_m * tiles_n;
@@ -356,15 +364,14 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
 
   // DMA: instruction j (wave w issues j = w L .. w L + L - 1) fills rows
   // 16 j .. 16 j + 15 of the stacked A|B tile; lane l lands at row 16 j + l / 4,
-  // stored chunk l % 4, which holds logical chunk (l % 4) ^ ((row >> 1) & 3).
-  // That XOR makes the fragment reads of 8 consecutive rows conflict-free.
+  // stored chunk l % 4, which holds logical chunk (l % 4) ^ swz(row).
   // (an instruction's 16 rows are all A or all B: BM is a multiple of 16)
   const uint16_t* src[L];
   int64_t kstep[L];
 #pragma unroll
   for (int i = 0; i < L; i++) {
     const int row = (wave * L + i) * 16 + (lane >> 2);
-    const int c = (lane & 3) ^ ((row >> 1) & 3);
+    const int c = (lane & 3) ^ swz(row);
     if (row < BM) {
       src[i] = a.A + (int64_t)min(m0 + row, a.M - 1) * a.lda + kbeg + c * 8;
       kstep[i] = BKS;
@@ -395,12 +402,12 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
 #pragma unroll
   for (int i = 0; i < MB; i++) {
     const int r = wave_m * WM + i * 32 + frow;
-    aoff[i] = r * ROWB + (((unsigned)fk ^ ((r >> 1) & 3)) << 4);
+    aoff[i] = r * ROWB + (((unsigned)fk ^ swz(r)) << 4);
   }
 #pragma unroll
   for (int j = 0; j < NB; j++) {
     const int r = wave_n * WN + j * 32 + frow;
-    boff[j] = (BM + r) * ROWB + (((unsigned)fk ^ ((r >> 1) & 3)) << 4);
+    boff[j] = (BM + r) * ROWB + (((unsigned)fk ^ swz(r)) << 4);
   }
   // k-step ks of a stage reads logical chunk 2 ks + fk; the XOR with the row
   // term commutes with the +2 (bit 1 only), so ks = 1 is the base ^ 32 bytes
