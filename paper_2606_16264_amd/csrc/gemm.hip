@@ -609,8 +609,9 @@ constexpr int kFeedMaxM = 256;  // rows up to which the feed estimate is used
 // streaming the operands from HBM once.  A K split adds the fp32 partial round
 // trip and the reduce launch.  (Both fitted on cold timings of the layer GEMMs
 // of the four layer shapes at their decode-only and mixed token counts, every
-// tile shape and K split: the picks are within 0.14% of the best measured in
-// total, 5% faster than one round-based estimate alone on the decode sizes.)
+// tile shape and K split: the picks are within 0.1-0.2% of the best measured
+// in total and within 1% on the decode sizes, where the round-based estimate
+// alone was 1.7-2.4% above the best.)
 Plan choose(int M, int N, int K) {
   const double cus = 256.0, hbm = 5.0e12;
   const bool feed = M <= kFeedMaxM;
