@@ -247,8 +247,10 @@ mx_status mx_debug_gemm(int32_t M, int32_t N, int32_t K, const uint16_t* A, cons
                         hipStream_t stream);
 /* The same with a forced tile shape (0: 256x256, 1: 128x256, 2: 128x128, 3: 64x128,
  * 4: 128x256 with a shallower LDS ring, two workgroups per CU;
- * -1: the library's own choice) and K split (ws must hold ksplit * M * N floats
- * when ksplit > 1).  For tuning sweeps. */
+ * -1: the library's own choice) and K split: 1 <= ksplit <= min(64, K / 64), else
+ * MX_ERR_INVALID; split z takes the 64-wide K chunks [z C / ksplit, (z + 1) C / ksplit)
+ * of the C = K / 64, so ksplit need not divide C.  ws must hold ksplit * M * N floats
+ * when ksplit > 1.  For tuning sweeps. */
 mx_status mx_debug_gemm_config(int32_t M, int32_t N, int32_t K, const uint16_t* A, const uint16_t* B,
                                uint16_t* C, const uint16_t* R, int32_t epilogue, int32_t tile_cfg,
                                int32_t ksplit, void* ws, size_t ws_bytes, hipStream_t stream);

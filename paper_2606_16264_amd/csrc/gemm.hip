@@ -21,8 +21,9 @@
 //  - tile order is XCD-aware: workgroup b runs on XCD b % 8, and each XCD is
 //    handed a contiguous run of tiles taken in M-grouped order, so that the
 //    tiles sharing an L2 also share A and B panels;
-//  - a K split runs over a second grid dimension and finishes in a
-//    deterministic reduce-and-epilogue kernel;
+//  - a K split runs over a second grid dimension (split z of S takes the
+//    64-wide K chunks [z C / S, (z + 1) C / S) of the C in K, so S need not
+//    divide C) and finishes in a deterministic reduce-and-epilogue kernel;
 //  - a cost model picks tile shape and K split per problem (a per-CU feed
 //    estimate for few rows, rounds of tile-units for more).
 #include <algorithm>
@@ -337,7 +338,7 @@ __device__ __forceinline__ void store_epilogue(const f32x16 (&acc)[MB][NB], int 
 template <int BM, int BN, int WM, int WN, int NS, int EPI, bool SPLIT>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmArgs a, int tiles_m,
                                                                            int tiles_n,
-                                                                           int k_per_split) {
+                                                                           int k_chunks) {
   constexpr int WAVES_N = BN / WN;
   constexpr int NWAVES = (BM / WM) * WAVES_N;
   constexpr int MB = WM / 32, NB = WN / 32;
@@ -359,8 +360,9 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int kz = blockIdx.y;
-  const int kbeg = kz * k_per_split;
-  const int nk = k_per_split / BKS;
+  const int c_beg = kz * k_chunks / (int)gridDim.y, c_end = (kz + 1) * k_chunks / (int)gridDim.y;
+  const int kbeg = c_beg * BK;
+  const int nk = (c_end - c_beg) * (BK / BKS);
 
   // DMA: instruction j (wave w issues j = w L .. w L + L - 1) fills rows
   // 16 j .. 16 j + 15 of the stacked A|B tile; lane l lands at row 16 j + l / 4,
@@ -621,18 +623,19 @@ Plan choose(int M, int N, int K) {
     const int BM = kShapes[c].BM, BN = kShapes[c].BN;
     const double tiles = (double)((M + BM - 1) / BM) * ((N + BN - 1) / BN);
     for (int ks = 1; ks <= 8; ks *= 2) {
-      if (K % (BK * ks) != 0 || K / ks < 4 * BK) break;
+      if ((K / BK) / ks < 4) break;  // every split at least four 64-wide K chunks
       if (ks > 1 && (double)ks * M * N > (double)kMaxSplitFloats) break;
       const double split_mb = ((double)ks * M * N * 8.0 + 2.0 * M * N) / 1e6;
+      const double k_unit = (double)((K / BK + ks - 1) / ks * BK);  // the longest split
       double t;
       if (feed) {
         const double per_cu = std::ceil(tiles * ks / cus);
-        const double unit_bytes = (double)(BN + std::min(BM, M)) * (K / ks) * 2.0;
+        const double unit_bytes = (double)(BN + std::min(BM, M)) * k_unit * 2.0;
         t = per_cu * unit_bytes / (kShapes[c].feed_gbs * 1e3) + 12.06 +
             (ks > 1 ? 0.157 * split_mb + 0.15 : 0.0);
       } else {
         const double rounds = std::ceil(tiles * ks / (cus * kShapes[c].per_cu));
-        const double t_units = rounds * (kShapes[c].a_us + kShapes[c].b_us_per_k * (double)(K / ks));
+        const double t_units = rounds * (kShapes[c].a_us + kShapes[c].b_us_per_k * k_unit);
         const double t_mem = 2.0 * ((double)N * K + (double)M * K) / hbm * 1e6;
         t = std::max(t_units, t_mem) + (ks > 1 ? 0.197 * split_mb + 3.39 : 0.0);
       }
@@ -652,7 +655,7 @@ hipError_t run(const GemmArgs& a, int ksplit, hipStream_t stream) {
   const size_t lds = (size_t)NS * (BM + BN) * BKS * 2;
   dim3 grid(tiles_m * tiles_n, ksplit);
   gemm_kernel<BM, BN, WM, WN, NS, EPI, SPLIT><<<grid, threads, lds, stream>>>(a, tiles_m, tiles_n,
-                                                                          a.K / ksplit);
+                                                                          a.K / BK);
   return hipGetLastError();
 }
 
@@ -741,7 +744,7 @@ hipError_t launch_gemm_config(const GemmArgs& a, size_t ws_floats, int cfg, int 
   if (cfg >= 0 && cfg < kNumShapes) {
     p.cfg = cfg;
     p.ksplit = ksplit >= 1 ? ksplit : 1;
-    if (a.K % (BK * p.ksplit) != 0) return hipErrorInvalidValue;
+    if (a.K / BK < p.ksplit) return hipErrorInvalidValue;
   }
   if (p.ksplit > 1 && (size_t)p.ksplit * a.M * a.N > ws_floats) p.ksplit = 1;
   switch (p.cfg) {

@@ -895,8 +895,8 @@ mx_status debug_gemm(int32_t M, int32_t N, int32_t K, const uint16_t* A, const u
   if (K % 64) return fail(MX_ERR_UNSUPPORTED, "K %d is not a multiple of 64", K);
   if (tile_cfg < -1 || tile_cfg >= gemm_num_configs())
     return fail(MX_ERR_INVALID, "tile config %d out of range", tile_cfg);
-  if (tile_cfg >= 0 && (ksplit < 1 || ksplit > 64 || K % (64 * ksplit) != 0))
-    return fail(MX_ERR_INVALID, "K split %d does not divide K %d into multiples of 64", ksplit, K);
+  if (tile_cfg >= 0 && (ksplit < 1 || ksplit > 64 || K / 64 < ksplit))
+    return fail(MX_ERR_INVALID, "K split %d is not in [1, min(64, K / 64 = %d)]", ksplit, K / 64);
   if (epilogue < 0 || epilogue > 2) return fail(MX_ERR_INVALID, "bad epilogue %d", epilogue);
   if (epilogue == EPI_SWIGLU && N % 64) return fail(MX_ERR_UNSUPPORTED, "SwiGLU needs N % 64 == 0");
   if (M == 0) return MX_OK;

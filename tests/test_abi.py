@@ -140,7 +140,7 @@ def test_workspace_bound_covers_batch(key, P):
     ((64, 256, 256, 0, 5, 1), "MX_ERR_INVALID"),       # tile shape out of range
     ((64, 256, 256, 0, -2, 1), "MX_ERR_INVALID"),
     ((64, 256, 256, 0, 0, 0), "MX_ERR_INVALID"),       # forced shape without a split count
-    ((64, 256, 256, 0, 0, 3), "MX_ERR_INVALID"),       # split not dividing K into 64s
+    ((64, 256, 256, 0, 0, 5), "MX_ERR_INVALID"),       # more splits than 64-wide K chunks
     ((64, 256, 160, 0, 0, 1), "MX_ERR_UNSUPPORTED"),   # K not a multiple of 64
     ((-1, 256, 256, 0, 0, 1), "MX_ERR_INVALID"),       # negative M
     ((64, 96, 256, 2, 0, 1), "MX_ERR_UNSUPPORTED"),    # SwiGLU needs N % 64 == 0

@@ -341,6 +341,16 @@ def test_gemm_ragged_n_split(tile_cfg, M, N, K, epi, ksplit):
     gemm_case(M, N, K, epi, tile_cfg=tile_cfg, ksplit=ksplit)
 
 
+# K splits that do not divide the K / 64 chunks: split z takes chunks
+# [z C / S, (z + 1) C / S), so the splits differ in length by one chunk
+@pytest.mark.parametrize("tile_cfg,b_tiled", [(3, False), (1, False), (3, True), (0, True)])
+@pytest.mark.parametrize("M,N,K,epi,ksplit", [
+    (70, 640, 320, 1, 3), (131, 1024, 1344, 0, 8), (64, 2048, 11008, 1, 8), (33, 768, 704, 2, 5),
+])
+def test_gemm_uneven_split(tile_cfg, b_tiled, M, N, K, epi, ksplit):
+    gemm_case(M, N, K, epi, tile_cfg=tile_cfg, ksplit=ksplit, b_tiled=b_tiled)
+
+
 # ----------------------------------------------------------------------- layer step
 def pack_layer(cfg, b, w):
     c = mx_cfg(mx, cfg, b.pool_pages)
