@@ -611,9 +611,13 @@ constexpr int kFeedMaxM = 256;  // rows up to which the feed estimate is used
 // streaming the operands from HBM once.  A K split adds the fp32 partial round
 // trip and the reduce launch.  (Both fitted on cold timings of the layer GEMMs
 // of the four layer shapes at their decode-only and mixed token counts, every
-// tile shape and K split: the picks are within 0.1-0.2% of the best measured
-// in total and within 1% on the decode sizes, where the round-based estimate
-// alone was 1.7-2.4% above the best.)
+// tile shape and K split of 1, 2, 4 or 8: the picks are within 0.1-0.2% of the
+// best measured in total and within 1% on the decode sizes, where the
+// round-based estimate alone was 1.7-2.4% above the best.)  Every split from 1
+// to 8 is a candidate: where the model moves to a split of 3, 5 or 6, the
+// measured time fell on 10 of 11 such problems (7B down projection at 576 rows
+// 92.8 -> 74.6 us with 128 x 256 tiles split three ways; Llama-3-8B down at
+// 2304 rows 343.7 -> 304.7 us) and rose by 0.9% on the eleventh.
 Plan choose(int M, int N, int K) {
   const double cus = 256.0, hbm = 5.0e12;
   const bool feed = M <= kFeedMaxM;
@@ -622,7 +626,7 @@ Plan choose(int M, int N, int K) {
   for (int c = 0; c < kNumShapes; c++) {
     const int BM = kShapes[c].BM, BN = kShapes[c].BN;
     const double tiles = (double)((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-    for (int ks = 1; ks <= 8; ks *= 2) {
+    for (int ks = 1; ks <= 8; ks++) {
       if ((K / BK) / ks < 4) break;  // every split at least four 64-wide K chunks
       if (ks > 1 && (double)ks * M * N > (double)kMaxSplitFloats) break;
       const double split_mb = ((double)ks * M * N * 8.0 + 2.0 * M * N) / 1e6;

@@ -115,8 +115,9 @@ inline void set_b_tiled(GemmArgs& g) {
 
 // Chooses a tile shape and split for the problem; ws_floats is the fp32
 // scratch available at args.partial.  A K split never needs more than
-// kMaxSplitFloats of scratch.
-constexpr size_t kMaxSplitFloats = size_t(16) << 20;
+// kMaxSplitFloats of scratch (256 MB: enough for a three-way split of the
+// down projection at a few thousand rows, where it saves 10-20%).
+constexpr size_t kMaxSplitFloats = size_t(64) << 20;
 hipError_t launch_gemm(const GemmArgs& args, size_t ws_floats, hipStream_t stream);
 // The same with a forced tile shape (index < gemm_num_configs()) and K split;
 // cfg < 0 uses the cost model.
