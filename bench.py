@@ -32,7 +32,7 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=int(os.environ.get("WORLD_SIZE", "1")))
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--config", default="c2", help="layer shape c1..c5")
     ap.add_argument("--prefill", type=int, nargs="*", default=None,
                     help="mixed prefill tokens per point (default: the shape's sweep)")
