@@ -140,6 +140,96 @@ __device__ __forceinline__ void rmsnorm_row(const uint16_t* __restrict__ x,
   for (int c = threadIdx.x; c < nchunk; c += 256) rms_scale_store(xr[c], gr[c], inv, outr + c);
 }
 
+// The split-K reduce of a residual GEMM fused with the RMSNorm of its output,
+// one row per block of 512 threads: x1 = bf16(sum_z partial[z] + R), the sums
+// taken in split order and then the residual, exactly as the stand-alone
+// reduce does, and h = RMSNorm(x1, g) from the rounded x1, exactly as
+// rmsnorm_row does; the row stays in registers between the two (rows of up to
+// 2 * 512 * 8 elements).  Every plane's loads of a thread are issued before
+// the first sum, so that the planes cost one memory round trip, not one each.
+constexpr int kNormThreads = 512;
+constexpr int kNormChunks = 2;  // 16-byte chunks per thread
+constexpr int kNormPlanes = 8;  // planes loaded ahead; more are summed one by one
+
+__global__ __launch_bounds__(kNormThreads) void reduce_residual_rmsnorm_kernel(
+    const float* __restrict__ partial, int ksplit, const uint16_t* __restrict__ R,
+    uint16_t* __restrict__ x1, const uint16_t* __restrict__ g, uint16_t* __restrict__ h, int M,
+    int H, float eps) {
+  __shared__ float red[kNormThreads / 64];
+  const int64_t row = blockIdx.x;
+  const int nchunk = H / 8;
+  const int64_t plane4 = (int64_t)M * H / 4;  // one plane in f32x4
+  const f32x4* prow = reinterpret_cast<const f32x4*>(partial + row * H);
+  const u32x4* rrow = reinterpret_cast<const u32x4*>(R + row * H);
+  const u32x4* gr = reinterpret_cast<const u32x4*>(g);
+  u32x4* xrow = reinterpret_cast<u32x4*>(x1 + row * H);
+  u32x4* hrow = reinterpret_cast<u32x4*>(h + row * H);
+  f32x4 pl[kNormChunks][kNormPlanes][2];
+  u32x4 r[kNormChunks], gv[kNormChunks], v[kNormChunks];
+#pragma unroll
+  for (int k = 0; k < kNormChunks; k++) {
+    const int c = threadIdx.x + k * kNormThreads;
+    const bool in = c < nchunk;
+#pragma unroll
+    for (int z = 0; z < kNormPlanes; z++) {
+      if (in && z < ksplit) {
+        pl[k][z][0] = prow[z * plane4 + 2 * c];
+        pl[k][z][1] = prow[z * plane4 + 2 * c + 1];
+      }
+    }
+    r[k] = in ? rrow[c] : u32x4{0, 0, 0, 0};
+    gv[k] = in ? gr[c] : u32x4{0, 0, 0, 0};
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int k = 0; k < kNormChunks; k++) {
+    const int c = threadIdx.x + k * kNormThreads;
+    v[k] = u32x4{0, 0, 0, 0};
+    if (c >= nchunk) continue;
+    f32x4 lo = pl[k][0][0], hi = pl[k][0][1];
+#pragma unroll
+    for (int z = 1; z < kNormPlanes; z++) {
+      if (z < ksplit) {
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+          lo[j] += pl[k][z][0][j];
+          hi[j] += pl[k][z][1][j];
+        }
+      }
+    }
+    for (int z = kNormPlanes; z < ksplit; z++) {
+      const f32x4 plo = prow[z * plane4 + 2 * c], phi = prow[z * plane4 + 2 * c + 1];
+#pragma unroll
+      for (int j = 0; j < 4; j++) {
+        lo[j] += plo[j];
+        hi[j] += phi[j];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 2; j++) {
+      v[k][j] = pack_bf16x2(lo[2 * j] + __uint_as_float(r[k][j] << 16),
+                            lo[2 * j + 1] + __uint_as_float(r[k][j] & 0xFFFF0000u));
+      v[k][2 + j] = pack_bf16x2(hi[2 * j] + __uint_as_float(r[k][2 + j] << 16),
+                                hi[2 * j + 1] + __uint_as_float(r[k][2 + j] & 0xFFFF0000u));
+    }
+    xrow[c] = v[k];
+    ss += sum_squares(v[k]);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < kNormThreads / 64; w++) tot += red[w];
+  const float inv = 1.0f / sqrtf(tot / (float)H + eps);
+#pragma unroll
+  for (int k = 0; k < kNormChunks; k++) {
+    const int c = threadIdx.x + k * kNormThreads;
+    if (c < nchunk) rms_scale_store(v[k], gv[k], inv, hrow + c);
+  }
+}
+
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict__ x,
                                                       const uint16_t* __restrict__ g,
                                                       uint16_t* __restrict__ out, int H,
@@ -297,6 +387,17 @@ hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* g, uint16_t* out, i
                           float eps, hipStream_t stream) {
   if (T == 0) return hipSuccess;
   rmsnorm_kernel<<<T, 256, 0, stream>>>(x, g, out, H, eps);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_residual_rmsnorm(const float* partial, int ksplit, const uint16_t* R,
+                                          uint16_t* x1, const uint16_t* g, uint16_t* h, int M,
+                                          int H, float eps, hipStream_t stream) {
+  if (M == 0) return hipSuccess;
+  if (H % 8 != 0 || H / 8 > kNormChunks * kNormThreads || ksplit < 1)
+    return hipErrorInvalidValue;
+  reduce_residual_rmsnorm_kernel<<<M, kNormThreads, 0, stream>>>(partial, ksplit, R, x1, g, h, M,
+                                                                 H, eps);
   return hipGetLastError();
 }
 

@@ -663,11 +663,13 @@ hipError_t run(const GemmArgs& a, int ksplit, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// reduce = false: a K split leaves its fp32 planes at a.partial for the caller
+// to reduce.
 template <int BM, int BN, int WM, int WN, int NS>
-hipError_t run_shape(const GemmArgs& a, int ksplit, hipStream_t stream) {
+hipError_t run_shape(const GemmArgs& a, int ksplit, bool reduce, hipStream_t stream) {
   if (ksplit > 1) {
     hipError_t e = run<BM, BN, WM, WN, NS, EPI_STORE, true>(a, ksplit, stream);
-    if (e != hipSuccess) return e;
+    if (e != hipSuccess || !reduce) return e;
     const bool paired = a.epilogue == EPI_SWIGLU || a.epilogue == EPI_QKV;
     const int64_t total = (int64_t)a.M * (paired ? a.N / 2 : a.N);
     const int blocks = (int)std::min<int64_t>((total + 255) / 256, 4096);
@@ -741,6 +743,18 @@ hipError_t launch_gemm(const GemmArgs& a, size_t ws_floats, hipStream_t stream) 
 
 int gemm_num_configs() { return kNumShapes; }
 
+namespace {
+hipError_t launch_plan(const GemmArgs& a, Plan p, bool reduce, hipStream_t stream) {
+  switch (p.cfg) {
+    case 0: return run_shape<256, 256, 128, 64, 4>(a, p.ksplit, reduce, stream);
+    case 1: return run_shape<128, 256, 64, 64, 4>(a, p.ksplit, reduce, stream);
+    case 2: return run_shape<128, 128, 64, 64, 4>(a, p.ksplit, reduce, stream);
+    case 3: return run_shape<64, 128, 32, 64, 4>(a, p.ksplit, reduce, stream);
+    default: return run_shape<128, 256, 64, 64, 3>(a, p.ksplit, reduce, stream);
+  }
+}
+}  // namespace
+
 hipError_t launch_gemm_config(const GemmArgs& a, size_t ws_floats, int cfg, int ksplit,
                               hipStream_t stream) {
   if (a.M == 0) return hipSuccess;
@@ -751,13 +765,17 @@ hipError_t launch_gemm_config(const GemmArgs& a, size_t ws_floats, int cfg, int 
     if (a.K / BK < p.ksplit) return hipErrorInvalidValue;
   }
   if (p.ksplit > 1 && (size_t)p.ksplit * a.M * a.N > ws_floats) p.ksplit = 1;
-  switch (p.cfg) {
-    case 0: return run_shape<256, 256, 128, 64, 4>(a, p.ksplit, stream);
-    case 1: return run_shape<128, 256, 64, 64, 4>(a, p.ksplit, stream);
-    case 2: return run_shape<128, 128, 64, 64, 4>(a, p.ksplit, stream);
-    case 3: return run_shape<64, 128, 32, 64, 4>(a, p.ksplit, stream);
-    default: return run_shape<128, 256, 64, 64, 3>(a, p.ksplit, stream);
-  }
+  return launch_plan(a, p, true, stream);
+}
+
+hipError_t launch_gemm_unreduced(const GemmArgs& a, size_t ws_floats, int* ksplit,
+                                 hipStream_t stream) {
+  *ksplit = 1;
+  if (a.M == 0) return hipSuccess;
+  Plan p = choose(a.M, a.N, a.K);
+  if (p.ksplit > 1 && (size_t)p.ksplit * a.M * a.N > ws_floats) p.ksplit = 1;
+  *ksplit = p.ksplit;
+  return launch_plan(a, p, false, stream);
 }
 
 }  // namespace mx

@@ -777,17 +777,26 @@ MX_EXPORT mx_status mx_layer_step(const mx_batch* batch, const mx_layer_cfg* cfg
                                      (int)p.merges.size(), d, stream);
           }), "attention launch")
   }
-  // a7: output projection + residual
+  // a7 + a8: output projection + residual, then RMSNorm 2.  When the
+  // projection is split over K, its reduce, the residual and the norm run as
+  // one kernel (timed as rmsnorm_2), which reads the fp32 planes once and
+  // keeps each x1 row in registers for the norm.
   {
     GemmArgs g{o, (const uint16_t*)(P + W.o), x1, x, scratch, M, H, nq * d, nq * d, nq * d, H, H, EPI_RESIDUAL, {}};
     set_b_tiled(g);
-    MX_CK(timed("gemm_o", stream, [&] { return launch_gemm(g, L.scratch_floats, stream); }),
-          "o gemm launch")
+    const uint16_t* g2 = (const uint16_t*)(P + W.g2);
+    const bool fuse = H <= 8192;  // a row in registers: H / 8 chunks over 256 threads, 4 each
+    int ks = 1;
+    MX_CK(timed("gemm_o", stream, [&] {
+            return fuse ? launch_gemm_unreduced(g, L.scratch_floats, &ks, stream)
+                        : launch_gemm(g, L.scratch_floats, stream);
+          }), "o gemm launch")
+    MX_CK(timed("rmsnorm_2", stream, [&] {
+            return ks > 1 ? launch_reduce_residual_rmsnorm(scratch, ks, x, x1, g2, h, M, H,
+                                                           cfg->rms_eps, stream)
+                          : launch_rmsnorm(x1, g2, h, M, H, cfg->rms_eps, stream);
+          }), "rmsnorm launch")
   }
-  // a8: RMSNorm 2
-  MX_CK(timed("rmsnorm_2", stream, [&] {
-          return launch_rmsnorm(x1, (const uint16_t*)(P + W.g2), h, M, H, cfg->rms_eps, stream);
-        }), "rmsnorm launch")
   // a9: gate/up projection + SwiGLU
   {
     GemmArgs g{h, (const uint16_t*)(P + W.gu), act, nullptr, scratch, M, 2 * F, H, H, H, F, 0, EPI_SWIGLU, {}};

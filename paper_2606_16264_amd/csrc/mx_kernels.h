@@ -53,6 +53,13 @@ hipError_t launch_prologue(const ReqDev* reqs, int R, int T, const int32_t* page
 hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* g, uint16_t* out, int T, int H,
                           float eps, hipStream_t stream);
 
+// The residual split-K reduce fused with the RMSNorm of its result:
+// x1 = bf16(sum_z partial[z] + R) over [M][H] fp32 planes (R, x1 [M][H] bf16),
+// then h = RMSNorm(x1, g).  H % 8 == 0 and H <= 8192.
+hipError_t launch_reduce_residual_rmsnorm(const float* partial, int ksplit, const uint16_t* R,
+                                          uint16_t* x1, const uint16_t* g, uint16_t* h, int M,
+                                          int H, float eps, hipStream_t stream);
+
 // KV append of given k/v rows [T][nkv][d] into the pools.
 hipError_t launch_kv_append(const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_pool,
                             uint16_t* v_pool, const int64_t* tok_slot, int T, int nkv, int d,
@@ -123,6 +130,11 @@ hipError_t launch_gemm(const GemmArgs& args, size_t ws_floats, hipStream_t strea
 // cfg < 0 uses the cost model.
 hipError_t launch_gemm_config(const GemmArgs& args, size_t ws_floats, int cfg, int ksplit,
                               hipStream_t stream);
+// The cost model's plan without the split-K reduce: with a K split (*ksplit > 1
+// on return) the fp32 planes are left at args.partial, [*ksplit][M][N], and
+// args' epilogue is not applied; without one the GEMM runs with its epilogue.
+hipError_t launch_gemm_unreduced(const GemmArgs& args, size_t ws_floats, int* ksplit,
+                                 hipStream_t stream);
 int gemm_num_configs();
 size_t gemm_scratch_floats(int M, int N, int K);
 hipError_t gemm_init();

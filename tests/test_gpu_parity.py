@@ -541,6 +541,30 @@ def test_layer_step_aligned_value_runs(cfg):
     assert changed_slots(got["v0"], got["v"], True) <= written
 
 
+MEDIUM_MHA = wl.LayerConfig("medium-mha", 1536, 2816, 12, 12, 128)
+
+
+def test_layer_step_split_reduces_all_rows():
+    """A 90-row batch of a 1536-wide layer on which every projection is split
+    over K (QKV three ways, gate/up four, down seven: 44 K chunks in uneven
+    splits), so every split reduce runs: the QKV one with RoPE and the KV
+    append, the SwiGLU one, the residual one, and the output projection's
+    reduce fused with the residual and the second RMSNorm.  Every row of every
+    stage and every new slot is checked against the oracle."""
+    say("case: layer step, every projection split over K (all rows)")
+    cfg = MEDIUM_MHA
+    rng = np.random.default_rng(17)
+    b = wl.custom_batch(rng, rng.integers(8, 300, size=60), [(30, 0)])
+    w = small_weights(rng, cfg)
+    x = wl.f32_to_bf16_bits(rng.standard_normal((b.T, cfg.hidden), dtype=np.float32))
+    got = run_layer(cfg, b, w, x, 2929)
+    kp, vp = wl.prior_kv_concat(cfg, b, 2929)
+    exp = oracle.layer_step(cfg.as_dict(), b.n_new, b.ctx_len, x, w, kp, vp)
+    rows = np.arange(b.T)
+    check_layer(cfg, b, got, exp, rows, cfg.name, staged_attention(cfg, b, x, w, kp, vp, rows))
+    check_pool_rows(cfg, b, got, exp.k_new, exp.v_new, rows)
+
+
 def test_layer_step_streams_and_ring():
     """Twelve layer steps (more than the eight pinned staging buffers), on the
     null stream and on torch streams that are dropped between calls: every
