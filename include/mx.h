@@ -226,9 +226,10 @@ mx_status mx_debug_gather(const mx_batch* batch, const mx_attn_shape* shape, int
 /* Launch timing, for profiling.  When enabled, every kernel launch of
  * mx_layer_step and mx_paged_attn is bracketed by two hipEvents recorded on the
  * caller's stream (the launch's own stream), tagged with the step it performs
- * ("token_map", "rmsnorm_1", "gemm_qkv", "paged_attn", "gemm_o", "rmsnorm_2",
+ * ("token_map+rmsnorm_1", "gemm_qkv", "paged_attn", "gemm_o", "rmsnorm_2",
  * "gemm_gate_up", "gemm_down"; a tag covers a split-K GEMM's reduce and the
- * attention's split merge).  Off by default. */
+ * attention's split merge, except that a split output projection's reduce runs
+ * fused with the second RMSNorm and is timed as "rmsnorm_2").  Off by default. */
 mx_status mx_profile_enable(int32_t on);
 /* Waits for the recorded events, accumulates their durations per tag and
  * returns the number of tags written (at most max_entries): names[i] is a
