@@ -6,10 +6,12 @@ with decodes): token map, RMSNorm, QKV GEMM, RoPE + KV append, paged attention
 GEMM + SwiGLU, down GEMM + residual.  Inputs are synthetic, seeded, and
 resident in HBM before the timed region.
 
-Default workload: the Llama-7B-shaped layer (hidden 4096, 32 x 128 MHA, FFN
-11008) with 64 decodes (contexts uniform in [512, 2048]) plus one 512-token
-prefill chunk; the decode-only point (P = 0) is timed beside it to give the
-latency-vs-mixed-prefill curve.  Prints one JSON line.
+Default workload: the 70B-shaped layer (hidden 8192, 64 query / 8 KV heads x
+128, FFN 28672) with 256 decodes (contexts uniform in [1024, 16384], a KV pool
+of about 150 GB) plus 0 .. 8192 mixed prefill tokens in steps of 1024; the
+headline is the last point (8192 prefill tokens, T = 8448) and the whole sweep
+is the latency-vs-mixed-prefill curve.  `--config c2|c3|c4` times the other
+shapes.  Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -33,7 +35,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=int(os.environ.get("WORLD_SIZE", "1")))
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=100)
-    ap.add_argument("--config", default="c2", help="layer shape c1..c5")
+    ap.add_argument("--config", default="c5", help="layer shape c1..c5")
     ap.add_argument("--prefill", type=int, nargs="*", default=None,
                     help="mixed prefill tokens per point (default: the shape's sweep)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
@@ -292,10 +294,20 @@ def kernel_breakdown(pt, steps, warmup):
     mx.mx_profile_enable(False)
     times = mx.mx_profile_read()
     parts = pt.parts
+    # the second RMSNorm runs fused with the output projection's split-K reduce
+    # when (some rows of) that projection are split over K: it then also reads
+    # the fp32 planes and the residual of the split rows and writes their x1
+    cfg, T = pt.cfg, pt.b.T
+    plan = mx.mx_debug_gemm_plan(T, cfg.hidden, cfg.n_q_heads * cfg.head_dim)
+    split_rows = T - plan["m_main"] if plan["m_main"] < T else T
+    ks = plan["tail_ksplit"] if plan["m_main"] < T else plan["ksplit"]
+    norm2 = parts["rmsnorm"]["bytes"] / 2
+    fused = norm2 + split_rows * cfg.hidden * (4.0 * ks + 2.0 + 2.0)
     algo = {"gemm_qkv": parts["qkv"], "gemm_o": parts["o"], "gemm_gate_up": parts["gate_up"],
             "gemm_down": parts["down"], "paged_attn": parts["attention"],
             "token_map+rmsnorm_1": {"flops": 0.0, "bytes": parts["rmsnorm"]["bytes"] / 2},
-            "rmsnorm_2": {"flops": 0.0, "bytes": parts["rmsnorm"]["bytes"] / 2}}
+            "rmsnorm_2": {"flops": 0.0, "bytes": norm2},
+            "o_reduce+rmsnorm_2": {"flops": 0.0, "bytes": fused}}
     res = {}
     for tag, (ms, n) in times.items():
         us = ms / max(n, 1) * 1e3
@@ -307,6 +319,17 @@ def kernel_breakdown(pt, steps, warmup):
                         achieved_GBps=a["bytes"] / sec / 1e9 if sec > 0 else 0.0,
                         TFLOPs=a["flops"] / sec / 1e12 if sec > 0 else 0.0)
     return res
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def cpu_baseline(key, cfg, w_host, budget_s):
@@ -353,7 +376,9 @@ def cpu_baseline(key, cfg, w_host, budget_s):
     return {"value": n * reps / total, "unit": "tokens/s", "cores": oracle.num_threads(),
             "kind": "oracle",
             "sample": f"{n_dec} decode requests + first {n_pre} tokens of the prefill chunk "
-                      f"({n} rows, full layer, fp64), {reps} evaluation(s) in {total:.1f} s"}
+                      f"({n} rows, full layer), {reps} evaluation(s) in {total:.1f} s",
+            "oracle": "plain C, fp64 arithmetic, gcc " + " ".join(oracle.CFLAGS),
+            "cpu": cpu_model()}
 
 
 def chunk_sweep(args, key, cfg, packed):

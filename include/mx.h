@@ -227,9 +227,11 @@ mx_status mx_debug_gather(const mx_batch* batch, const mx_attn_shape* shape, int
  * mx_layer_step and mx_paged_attn is bracketed by two hipEvents recorded on the
  * caller's stream (the launch's own stream), tagged with the step it performs
  * ("token_map+rmsnorm_1", "gemm_qkv", "paged_attn", "gemm_o", "rmsnorm_2",
- * "gemm_gate_up", "gemm_down"; a tag covers a split-K GEMM's reduce and the
- * attention's split merge, except that a split output projection's reduce runs
- * fused with the second RMSNorm and is timed as "rmsnorm_2").  Off by default. */
+ * "gemm_gate_up", "gemm_down"; a tag covers a split-K GEMM's reduce, the
+ * launches of a GEMM whose rows run as two parts, and the attention's split
+ * merge, except that when rows of the output projection are split over K their
+ * reduce runs fused with the second RMSNorm, timed as "o_reduce+rmsnorm_2"
+ * instead of "rmsnorm_2").  Off by default. */
 mx_status mx_profile_enable(int32_t on);
 /* Waits for the recorded events, accumulates their durations per tag and
  * returns the number of tags written (at most max_entries): names[i] is a
@@ -263,6 +265,33 @@ mx_status mx_debug_gemm_tiled(int32_t M, int32_t N, int32_t K, const uint16_t* A
                               const uint16_t* B_tiled, uint16_t* C, const uint16_t* R,
                               int32_t epilogue, int32_t tile_cfg, int32_t ksplit, void* ws,
                               size_t ws_bytes, hipStream_t stream);
+
+/* The tile plan the library's cost model picks for an M x N x K projection
+ * (host only, touches no device): plan[0] tile shape (numbered as for
+ * mx_debug_gemm_config) and plan[1] K split of rows [0, plan[2]); when
+ * plan[2] < M the remaining rows run as a second GEMM after the first, with
+ * tile shape plan[3] and K split plan[4] (plan[2] == M: one launch, plan[3] = -1).
+ * K must be a multiple of 64.  For tests that must know which path a shape takes. */
+mx_status mx_debug_gemm_plan(int32_t M, int32_t N, int32_t K, int32_t plan[5]);
+/* A forced row split with B in the packed tile layout (as mx_debug_gemm_tiled):
+ * rows [0, m_main) with tile shape main_cfg and no K split, then rows
+ * [m_main, M) as a GEMM of their own with tile shape tail_cfg and K split
+ * tail_ksplit (ws holds tail_ksplit * (M - m_main) * N floats when it is > 1).
+ * 1 <= m_main < M, N % 16 == 0, K % 64 == 0.  For tests of the row split. */
+mx_status mx_debug_gemm_rows(int32_t M, int32_t N, int32_t K, const uint16_t* A,
+                             const uint16_t* B_tiled, uint16_t* C, const uint16_t* R,
+                             int32_t epilogue, int32_t m_main, int32_t main_cfg, int32_t tail_cfg,
+                             int32_t tail_ksplit, void* ws, size_t ws_bytes, hipStream_t stream);
+/* The output projection's split-K reduce fused with the second RMSNorm, on its
+ * own: for rows r >= split_row, x1[r] = bf16(sum_z partial[z][r - split_row] + R[r])
+ * (partial: ksplit fp32 planes [M - split_row][H], summed in plane order, then
+ * the residual); rows r < split_row hold x1 already.  Then h[r] = RMSNorm(x1[r]) * g
+ * for every row, from the rounded x1.  R, x1, h [M][H] bf16, g [H] bf16;
+ * H % 8 == 0 and H <= 8192.  For tests of the kernel the layer step runs. */
+mx_status mx_debug_reduce_residual_rmsnorm(const float* partial, int32_t ksplit, const uint16_t* R,
+                                           uint16_t* x1, const uint16_t* g, uint16_t* h, int32_t M,
+                                           int32_t H, float eps, int32_t split_row,
+                                           hipStream_t stream);
 
 #ifdef __cplusplus
 }

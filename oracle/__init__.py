@@ -19,10 +19,14 @@ _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 _SRC = os.path.join(_HERE, "oracle.c")
 
 
+CFLAGS = ["-O2", "-march=x86-64-v3", "-fopenmp"]
+
+
 def build(verbose: bool = False) -> str:
     """Compile liboracle.so with gcc (plain C, OpenMP)."""
-    cmd = ["gcc", "-O2", "-march=x86-64-v3", "-fopenmp", "-fPIC", "-shared", "-std=c11",
-           "-Wall", "-Wextra", "-Wno-unused-parameter", "-o", _LIB_PATH + ".tmp", _SRC, "-lm"]
+    cmd = ["gcc"] + CFLAGS + ["-fPIC", "-shared", "-std=c11",
+                              "-Wall", "-Wextra", "-Wno-unused-parameter", "-o", _LIB_PATH + ".tmp",
+                              _SRC, "-lm"]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)

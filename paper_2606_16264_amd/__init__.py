@@ -29,7 +29,8 @@ EXPORTED = [
     "mx_workspace_bytes", "mx_packed_weights_bytes", "mx_pack_weights", "mx_kv_append",
     "mx_paged_attn", "mx_layer_step", "mx_layer_workspace_offsets", "mx_debug_token_map",
     "mx_debug_gather", "mx_debug_gemm_ws_bytes", "mx_debug_gemm", "mx_debug_gemm_config",
-    "mx_debug_gemm_tiled",
+    "mx_debug_gemm_tiled", "mx_debug_gemm_plan", "mx_debug_gemm_rows",
+    "mx_debug_reduce_residual_rmsnorm",
     "mx_profile_enable", "mx_profile_read",
 ]
 
@@ -98,6 +99,11 @@ def _load() -> ctypes.CDLL:
         "mx_debug_gemm": ([I32, I32, I32, P, P, P, P, I32, P, SZ, P], ctypes.c_int),
         "mx_debug_gemm_config": ([I32, I32, I32, P, P, P, P, I32, I32, I32, P, SZ, P], ctypes.c_int),
         "mx_debug_gemm_tiled": ([I32, I32, I32, P, P, P, P, I32, I32, I32, P, SZ, P], ctypes.c_int),
+        "mx_debug_gemm_plan": ([I32, I32, I32, ctypes.POINTER(I32)], ctypes.c_int),
+        "mx_debug_gemm_rows": ([I32, I32, I32, P, P, P, P, I32, I32, I32, I32, I32, P, SZ, P],
+                               ctypes.c_int),
+        "mx_debug_reduce_residual_rmsnorm": ([P, I32, P, P, P, P, I32, I32, ctypes.c_float, I32, P],
+                                             ctypes.c_int),
         "mx_profile_enable": ([I32], ctypes.c_int),
         "mx_profile_read": ([ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float),
                              ctypes.POINTER(ctypes.c_int32), I32], I32),
@@ -277,6 +283,32 @@ def mx_debug_gemm(A, B, C, R=None, epilogue: int = EPI_STORE, ws=None, stream=No
         fn = _lib.mx_debug_gemm_config
     _check(fn(M, N, K, _ptr(A), _ptr(B), _ptr(C), _ptr(R), epilogue, tile_cfg, ksplit, _ptr(ws),
               0 if ws is None else ws.numel(), _stream(stream)))
+
+
+def mx_debug_gemm_plan(M: int, N: int, K: int) -> dict:
+    """The cost model's plan of an M x N x K projection (host only)."""
+    out = (ctypes.c_int32 * 5)()
+    _check(_lib.mx_debug_gemm_plan(M, N, K, out))
+    return {"cfg": out[0], "ksplit": out[1], "m_main": out[2], "tail_cfg": out[3],
+            "tail_ksplit": out[4]}
+
+
+def mx_debug_gemm_rows(A, B_tiled, C, R, epilogue: int, N: int, m_main: int, main_cfg: int,
+                       tail_cfg: int, tail_ksplit: int, ws=None, stream=None) -> None:
+    """A forced row split (B in the packed tile layout): rows [0, m_main) with
+    tile shape main_cfg, the rest with tail_cfg split tail_ksplit ways over K."""
+    M, K = A.shape
+    _check(_lib.mx_debug_gemm_rows(M, N, K, _ptr(A), _ptr(B_tiled), _ptr(C), _ptr(R), epilogue,
+                                   m_main, main_cfg, tail_cfg, tail_ksplit, _ptr(ws),
+                                   0 if ws is None else ws.numel(), _stream(stream)))
+
+
+def mx_debug_reduce_residual_rmsnorm(partial, ksplit: int, R, x1, g, h, eps: float = 1e-5,
+                                     split_row: int = 0, stream=None) -> None:
+    """The output projection's fused split-K reduce + residual + RMSNorm."""
+    M, H = R.shape
+    _check(_lib.mx_debug_reduce_residual_rmsnorm(_ptr(partial), ksplit, _ptr(R), _ptr(x1), _ptr(g),
+                                                 _ptr(h), M, H, eps, split_row, _stream(stream)))
 
 
 def mx_profile_enable(on: bool = True) -> None:

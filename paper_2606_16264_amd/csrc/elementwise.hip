@@ -145,27 +145,64 @@ __device__ __forceinline__ void rmsnorm_row(const uint16_t* __restrict__ x,
 // taken in split order and then the residual, exactly as the stand-alone
 // reduce does, and h = RMSNorm(x1, g) from the rounded x1, exactly as
 // rmsnorm_row does; the row stays in registers between the two (rows of up to
-// 2 * 512 * 8 elements).  Every plane's loads of a thread are issued before
-// the first sum, so that the planes cost one memory round trip, not one each.
-constexpr int kNormThreads = 512;
-constexpr int kNormChunks = 2;  // 16-byte chunks per thread
-constexpr int kNormPlanes = 8;  // planes loaded ahead; more are summed one by one
+// kFusedNormMaxH elements).  Every plane's loads of a thread (up to
+// kNormPlanes of them) are issued before the first sum, so that the planes
+// cost one memory round trip, not one each; further planes are summed one by
+// one.
+
+// Rows below split_row were completed by the GEMM itself (a row split of the
+// projection): their blocks read x1 and only normalise it.
+__device__ __forceinline__ float norm_complete_row(const u32x4* __restrict__ xrow, int nchunk,
+                                                   u32x4 (&v)[kNormChunks]) {
+  float ss = 0.f;
+#pragma unroll
+  for (int k = 0; k < kNormChunks; k++) {
+    const int c = threadIdx.x + k * kNormThreads;
+    v[k] = c < nchunk ? xrow[c] : u32x4{0, 0, 0, 0};
+    ss += sum_squares(v[k]);
+  }
+  return ss;
+}
 
 __global__ __launch_bounds__(kNormThreads) void reduce_residual_rmsnorm_kernel(
     const float* __restrict__ partial, int ksplit, const uint16_t* __restrict__ R,
     uint16_t* __restrict__ x1, const uint16_t* __restrict__ g, uint16_t* __restrict__ h, int M,
-    int H, float eps) {
+    int H, float eps, int split_row) {
   __shared__ float red[kNormThreads / 64];
   const int64_t row = blockIdx.x;
   const int nchunk = H / 8;
-  const int64_t plane4 = (int64_t)M * H / 4;  // one plane in f32x4
-  const f32x4* prow = reinterpret_cast<const f32x4*>(partial + row * H);
-  const u32x4* rrow = reinterpret_cast<const u32x4*>(R + row * H);
   const u32x4* gr = reinterpret_cast<const u32x4*>(g);
   u32x4* xrow = reinterpret_cast<u32x4*>(x1 + row * H);
   u32x4* hrow = reinterpret_cast<u32x4*>(h + row * H);
+  u32x4 gv[kNormChunks], v[kNormChunks];
+  if (row < split_row) {
+#pragma unroll
+    for (int k = 0; k < kNormChunks; k++) {
+      const int c = threadIdx.x + k * kNormThreads;
+      gv[k] = c < nchunk ? gr[c] : u32x4{0, 0, 0, 0};
+    }
+    float ss = norm_complete_row(xrow, nchunk, v);
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    float tot = 0.f;
+#pragma unroll
+    for (int w = 0; w < kNormThreads / 64; w++) tot += red[w];
+    const float inv = 1.0f / sqrtf(tot / (float)H + eps);
+#pragma unroll
+    for (int k = 0; k < kNormChunks; k++) {
+      const int c = threadIdx.x + k * kNormThreads;
+      if (c < nchunk) rms_scale_store(v[k], gv[k], inv, hrow + c);
+    }
+    return;
+  }
+  const int64_t prow_idx = row - split_row;                  // row within the planes
+  const int64_t plane4 = (int64_t)(M - split_row) * H / 4;   // one plane in f32x4
+  const f32x4* prow = reinterpret_cast<const f32x4*>(partial + prow_idx * H);
+  const u32x4* rrow = reinterpret_cast<const u32x4*>(R + row * H);
   f32x4 pl[kNormChunks][kNormPlanes][2];
-  u32x4 r[kNormChunks], gv[kNormChunks], v[kNormChunks];
+  u32x4 r[kNormChunks];
 #pragma unroll
   for (int k = 0; k < kNormChunks; k++) {
     const int c = threadIdx.x + k * kNormThreads;
@@ -392,12 +429,12 @@ hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* g, uint16_t* out, i
 
 hipError_t launch_reduce_residual_rmsnorm(const float* partial, int ksplit, const uint16_t* R,
                                           uint16_t* x1, const uint16_t* g, uint16_t* h, int M,
-                                          int H, float eps, hipStream_t stream) {
+                                          int H, float eps, int split_row, hipStream_t stream) {
   if (M == 0) return hipSuccess;
-  if (H % 8 != 0 || H / 8 > kNormChunks * kNormThreads || ksplit < 1)
+  if (H % 8 != 0 || H > kFusedNormMaxH || ksplit < 1 || split_row < 0 || split_row > M)
     return hipErrorInvalidValue;
   reduce_residual_rmsnorm_kernel<<<M, kNormThreads, 0, stream>>>(partial, ksplit, R, x1, g, h, M,
-                                                                 H, eps);
+                                                                 H, eps, split_row);
   return hipGetLastError();
 }
 

@@ -28,6 +28,9 @@
 //    estimate for few rows, rounds of tile-units for more).
 #include <algorithm>
 #include <cmath>
+#include <map>
+#include <mutex>
+#include <tuple>
 
 #include "mx_device.h"
 #include "mx_kernels.h"
@@ -574,11 +577,6 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int kspl
   }
 }
 
-struct Plan {
-  int cfg;     // tile shape index into kShapes
-  int ksplit;
-};
-
 struct Shape {
   int BM, BN;
   // time of one round of tile-units on the chip: a + b * (K slice length),
@@ -601,8 +599,10 @@ constexpr Shape kShapes[] = {{256, 256, 3.471, 0.02443, 1, 33.8},
                              {128, 256, 0.978, 0.0287, 2, 42.1}};
 constexpr int kNumShapes = 5;
 constexpr int kFeedMaxM = 256;  // rows up to which the feed estimate is used
+constexpr double kCUs = 256.0;
 
-// Estimated time of each (tile shape, K split) choice, two regimes.  Few rows
+// Estimated time (us) of one GEMM launch with tile shape c and K split ks, in
+// two regimes, or a negative value when the choice is not allowed.  Few rows
 // (M <= kFeedMaxM): the layer's weights arrive cold from HBM and the busiest
 // CU's feed bounds the time: its tile-units (ceil(units / 256)) times the
 // bytes one unit streams (its A and B rows over its K slice) at the shape's
@@ -618,38 +618,122 @@ constexpr int kFeedMaxM = 256;  // rows up to which the feed estimate is used
 // measured time fell on 10 of 11 such problems (7B down projection at 576 rows
 // 92.8 -> 74.6 us with 128 x 256 tiles split three ways; Llama-3-8B down at
 // 2304 rows 343.7 -> 304.7 us) and rose by 0.9% on the eleventh.
-Plan choose(int M, int N, int K) {
-  const double cus = 256.0, hbm = 5.0e12;
-  const bool feed = M <= kFeedMaxM;
-  Plan best{kNumShapes - 1, 1};
-  double best_t = 1e30;
+double estimate(int c, int ks, int M, int N, int K) {
+  const double hbm = 5.0e12;
+  if ((K / BK) / ks < 4) return -1.0;  // every split at least four 64-wide K chunks
+  if (ks > 1 && (double)ks * M * N > (double)kMaxSplitFloats) return -1.0;
+  const int BM = kShapes[c].BM, BN = kShapes[c].BN;
+  const double tiles = (double)((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+  const double split_mb = ((double)ks * M * N * 8.0 + 2.0 * M * N) / 1e6;
+  const double k_unit = (double)((K / BK + ks - 1) / ks * BK);  // the longest split
+  if (M <= kFeedMaxM) {
+    const double per_cu = std::ceil(tiles * ks / kCUs);
+    const double unit_bytes = (double)(BN + std::min(BM, M)) * k_unit * 2.0;
+    return per_cu * unit_bytes / (kShapes[c].feed_gbs * 1e3) + 12.06 +
+           (ks > 1 ? 0.157 * split_mb + 0.15 : 0.0);
+  }
+  const double rounds = std::ceil(tiles * ks / (kCUs * kShapes[c].per_cu));
+  const double t_units = rounds * (kShapes[c].a_us + kShapes[c].b_us_per_k * k_unit);
+  const double t_mem = 2.0 * ((double)N * K + (double)M * K) / hbm * 1e6;
+  return std::max(t_units, t_mem) + (ks > 1 ? 0.197 * split_mb + 3.39 : 0.0);
+}
+
+struct Pick {
+  int cfg, ksplit;
+  double t;
+};
+
+// The best (tile shape, K split) of one launch over all M rows.
+Pick choose_one(int M, int N, int K) {
+  Pick best{kNumShapes - 1, 1, 1e30};
+  for (int c = 0; c < kNumShapes; c++)
+    for (int ks = 1; ks <= 8; ks++) {
+      const double t = estimate(c, ks, M, N, K);
+      if (t < 0.0) break;
+      if (t < best.t * 0.98) best = {c, ks, t};
+    }
+  return best;
+}
+
+// Launch plan of one GEMM.  Rows [0, m_main) run with tile shape cfg and K
+// split ksplit; when m_main < M, the remaining rows run as a second GEMM of
+// their own (tile shape tail_cfg, K split tail_ksplit) after the first.  The
+// row split removes the last, mostly empty round of a problem whose tiles
+// fill a few rounds and a little more (70B-shaped down projection at 8448
+// rows: 1056 tiles of 256 x 256, 4.125 rounds of 256 CUs, run as 1024 tiles in
+// four full rounds plus 256 rows split eight ways over K).
+struct Plan {
+  int cfg, ksplit;
+  int m_main;
+  int tail_cfg, tail_ksplit;
+};
+
+Plan plan_uncached(int M, int N, int K) {
+  const Pick whole = choose_one(M, N, K);
+  Plan best{whole.cfg, whole.ksplit, M, -1, 0};
+  if (M <= 2 * kFeedMaxM) return best;
+  double best_t = whole.t;
+  // first part: whole rounds of one tile shape without a K split; second part:
+  // the remaining rows, planned as a launch of their own (plus a launch gap)
   for (int c = 0; c < kNumShapes; c++) {
     const int BM = kShapes[c].BM, BN = kShapes[c].BN;
-    const double tiles = (double)((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-    for (int ks = 1; ks <= 8; ks++) {
-      if ((K / BK) / ks < 4) break;  // every split at least four 64-wide K chunks
-      if (ks > 1 && (double)ks * M * N > (double)kMaxSplitFloats) break;
-      const double split_mb = ((double)ks * M * N * 8.0 + 2.0 * M * N) / 1e6;
-      const double k_unit = (double)((K / BK + ks - 1) / ks * BK);  // the longest split
-      double t;
-      if (feed) {
-        const double per_cu = std::ceil(tiles * ks / cus);
-        const double unit_bytes = (double)(BN + std::min(BM, M)) * k_unit * 2.0;
-        t = per_cu * unit_bytes / (kShapes[c].feed_gbs * 1e3) + 12.06 +
-            (ks > 1 ? 0.157 * split_mb + 0.15 : 0.0);
-      } else {
-        const double rounds = std::ceil(tiles * ks / (cus * kShapes[c].per_cu));
-        const double t_units = rounds * (kShapes[c].a_us + kShapes[c].b_us_per_k * k_unit);
-        const double t_mem = 2.0 * ((double)N * K + (double)M * K) / hbm * 1e6;
-        t = std::max(t_units, t_mem) + (ks > 1 ? 0.197 * split_mb + 3.39 : 0.0);
-      }
-      if (t < best_t * 0.98) {
+    const double slots = kCUs * kShapes[c].per_cu;
+    const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
+    for (int j = tiles_m - 1; j >= 1 && M - j * BM <= 4 * kFeedMaxM; j--) {
+      const double tiles = (double)j * tiles_n;
+      const double frac = tiles / slots - std::floor(tiles / slots);
+      if (frac > 0.0 && frac < 0.75) continue;  // only (nearly) full last rounds
+      const double t_main = estimate(c, 1, j * BM, N, K);
+      if (t_main < 0.0) continue;
+      const Pick tail = choose_one(M - j * BM, N, K);
+      const double t = t_main + tail.t + 4.0;
+      if (t < best_t * 0.97) {
         best_t = t;
-        best = {c, ks};
+        best = {c, 1, j * BM, tail.cfg, tail.ksplit};
       }
     }
   }
   return best;
+}
+
+// Plans are cached per problem: the layer step plans four GEMMs per call.
+Plan plan_gemm(int M, int N, int K) {
+  static std::mutex mu;
+  static std::map<std::tuple<int, int, int>, Plan> cache;
+  const auto key = std::make_tuple(M, N, K);
+  {
+    std::lock_guard<std::mutex> g(mu);
+    auto it = cache.find(key);
+    if (it != cache.end()) return it->second;
+  }
+  const Plan p = plan_uncached(M, N, K);
+  std::lock_guard<std::mutex> g(mu);
+  if (cache.size() > 4096) cache.clear();
+  cache[key] = p;
+  return p;
+}
+
+// Scratch (fp32 elements) that a plan's K split needs.
+size_t plan_scratch(const Plan& p, int M, int N) {
+  if (p.m_main < M) return p.tail_ksplit > 1 ? (size_t)p.tail_ksplit * (M - p.m_main) * N : 0;
+  return p.ksplit > 1 ? (size_t)p.ksplit * M * N : 0;
+}
+
+// The GEMM of rows [m0, M) of a: every row-indexed operand moves by m0 rows
+// (A, C, R and, for the QKV epilogue, the rotary table, the token slots and
+// q_out; the pools are addressed through the slots).
+GemmArgs rows_from(const GemmArgs& a, int m0) {
+  GemmArgs t = a;
+  t.M = a.M - m0;
+  t.A = a.A + (int64_t)m0 * a.lda;
+  if (t.C) t.C = a.C + (int64_t)m0 * a.ldc;
+  if (t.R) t.R = a.R + (int64_t)m0 * a.ldr;
+  if (a.epilogue == EPI_QKV) {
+    t.qkv.rope_cs = a.qkv.rope_cs + (int64_t)m0 * (a.qkv.head_dim / 2);
+    t.qkv.tok_slot = a.qkv.tok_slot + m0;
+    t.qkv.q_out = a.qkv.q_out + (int64_t)m0 * a.qkv.nq * a.qkv.head_dim;
+  }
+  return t;
 }
 
 template <int BM, int BN, int WM, int WN, int NS, int EPI, bool SPLIT>
@@ -733,8 +817,16 @@ hipError_t gemm_init() {
 }
 
 size_t gemm_scratch_floats(int M, int N, int K) {
-  const Plan p = choose(M, N, K);
-  return p.ksplit > 1 ? (size_t)p.ksplit * M * N : 0;
+  return plan_scratch(plan_gemm(M, N, K), M, N);
+}
+
+void gemm_plan(int M, int N, int K, int out[5]) {
+  const Plan p = plan_gemm(M, N, K);
+  out[0] = p.cfg;
+  out[1] = p.ksplit;
+  out[2] = p.m_main;
+  out[3] = p.tail_cfg;
+  out[4] = p.tail_ksplit;
 }
 
 hipError_t launch_gemm(const GemmArgs& a, size_t ws_floats, hipStream_t stream) {
@@ -744,37 +836,72 @@ hipError_t launch_gemm(const GemmArgs& a, size_t ws_floats, hipStream_t stream) 
 int gemm_num_configs() { return kNumShapes; }
 
 namespace {
-hipError_t launch_plan(const GemmArgs& a, Plan p, bool reduce, hipStream_t stream) {
-  switch (p.cfg) {
-    case 0: return run_shape<256, 256, 128, 64, 4>(a, p.ksplit, reduce, stream);
-    case 1: return run_shape<128, 256, 64, 64, 4>(a, p.ksplit, reduce, stream);
-    case 2: return run_shape<128, 128, 64, 64, 4>(a, p.ksplit, reduce, stream);
-    case 3: return run_shape<64, 128, 32, 64, 4>(a, p.ksplit, reduce, stream);
-    default: return run_shape<128, 256, 64, 64, 3>(a, p.ksplit, reduce, stream);
+hipError_t launch_shape(const GemmArgs& a, int cfg, int ksplit, bool reduce, hipStream_t stream) {
+  switch (cfg) {
+    case 0: return run_shape<256, 256, 128, 64, 4>(a, ksplit, reduce, stream);
+    case 1: return run_shape<128, 256, 64, 64, 4>(a, ksplit, reduce, stream);
+    case 2: return run_shape<128, 128, 64, 64, 4>(a, ksplit, reduce, stream);
+    case 3: return run_shape<64, 128, 32, 64, 4>(a, ksplit, reduce, stream);
+    default: return run_shape<128, 256, 64, 64, 3>(a, ksplit, reduce, stream);
   }
+}
+
+// A plan whose K split needs more scratch than there is runs that part unsplit.
+Plan fit_scratch(Plan p, int M, int N, size_t ws_floats) {
+  if (plan_scratch(p, M, N) > ws_floats) {
+    if (p.m_main < M)
+      p.tail_ksplit = 1;
+    else
+      p.ksplit = 1;
+  }
+  return p;
+}
+
+// reduce = false: the K split of the last part (the tail rows, or all rows
+// without a row split) leaves its fp32 planes at a.partial for the caller.
+hipError_t launch_plan(const GemmArgs& a, const Plan& p, bool reduce, hipStream_t stream) {
+  if (p.m_main >= a.M) return launch_shape(a, p.cfg, p.ksplit, reduce, stream);
+  GemmArgs head = a;
+  head.M = p.m_main;
+  hipError_t e = launch_shape(head, p.cfg, p.ksplit, true, stream);
+  if (e != hipSuccess) return e;
+  return launch_shape(rows_from(a, p.m_main), p.tail_cfg, p.tail_ksplit, reduce, stream);
 }
 }  // namespace
 
 hipError_t launch_gemm_config(const GemmArgs& a, size_t ws_floats, int cfg, int ksplit,
                               hipStream_t stream) {
   if (a.M == 0) return hipSuccess;
-  Plan p = choose(a.M, a.N, a.K);
+  Plan p = plan_gemm(a.M, a.N, a.K);
   if (cfg >= 0 && cfg < kNumShapes) {
-    p.cfg = cfg;
-    p.ksplit = ksplit >= 1 ? ksplit : 1;
+    p = Plan{cfg, ksplit >= 1 ? ksplit : 1, a.M, -1, 0};
     if (a.K / BK < p.ksplit) return hipErrorInvalidValue;
   }
-  if (p.ksplit > 1 && (size_t)p.ksplit * a.M * a.N > ws_floats) p.ksplit = 1;
+  return launch_plan(a, fit_scratch(p, a.M, a.N, ws_floats), true, stream);
+}
+
+hipError_t launch_gemm_rows(const GemmArgs& a, size_t ws_floats, int m_main, int cfg,
+                            int tail_cfg, int tail_ksplit, hipStream_t stream) {
+  if (a.M == 0) return hipSuccess;
+  if (m_main < 1 || m_main >= a.M || cfg < 0 || cfg >= kNumShapes || tail_cfg < 0 ||
+      tail_cfg >= kNumShapes || tail_ksplit < 1 || a.K / BK < tail_ksplit)
+    return hipErrorInvalidValue;
+  const Plan p{cfg, 1, m_main, tail_cfg, tail_ksplit};
+  if (plan_scratch(p, a.M, a.N) > ws_floats) return hipErrorInvalidValue;
   return launch_plan(a, p, true, stream);
 }
 
-hipError_t launch_gemm_unreduced(const GemmArgs& a, size_t ws_floats, int* ksplit,
+hipError_t launch_gemm_unreduced(const GemmArgs& a, size_t ws_floats, int* split_row, int* ksplit,
                                  hipStream_t stream) {
+  *split_row = a.M;
   *ksplit = 1;
   if (a.M == 0) return hipSuccess;
-  Plan p = choose(a.M, a.N, a.K);
-  if (p.ksplit > 1 && (size_t)p.ksplit * a.M * a.N > ws_floats) p.ksplit = 1;
-  *ksplit = p.ksplit;
+  const Plan p = fit_scratch(plan_gemm(a.M, a.N, a.K), a.M, a.N, ws_floats);
+  const int ks = p.m_main < a.M ? p.tail_ksplit : p.ksplit;
+  if (ks > 1) {
+    *split_row = p.m_main < a.M ? p.m_main : 0;
+    *ksplit = ks;
+  }
   return launch_plan(a, p, false, stream);
 }
 

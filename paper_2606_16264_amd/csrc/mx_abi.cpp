@@ -777,23 +777,23 @@ MX_EXPORT mx_status mx_layer_step(const mx_batch* batch, const mx_layer_cfg* cfg
                                      (int)p.merges.size(), d, stream);
           }), "attention launch")
   }
-  // a7 + a8: output projection + residual, then RMSNorm 2.  When the
-  // projection is split over K, its reduce, the residual and the norm run as
-  // one kernel (timed as rmsnorm_2), which reads the fp32 planes once and
-  // keeps each x1 row in registers for the norm.
+  // a7 + a8: output projection + residual, then RMSNorm 2.  When (some rows
+  // of) the projection are split over K, their reduce, the residual and the
+  // norm of every row run as one kernel (timed as o_reduce+rmsnorm_2), which
+  // reads the fp32 planes once and keeps each x1 row in registers for the norm.
   {
     GemmArgs g{o, (const uint16_t*)(P + W.o), x1, x, scratch, M, H, nq * d, nq * d, nq * d, H, H, EPI_RESIDUAL, {}};
     set_b_tiled(g);
     const uint16_t* g2 = (const uint16_t*)(P + W.g2);
-    const bool fuse = H <= 8192;  // a row in registers: H / 8 chunks over 256 threads, 4 each
-    int ks = 1;
+    const bool fuse = H <= kFusedNormMaxH;  // the fused kernel holds a row in registers
+    int split_row = M, ks = 1;
     MX_CK(timed("gemm_o", stream, [&] {
-            return fuse ? launch_gemm_unreduced(g, L.scratch_floats, &ks, stream)
+            return fuse ? launch_gemm_unreduced(g, L.scratch_floats, &split_row, &ks, stream)
                         : launch_gemm(g, L.scratch_floats, stream);
           }), "o gemm launch")
-    MX_CK(timed("rmsnorm_2", stream, [&] {
+    MX_CK(timed(ks > 1 ? "o_reduce+rmsnorm_2" : "rmsnorm_2", stream, [&] {
             return ks > 1 ? launch_reduce_residual_rmsnorm(scratch, ks, x, x1, g2, h, M, H,
-                                                           cfg->rms_eps, stream)
+                                                           cfg->rms_eps, split_row, stream)
                           : launch_rmsnorm(x1, g2, h, M, H, cfg->rms_eps, stream);
           }), "rmsnorm launch")
   }
@@ -948,6 +948,75 @@ MX_EXPORT mx_status mx_debug_gemm_tiled(int32_t M, int32_t N, int32_t K, const u
                                         void* ws, size_t ws_bytes, hipStream_t stream) {
   return debug_gemm(M, N, K, A, B_tiled, true, C, R, epilogue, tile_cfg, ksplit, ws, ws_bytes,
                     stream);
+}
+
+MX_EXPORT mx_status mx_debug_gemm_plan(int32_t M, int32_t N, int32_t K, int32_t plan[5]) {
+  g_err.clear();
+  if (M < 0 || N <= 0 || K <= 0 || K % 64) return fail(MX_ERR_INVALID, "bad GEMM shape %d x %d x %d", M, N, K);
+  if (!plan) return fail(MX_ERR_NULL, "plan is NULL");
+  int out[5];
+  gemm_plan(M, N, K, out);
+  for (int i = 0; i < 5; i++) plan[i] = out[i];
+  return MX_OK;
+}
+
+MX_EXPORT mx_status mx_debug_gemm_rows(int32_t M, int32_t N, int32_t K, const uint16_t* A,
+                                       const uint16_t* B_tiled, uint16_t* C, const uint16_t* R,
+                                       int32_t epilogue, int32_t m_main, int32_t main_cfg,
+                                       int32_t tail_cfg, int32_t tail_ksplit, void* ws,
+                                       size_t ws_bytes, hipStream_t stream) {
+  g_err.clear();
+  if (M < 2 || N <= 0 || K <= 0) return fail(MX_ERR_INVALID, "bad GEMM shape %d x %d x %d", M, N, K);
+  if (N % 16 || K % 64) return fail(MX_ERR_UNSUPPORTED, "tiled weights need N %% 16 == 0 and K %% 64 == 0");
+  if (m_main < 1 || m_main >= M) return fail(MX_ERR_INVALID, "m_main %d not in [1, M)", m_main);
+  if (main_cfg < 0 || main_cfg >= gemm_num_configs() || tail_cfg < 0 || tail_cfg >= gemm_num_configs())
+    return fail(MX_ERR_INVALID, "tile config out of range");
+  if (tail_ksplit < 1 || tail_ksplit > 64 || K / 64 < tail_ksplit)
+    return fail(MX_ERR_INVALID, "K split %d is not in [1, min(64, K / 64 = %d)]", tail_ksplit, K / 64);
+  if (epilogue < 0 || epilogue > 2) return fail(MX_ERR_INVALID, "bad epilogue %d", epilogue);
+  if (epilogue == EPI_SWIGLU && N % 64) return fail(MX_ERR_UNSUPPORTED, "SwiGLU needs N % 64 == 0");
+  if (!A || !B_tiled || !C || (epilogue == EPI_RESIDUAL && !R)) return fail(MX_ERR_NULL, "NULL operand");
+  if (mx_status sa = check_aligned({A, B_tiled, C, R, ws}); sa != MX_OK) return sa;
+  if (epilogue == EPI_RESIDUAL) {
+    const size_t bytes = (size_t)M * N * 2;
+    const char *c0 = (const char*)C, *r0 = (const char*)R;
+    if (c0 < r0 + bytes && r0 < c0 + bytes) return fail(MX_ERR_INVALID, "R overlaps C");
+  }
+  const size_t need = tail_ksplit > 1 ? (size_t)tail_ksplit * (M - m_main) * N : 0;
+  if (need && (!ws || ws_bytes < need * 4))
+    return fail(MX_ERR_TOO_LARGE, "GEMM scratch %zu bytes < %zu", ws_bytes, need * 4);
+  DeviceState* ds;
+  mx_status st = device_state(&ds);
+  if (st != MX_OK) return st;
+  const int ldc = epilogue == EPI_SWIGLU ? N / 2 : N;
+  GemmArgs g{A, B_tiled, C, R, (float*)ws, M, N, K, K, K, ldc, N, epilogue, {}};
+  set_b_tiled(g);
+  hipError_t e = launch_gemm_rows(g, ws ? ws_bytes / 4 : 0, m_main, main_cfg, tail_cfg, tail_ksplit,
+                                  stream);
+  if (e != hipSuccess) return hip_fail(e, "gemm launch");
+  return MX_OK;
+}
+
+MX_EXPORT mx_status mx_debug_reduce_residual_rmsnorm(const float* partial, int32_t ksplit,
+                                                     const uint16_t* R, uint16_t* x1,
+                                                     const uint16_t* g, uint16_t* h, int32_t M,
+                                                     int32_t H, float eps, int32_t split_row,
+                                                     hipStream_t stream) {
+  g_err.clear();
+  if (M < 0 || H <= 0 || H % 8) return fail(MX_ERR_INVALID, "bad shape %d x %d", M, H);
+  if (H > kFusedNormMaxH) return fail(MX_ERR_UNSUPPORTED, "H %d > %d", H, kFusedNormMaxH);
+  if (ksplit < 1) return fail(MX_ERR_INVALID, "ksplit %d < 1", ksplit);
+  if (split_row < 0 || split_row > M) return fail(MX_ERR_INVALID, "split_row %d not in [0, M]", split_row);
+  if (M == 0) return MX_OK;
+  if ((split_row < M && !partial) || !R || !x1 || !g || !h) return fail(MX_ERR_NULL, "NULL operand");
+  if (mx_status sa = check_aligned({partial, R, x1, g, h}); sa != MX_OK) return sa;
+  DeviceState* ds;
+  mx_status st = device_state(&ds);
+  if (st != MX_OK) return st;
+  hipError_t e = launch_reduce_residual_rmsnorm(partial, ksplit, R, x1, g, h, M, H, eps, split_row,
+                                                stream);
+  if (e != hipSuccess) return hip_fail(e, "reduce launch");
+  return MX_OK;
 }
 
 MX_EXPORT mx_status mx_profile_enable(int32_t on) {

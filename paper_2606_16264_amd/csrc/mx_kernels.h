@@ -55,10 +55,19 @@ hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* g, uint16_t* out, i
 
 // The residual split-K reduce fused with the RMSNorm of its result:
 // x1 = bf16(sum_z partial[z] + R) over [M][H] fp32 planes (R, x1 [M][H] bf16),
-// then h = RMSNorm(x1, g).  H % 8 == 0 and H <= 8192.
+// then h = RMSNorm(x1, g).  One row per block of kNormThreads threads, each
+// holding kNormChunks 16-byte chunks of the row in registers, so H % 8 == 0 and
+// H <= kFusedNormMaxH; the first kNormPlanes planes are loaded ahead of the
+// first sum, any further ones are summed as they arrive.
+constexpr int kNormThreads = 512;
+constexpr int kNormChunks = 2;
+constexpr int kNormPlanes = 8;
+constexpr int kFusedNormMaxH = 8 * kNormChunks * kNormThreads;
+// Rows below split_row are complete already (x1 written): they are only
+// normalised; the planes hold rows split_row .. M - 1, [ksplit][M - split_row][H].
 hipError_t launch_reduce_residual_rmsnorm(const float* partial, int ksplit, const uint16_t* R,
                                           uint16_t* x1, const uint16_t* g, uint16_t* h, int M,
-                                          int H, float eps, hipStream_t stream);
+                                          int H, float eps, int split_row, hipStream_t stream);
 
 // KV append of given k/v rows [T][nkv][d] into the pools.
 hipError_t launch_kv_append(const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_pool,
@@ -130,13 +139,23 @@ hipError_t launch_gemm(const GemmArgs& args, size_t ws_floats, hipStream_t strea
 // cfg < 0 uses the cost model.
 hipError_t launch_gemm_config(const GemmArgs& args, size_t ws_floats, int cfg, int ksplit,
                               hipStream_t stream);
-// The cost model's plan without the split-K reduce: with a K split (*ksplit > 1
-// on return) the fp32 planes are left at args.partial, [*ksplit][M][N], and
-// args' epilogue is not applied; without one the GEMM runs with its epilogue.
-hipError_t launch_gemm_unreduced(const GemmArgs& args, size_t ws_floats, int* ksplit,
-                                 hipStream_t stream);
+// A forced row split: rows [0, m_main) with tile shape cfg (no K split), then
+// rows [m_main, M) as a GEMM of their own with tile_cfg and tail_ksplit.
+hipError_t launch_gemm_rows(const GemmArgs& args, size_t ws_floats, int m_main, int cfg,
+                            int tail_cfg, int tail_ksplit, hipStream_t stream);
+// The cost model's plan without the last split-K reduce.  On return, rows
+// [0, *split_row) are complete (epilogue applied); when *ksplit > 1, rows
+// [*split_row, M) are left as fp32 planes at args.partial,
+// [*ksplit][M - *split_row][N], without the epilogue (*split_row = M and
+// *ksplit = 1 when every row is complete).
+hipError_t launch_gemm_unreduced(const GemmArgs& args, size_t ws_floats, int* split_row,
+                                 int* ksplit, hipStream_t stream);
 int gemm_num_configs();
 size_t gemm_scratch_floats(int M, int N, int K);
+// The cost model's plan of an M x N x K problem: out[0] tile shape and out[1]
+// K split of rows [0, out[2]); out[3] tile shape and out[4] K split of the
+// remaining rows (out[2] == M: no row split, out[3] = -1).
+void gemm_plan(int M, int N, int K, int out[5]);
 hipError_t gemm_init();
 
 // Weight packing: copies a [N][K] bf16 matrix into the GEMMs' tiled layout

@@ -92,3 +92,26 @@ def truncated_subbatch(b: wl.Batch, rows):
     sub = b.subset(reqs)
     sub.n_new = np.array(n_new, np.int32)
     return sub, reqs, np.array(sub_rows, np.int64), np.array(tok_idx, np.int64)
+
+
+def bf16_half_ulp(v) -> np.ndarray:
+    """Half the bf16 ulp at each value's binade (8 significant bits): the most
+    that rounding a real number to the stored bf16 value v can have moved it."""
+    v = np.abs(np.asarray(v, np.float64))
+    e = np.floor(np.log2(np.maximum(v, 2.0 ** -126)))
+    return 2.0 ** (e - 8)
+
+
+def branch_err_rows(got_branch, exp_branch, allowance) -> tuple:
+    """Per-row error of a residual branch recovered from bf16-stored sums.
+    The GPU stores base + branch rounded once to bf16, so the branch read back
+    as (stored - base) carries up to `allowance` (half an ulp of each stored
+    value involved) per element on top of the kernel's own error.  Returns
+    (raw, net): max_j |got - exp| / max_j |exp| without and with the allowance
+    taken off each element's difference."""
+    got = np.asarray(got_branch, np.float64).reshape(len(got_branch), -1)
+    exp = np.asarray(exp_branch, np.float64).reshape(len(exp_branch), -1)
+    al = np.asarray(allowance, np.float64).reshape(got.shape)
+    diff = np.abs(got - exp)
+    den = np.maximum(np.abs(exp).max(axis=1), 1e-30)
+    return diff.max(axis=1) / den, np.maximum(diff - al, 0.0).max(axis=1) / den

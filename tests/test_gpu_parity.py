@@ -13,8 +13,9 @@ import pytest
 
 import oracle
 import workload as wl
-from helpers import (TOL, assert_rows_close, bits_to_f64, dev, host_bits, mx_batch, mx_cfg,
-                     mx_shape, rel_err_rows, sample_rows, truncated_subbatch)
+from helpers import (TOL, assert_rows_close, bf16_half_ulp, bits_to_f64, branch_err_rows, dev,
+                     host_bits, mx_batch, mx_cfg, mx_shape, rel_err_rows, sample_rows,
+                     truncated_subbatch)
 
 pytestmark = pytest.mark.gpu
 
@@ -363,6 +364,10 @@ def pack_layer(cfg, b, w):
 
 def run_layer(cfg, b, w, x, seed, reps=1, keep_before=False):
     c, packed = pack_layer(cfg, b, w)
+    if b.pool_pages * cfg.kv_bytes_per_token * 16 > (16 << 30):
+        # a pool of this size (the 70B shape's is ~150 GB) must not land next
+        # to a cached block of an earlier one: hand cached memory back first
+        torch.cuda.empty_cache()
     k, v = wdev.alloc_pools(cfg, b.pool_pages)
     wdev.fill_pools(k, v, cfg, b, seed, poison=True)
     before = dict(k0=k.clone(), v0=v.clone()) if keep_before else {}
@@ -418,18 +423,27 @@ def staged_attention(cfg, sub, x_sub, w, kp, vp, sub_rows):
                                    cfg.scale)
 
 
-def check_layer(cfg, b, got, exp, rows_gpu, what, o_ref=None):
+def check_layer(cfg, b, got, exp, rows_gpu, what, o_ref=None, x=None, branch_allowance=True):
     """Stage-by-stage comparison of the GPU iteration with the oracle on the
-    evaluated rows.  Every stage is measured; the layer output y, the branch
-    sum y - x, the projections and the SwiGLU output are gated at 2e-2 against
-    the exact oracle; the attention output is gated at 2e-2 against the
-    stage-emulating oracle pipeline (o_ref, see staged_attention), and its
-    error against the exact oracle is reported."""
+    evaluated rows.  Gated at 2e-2 (max relative error per row) against the
+    exact oracle: q, x1, h2, the SwiGLU output a, the layer output y, and the
+    residual branches with the residual stripped: the attention branch x1 - x,
+    the MLP branch y - x1 and their sum y - x (x: the bf16 input bits of the
+    whole batch).  A branch can be small next to the residual x ~ N(0, 1), so
+    an error in it would hide under y or x1 alone.  The GPU stores x1 and y in
+    bf16, rounded once; a branch read back from them carries up to half an ulp
+    of each stored value involved, which is taken off each element's
+    difference before the 2e-2 gate (branch_allowance; False gates the raw
+    difference).  The attention output o is gated at 2e-2 per head row against
+    the stage-emulating oracle pipeline (o_ref, see staged_attention); its
+    error against the exact oracle is reported per head row and per token row."""
     d = cfg.head_dim
+    n = len(rows_gpu)
     g = lambda name: bits_to_f64(got[name])[rows_gpu]
     errs = {
         "q": rel_err_rows(g("q").reshape(-1, d), exp.q.reshape(-1, d)).max(),
         "o_vs_exact": rel_err_rows(g("o").reshape(-1, d), exp.o.reshape(-1, d)).max(),
+        "o_row_vs_exact": rel_err_rows(g("o").reshape(n, -1), exp.o.reshape(n, -1)).max(),
         "x1": rel_err_rows(g("x1"), exp.x1).max(),
         "h2": rel_err_rows(g("h2"), exp.h2).max(),
         "a": rel_err_rows(g("a"), exp.a).max(),
@@ -437,10 +451,25 @@ def check_layer(cfg, b, got, exp, rows_gpu, what, o_ref=None):
     }
     if o_ref is not None:
         errs["o"] = rel_err_rows(g("o").reshape(-1, d), o_ref.reshape(-1, d)).max()
+    branches = {}
+    if x is not None:
+        xr = wl.bf16_bits_to_f64(np.asarray(x)[rows_gpu])
+        x1g, yg = g("x1"), g("y")
+        hx1, hy = bf16_half_ulp(x1g), bf16_half_ulp(yg)
+        branches = {"x1-x": (x1g - xr, exp.x1 - xr, hx1),
+                    "y-x1": (yg - x1g, exp.y - exp.x1, hy),
+                    "y-x": (yg - xr, exp.y - xr, hx1 + hy)}
+        for name, (gb, eb, al) in branches.items():
+            raw, net = branch_err_rows(gb, eb, al if branch_allowance else np.zeros_like(al))
+            errs[f"{name}_raw"] = raw.max()
+            errs[name] = net.max()
     say(f"  {what} stage errors: " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()))
     for name in ("q", "x1", "h2", "a", "y"):
-        assert_rows_close(g(name).reshape(len(rows_gpu), -1), getattr(exp, name).reshape(len(rows_gpu), -1),
+        assert_rows_close(g(name).reshape(n, -1), getattr(exp, name).reshape(n, -1),
                           what=f"{what} {name}")
+    for name in branches:
+        assert np.isfinite(errs[name]) and errs[name] <= TOL, \
+            f"{what} branch {name}: max per-row relative error {errs[name]:.3e} > {TOL}"
     if o_ref is not None:
         assert_rows_close(g("o").reshape(-1, d), o_ref.reshape(-1, d), what=f"{what} attention o")
     return errs
@@ -472,7 +501,7 @@ def test_layer_step_c1_full():
     exp = oracle.layer_step(cfg.as_dict(), b.n_new, b.ctx_len, x, w, kp, vp)
     rows = np.arange(b.T)
     o_ref = staged_attention(cfg, b, x, w, kp, vp, rows)
-    errs = check_layer(cfg, b, got, exp, rows, "c1", o_ref)
+    errs = check_layer(cfg, b, got, exp, rows, "c1", o_ref, x=x)
     check_pool_rows(cfg, b, got, exp.k_new, exp.v_new, rows)
     say("  errors", {k: f"{v:.2e}" for k, v in errs.items()})
 
@@ -495,7 +524,7 @@ def test_layer_step_small_gqa_full():
     kp, vp = wl.prior_kv_concat(cfg, b, 4242)
     exp = oracle.layer_step(cfg.as_dict(), b.n_new, b.ctx_len, x, ws, kp, vp)
     rows = np.arange(b.T)
-    check_layer(cfg, b, got, exp, rows, "small-gqa", staged_attention(cfg, b, x, ws, kp, vp, rows))
+    check_layer(cfg, b, got, exp, rows, "small-gqa", staged_attention(cfg, b, x, ws, kp, vp, rows), x=x)
     check_pool_rows(cfg, b, got, exp.k_new, exp.v_new, rows)
 
 
@@ -534,7 +563,7 @@ def test_layer_step_aligned_value_runs(cfg):
     kp, vp = wl.prior_kv_concat(cfg, b, 4343)
     exp = oracle.layer_step(cfg.as_dict(), b.n_new, b.ctx_len, x, w, kp, vp)
     rows = np.arange(b.T)
-    check_layer(cfg, b, got, exp, rows, cfg.name, staged_attention(cfg, b, x, w, kp, vp, rows))
+    check_layer(cfg, b, got, exp, rows, cfg.name, staged_attention(cfg, b, x, w, kp, vp, rows), x=x)
     check_pool_rows(cfg, b, got, exp.k_new, exp.v_new, rows)
     written = set(oracle.token_map(b.n_new, b.ctx_len, b.page_tables, 16).tok_slot.tolist())
     assert changed_slots(got["k0"], got["k"], False) <= written
@@ -561,7 +590,7 @@ def test_layer_step_split_reduces_all_rows():
     kp, vp = wl.prior_kv_concat(cfg, b, 2929)
     exp = oracle.layer_step(cfg.as_dict(), b.n_new, b.ctx_len, x, w, kp, vp)
     rows = np.arange(b.T)
-    check_layer(cfg, b, got, exp, rows, cfg.name, staged_attention(cfg, b, x, w, kp, vp, rows))
+    check_layer(cfg, b, got, exp, rows, cfg.name, staged_attention(cfg, b, x, w, kp, vp, rows), x=x)
     check_pool_rows(cfg, b, got, exp.k_new, exp.v_new, rows)
 
 
@@ -625,15 +654,30 @@ def test_layer_step_degenerate_batches(case):
     kp, vp = wl.prior_kv_concat(cfg, b, 515)
     exp = oracle.layer_step(cfg.as_dict(), b.n_new, b.ctx_len, x, w, kp, vp)
     rows = np.arange(b.T)
-    check_layer(cfg, b, got, exp, rows, case, staged_attention(cfg, b, x, w, kp, vp, rows))
+    check_layer(cfg, b, got, exp, rows, case, staged_attention(cfg, b, x, w, kp, vp, rows), x=x)
     check_pool_rows(cfg, b, got, exp.k_new, exp.v_new, rows)
     written = set(oracle.token_map(b.n_new, b.ctx_len, b.page_tables, 16).tok_slot.tolist())
     assert changed_slots(got["k0"], got["k"], False) <= written
     assert changed_slots(got["v0"], got["v"], True) <= written
 
 
-@pytest.mark.parametrize("key,P,ctx", [("c2", 512, 0), ("c2", 0, 0), ("c3", 1024, 0), ("c4", 2048, 0),
-                                       ("c4", 2048, 6144), ("c5", 1024, 0)])
+def gemm_plans(cfg, T):
+    """The cost model's plan of each projection of the layer at T rows."""
+    H, F, nq, nkv, d = cfg.hidden, cfg.ffn, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    return {name: mx.mx_debug_gemm_plan(T, N, K) for name, (N, K) in (
+        ("qkv", ((nq + 2 * nkv) * d, H)), ("o", (H, nq * d)), ("gate_up", (2 * F, H)),
+        ("down", (H, F)))}
+
+
+# Every sweep point of the 13B and 70B shapes that the benchmark reports
+# beyond the chunk-free points (the 70B shape at P = 0, 4096 and 8192 is its
+# headline curve's start, middle and end), plus a chunk after 6144 cached tokens.
+SAMPLED_CASES = [("c2", 512, 0), ("c2", 0, 0), ("c3", 256, 0), ("c3", 1024, 0), ("c3", 2048, 0),
+                 ("c3", 4096, 0), ("c4", 2048, 0), ("c4", 2048, 6144), ("c5", 0, 0),
+                 ("c5", 1024, 0), ("c5", 4096, 0), ("c5", 8192, 0)]
+
+
+@pytest.mark.parametrize("key,P,ctx", SAMPLED_CASES)
 def test_layer_step_sampled(key, P, ctx):
     """Full-size layer iteration (the benchmark's launch configuration),
     checked on sampled rows: the oracle evaluates the requests that own them,
@@ -646,17 +690,236 @@ def test_layer_step_sampled(key, P, ctx):
     w = wl.make_weights(cfg, key)
     x = wl.make_x(cfg, b.T, key)
     seed = wl.kv_seed(key)
+    say(f"  T={b.T} plans: {gemm_plans(cfg, b.T)}")
     got = run_layer(cfg, b, w, x, seed)
     rng = np.random.default_rng(3)
     # the 70B shape's contexts reach 16384 tokens: fewer sampled requests keep
     # the oracle's host copy of their cached keys and values small
     big = key == "c5"
     rows = sample_rows(b, rng, n_decode=4 if big else 16, n_prefill_random=8 if big else 30)
+    if big and b.T > 8192:
+        # rows on both sides of the row split of the 70B projections (8192 rows
+        # in whole rounds of tiles, the rest as a GEMM of their own)
+        rows = np.unique(np.concatenate([rows, [8191, 8192, 8193]]))
     sub, reqs, sub_rows, tok_idx = truncated_subbatch(b, rows)
     kp, vp = wl.prior_kv_concat(cfg, sub, seed)
     exp = oracle.layer_step(cfg.as_dict(), sub.n_new, sub.ctx_len, x[tok_idx], w, kp, vp,
                             rows=sub_rows)
     o_ref = staged_attention(cfg, sub, x[tok_idx], w, kp, vp, sub_rows)
-    errs = check_layer(cfg, b, got, exp, rows, key, o_ref)
+    errs = check_layer(cfg, b, got, exp, rows, key, o_ref, x=x)
     check_pool_rows(cfg, b, got, exp.k_new, exp.v_new, tok_idx)
     say("  errors", {k: f"{v:.2e}" for k, v in errs.items()})
+
+
+def test_layer_step_small_residual_branches():
+    """The residual x scaled down 16-fold (an exact power of two), so that the
+    attention and MLP branches dominate x1 and y: the branches x1 - x, y - x1
+    and y - x are gated at 2e-2 against the exact oracle on the raw
+    difference, with no allowance for the bf16 storage of x1 and y.  (RMSNorm
+    makes h, and so every branch input, nearly independent of x's scale.)"""
+    say("case: layer step with a small residual (branches gated raw)")
+    cfg = SMALL_GQA
+    rng = np.random.default_rng(4545)
+    b = wl.custom_batch(rng, [5, 16, 300, 1000, 2047, 64], [(150, 0), (40, 96), (1, 0)])
+    w = small_weights(rng, cfg)
+    x = wl.f32_to_bf16_bits(rng.standard_normal((b.T, cfg.hidden), dtype=np.float32) / 16.0)
+    got = run_layer(cfg, b, w, x, 616)
+    kp, vp = wl.prior_kv_concat(cfg, b, 616)
+    exp = oracle.layer_step(cfg.as_dict(), b.n_new, b.ctx_len, x, w, kp, vp)
+    rows = np.arange(b.T)
+    check_layer(cfg, b, got, exp, rows, "small-residual", staged_attention(cfg, b, x, w, kp, vp, rows),
+                x=x, branch_allowance=False)
+
+
+# ----------------------------------------------------------------------- GEMM row split
+# A GEMM whose rows run as two launches: rows [0, m_main) in whole rounds of
+# tiles, the rest as a GEMM of its own (split over K or not).  Every epilogue
+# of the debug entry point, ragged tails, weights in the packed tile layout.
+@pytest.mark.parametrize("M,N,K,epi,m_main,main_cfg,tail_cfg,tail_ks", [
+    (700, 2048, 1024, 0, 512, 0, 3, 4), (700, 2048, 1024, 1, 512, 1, 1, 1),
+    (577, 1024, 2048, 2, 512, 2, 3, 8), (1100, 1040, 512, 1, 1024, 0, 0, 3),
+    (300, 4096, 4096, 1, 256, 0, 1, 8), (300, 768, 704, 2, 256, 4, 2, 5),
+])
+def test_gemm_row_split(M, N, K, epi, m_main, main_cfg, tail_cfg, tail_ks):
+    say(f"case: gemm row split M={M} N={N} K={K} epi={epi} m_main={m_main} "
+        f"cfg={main_cfg} tail={tail_cfg}/{tail_ks}")
+    rng = np.random.default_rng(M + 3 * N + K + epi)
+    a = wl.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
+    w = wl.f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * 0.02)
+    r = wl.f32_to_bf16_bits(rng.standard_normal((M, N), dtype=np.float32))
+    ncol = N // 2 if epi == 2 else N
+    lead = -(-2 * ncol // 8) * 8
+    buf16 = torch.full((lead + (M + 2) * ncol,), CANARY, dtype=torch.int16, device="cuda")
+    C = buf16.view(torch.uint16)[lead:lead + M * ncol].view(M, ncol)
+    ws = ws_tensor(max(tail_ks * (M - m_main) * N * 4 if tail_ks > 1 else 0, 256))
+    wt = np.ascontiguousarray(w.reshape(N // 16, 16, K // 32, 32).transpose(0, 2, 1, 3))
+    mx.mx_debug_gemm_rows(dev(a), dev(wt.reshape(-1)), C, dev(r) if epi == 1 else None, epi, N,
+                          m_main, main_cfg, tail_cfg, tail_ks, ws)
+    sync()
+    guard = torch.cat([buf16[:lead], buf16[lead + M * ncol:]]).cpu().numpy()
+    assert (guard == CANARY).all(), "GEMM wrote outside C"
+    acc = oracle.linear(wl.bf16_bits_to_f64(a), w)
+    if epi == 1:
+        exp = acc + wl.bf16_bits_to_f64(r)
+    elif epi == 2:
+        blocks = acc.reshape(M, N // 64, 2, 32)
+        exp = oracle.silu_mul(np.concatenate([blocks[:, :, 0].reshape(M, -1),
+                                              blocks[:, :, 1].reshape(M, -1)], axis=1))
+    else:
+        exp = acc
+    assert_rows_close(bits_to_f64(C), exp, what="gemm row split")
+
+
+def test_gemm_plan_rows_at_benchmark_point():
+    """The 70B-shaped projections at 8448 rows (the benchmark's headline
+    point): down, O and QKV run 8192 rows in whole rounds of 256 x 256 tiles
+    and the last 256 rows as a GEMM of their own split over K; gate/up, whose
+    tiles fill 28.9 rounds, runs as one launch."""
+    plans = gemm_plans(wl.CONFIGS["c5"], 8448)
+    say(f"  plans: {plans}")
+    for name in ("qkv", "o", "down"):
+        assert plans[name]["m_main"] == 8192 and plans[name]["cfg"] == 0, name
+        assert plans[name]["tail_ksplit"] > 1, name
+    assert plans["gate_up"]["m_main"] == 8448
+
+
+# ----------------------------------------------------------------------- fused O reduce + RMSNorm
+@pytest.mark.parametrize("H", [1536, 5120, 8192])
+@pytest.mark.parametrize("ks,split_row", [(2, 0), (8, 0), (9, 0), (4, 37)])
+def test_reduce_residual_rmsnorm(H, ks, split_row):
+    """The output projection's split-K reduce fused with the residual and the
+    second RMSNorm: a partly filled second register chunk (H = 5120), both
+    chunks full (8192), more planes than are loaded ahead (9 > 8), and rows
+    completed by the GEMM itself (split_row > 0: the row split).  x1 against
+    the fp64 sum of the planes and the residual (one bf16 rounding: within
+    half an ulp plus the fp32 sums' error); h against the oracle's RMSNorm of
+    the GPU's x1 at 2e-2, and x1 bit for bit where rows were complete."""
+    say(f"case: reduce+rmsnorm H={H} ks={ks} split_row={split_row}")
+    M = 97
+    rng = np.random.default_rng(H + ks + split_row)
+    planes = (rng.standard_normal((ks, M - split_row, H)) * 0.5).astype(np.float32)
+    r = wl.f32_to_bf16_bits(rng.standard_normal((M, H), dtype=np.float32))
+    x1_done = wl.f32_to_bf16_bits(rng.standard_normal((M, H), dtype=np.float32))
+    g = wl.f32_to_bf16_bits(1 + 0.1 * rng.standard_normal(H, dtype=np.float32))
+    x1 = dev(x1_done)
+    h = torch.empty((M, H), dtype=torch.uint16, device="cuda")
+    mx.mx_debug_reduce_residual_rmsnorm(torch.from_numpy(planes).cuda(), ks, dev(r), x1, dev(g), h,
+                                        eps=1e-5, split_row=split_row)
+    sync()
+    got_x1 = bits_to_f64(x1)
+    np.testing.assert_array_equal(host_bits(x1)[:split_row], x1_done[:split_row])
+    exact = planes.astype(np.float64).sum(axis=0) + wl.bf16_bits_to_f64(r[split_row:])
+    tail = got_x1[split_row:]
+    # fp32 sums of ks planes and the residual: each partial sum's rounding is at
+    # most 2^-24 of the summands' magnitude sum; then one rounding to bf16
+    mag = np.abs(planes.astype(np.float64)).sum(axis=0) + np.abs(wl.bf16_bits_to_f64(r[split_row:]))
+    bound = bf16_half_ulp(tail) + (ks + 1) * mag * 2.0 ** -24 + 1e-30
+    assert (np.abs(tail - exact) <= bound).all(), "x1 off by more than one rounding"
+    exp_h = oracle.rmsnorm(got_x1, wl.bf16_bits_to_f64(g), 1e-5)
+    assert_rows_close(bits_to_f64(h), exp_h, what="h")
+
+
+# ----------------------------------------------------------------------- row split in the layer
+G2048 = wl.LayerConfig("gqa-2048", 2048, 5632, 16, 4, 128)
+
+
+def test_layer_step_row_split_all_rows():
+    """A 2696-row iteration of a 2048-wide GQA layer on which the QKV
+    projection runs its first 2688 rows in whole rounds and the last 8 as a GEMM
+    of their own split over K: the fused QKV epilogue (RoPE, q, and the KV
+    append) of those rows runs in the split reduce with the rotary table,
+    token slots and q rows taken from row 2688 on.  Every row of every stage
+    and every new slot against the oracle."""
+    say("case: layer step with row-split projections (all rows)")
+    cfg = G2048
+    rng = np.random.default_rng(2696)
+    dec = rng.integers(8, 600, size=100)
+    b = wl.custom_batch(rng, dec, [(1000, 0), (900, 37), (696, 5)])
+    assert b.T == 2696
+    plans = gemm_plans(cfg, b.T)
+    say(f"  plans: {plans}")
+    assert plans["qkv"]["m_main"] < b.T and plans["qkv"]["tail_ksplit"] > 1
+    w = small_weights(rng, cfg)
+    x = wl.f32_to_bf16_bits(rng.standard_normal((b.T, cfg.hidden), dtype=np.float32))
+    got = run_layer(cfg, b, w, x, 2696, keep_before=True)
+    kp, vp = wl.prior_kv_concat(cfg, b, 2696)
+    exp = oracle.layer_step(cfg.as_dict(), b.n_new, b.ctx_len, x, w, kp, vp)
+    rows = np.arange(b.T)
+    check_layer(cfg, b, got, exp, rows, cfg.name, staged_attention(cfg, b, x, w, kp, vp, rows), x=x)
+    check_pool_rows(cfg, b, got, exp.k_new, exp.v_new, rows)
+    written = set(oracle.token_map(b.n_new, b.ctx_len, b.page_tables, 16).tok_slot.tolist())
+    assert changed_slots(got["k0"], got["k"], False) <= written
+    assert changed_slots(got["v0"], got["v"], True) <= written
+
+
+# ----------------------------------------------------------------------- randomised batches
+from hypothesis import HealthCheck, given, settings  # noqa: E402
+from hypothesis import strategies as st  # noqa: E402
+
+RANDOM_SETTINGS = dict(derandomize=True, deadline=None, database=None,
+                       suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large,
+                                              HealthCheck.function_scoped_fixture])
+
+
+@st.composite
+def ctx_near_page_edge(draw, lo_pages=0, hi_pages=64):
+    """A cached length that ends on a page boundary or one token short of it."""
+    k = draw(st.integers(lo_pages, hi_pages))
+    return max(16 * k + draw(st.sampled_from([0, 15])), 0)
+
+
+@st.composite
+def mixed_batch(draw, max_prefill=300):
+    """Decodes (1..8, cached lengths at or just below page edges) and prefill
+    chunks (0..3, with or without a cached prefix), in random order."""
+    dec = [max(1, draw(ctx_near_page_edge(0, 80))) for _ in range(draw(st.integers(0, 8)))]
+    pre = [(draw(st.integers(1, max_prefill)), draw(ctx_near_page_edge(0, 20)) * draw(st.integers(0, 1)))
+           for _ in range(draw(st.integers(0 if dec else 1, 3)))]
+    seed = draw(st.integers(0, 2 ** 31 - 1))
+    return dec, pre, seed
+
+
+HEADS = st.sampled_from([(4, 4, 64), (8, 8, 128), (8, 2, 128), (16, 4, 64), (16, 2, 128),
+                         (32, 4, 128), (8, 1, 64)])
+
+
+@settings(max_examples=24, **RANDOM_SETTINGS)
+@given(batch=mixed_batch(), heads=HEADS)
+def test_paged_attn_random_batches(batch, heads):
+    """mx_paged_attn against the exact oracle (same bf16 q, k, v on both sides)
+    on random mixed batches: request count and phases, chunk lengths, cached
+    lengths at page edges, GQA group sizes 1, 4 and 8, head_dim 64 and 128."""
+    dec, pre, seed = batch
+    nq, nkv, d = heads
+    say(f"case: random attention nq={nq} nkv={nkv} d={d} decodes={dec} prefills={pre} seed={seed}")
+    rng = np.random.default_rng(seed)
+    cfg = wl.LayerConfig("t", 256, 256, nq, nkv, d)
+    b = wl.custom_batch(rng, dec, pre)
+    c = attention_case(cfg, b, seed % 1000 + 1, rng)
+    out = torch.empty((b.T, nq, d), dtype=torch.uint16, device="cuda")
+    mx.mx_paged_attn(c["mb"], c["shape"], c["q"], c["k"], c["v"], out, c["ws"])
+    sync()
+    assert_rows_close(bits_to_f64(out).reshape(b.T * nq, d), c["exp"].reshape(b.T * nq, d),
+                      what="attention")
+
+
+@settings(max_examples=10, **RANDOM_SETTINGS)
+@given(batch=mixed_batch(max_prefill=200), heads=HEADS)
+def test_layer_step_random_batches(batch, heads):
+    """mx_layer_step on random mixed batches of a small layer (hidden 512):
+    every row of every stage and the branch sums against the exact oracle,
+    every new slot in the pools."""
+    dec, pre, seed = batch
+    nq, nkv, d = heads
+    say(f"case: random layer nq={nq} nkv={nkv} d={d} decodes={dec} prefills={pre} seed={seed}")
+    rng = np.random.default_rng(seed)
+    cfg = wl.LayerConfig("rand", 512, 704, nq, nkv, d)
+    b = wl.custom_batch(rng, dec, pre)
+    w = small_weights(rng, cfg)
+    x = wl.f32_to_bf16_bits(rng.standard_normal((b.T, cfg.hidden), dtype=np.float32))
+    got = run_layer(cfg, b, w, x, seed % 1000 + 1)
+    kp, vp = wl.prior_kv_concat(cfg, b, seed % 1000 + 1)
+    exp = oracle.layer_step(cfg.as_dict(), b.n_new, b.ctx_len, x, w, kp, vp)
+    rows = np.arange(b.T)
+    check_layer(cfg, b, got, exp, rows, "random", staged_attention(cfg, b, x, w, kp, vp, rows), x=x)
+    check_pool_rows(cfg, b, got, exp.k_new, exp.v_new, rows)

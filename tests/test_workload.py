@@ -65,3 +65,21 @@ def test_prior_kv_matches_host_pool():
             page = b.page_tables[r][j // 16]
             np.testing.assert_array_equal(k[j], kp[page, :, j % 16])
             np.testing.assert_array_equal(v[j], vp[page, :, j % 16])
+
+
+def test_bf16_half_ulp_bounds_rounding():
+    """The branch gates of the layer parity tests take half an ulp of each
+    stored bf16 value off the difference: that must bound the error of
+    rounding any real number to that value (and be no looser than needed)."""
+    import numpy as np
+    from helpers import bf16_half_ulp
+    rng = np.random.default_rng(8)
+    v = np.concatenate([rng.standard_normal(100000) * 10.0 ** rng.integers(-6, 6, 100000),
+                        [1.0, -2.0, 0.5, 255.9, 256.0, 1e-3]])
+    r = wl.bf16_bits_to_f64(wl.f32_to_bf16_bits(v.astype(np.float32)))
+    err = np.abs(r - v.astype(np.float32).astype(np.float64))
+    hu = bf16_half_ulp(r)
+    assert (err <= hu).all()
+    # tight: at 1.0 the bf16 spacing is 2^-7, so half an ulp is 2^-8
+    assert bf16_half_ulp(np.array([1.0, 1.5, 2.0]))[0] == 2.0 ** -8
+    assert bf16_half_ulp(np.array([2.0]))[0] == 2.0 ** -7
