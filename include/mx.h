@@ -5,9 +5,9 @@
  * iterations whose batch mixes requests in the prefill phase (a chunk of
  * prompt tokens, possibly continuing an earlier chunk) with requests in the
  * decode phase (one new token each); prefill chunks are piggybacked onto the
- * running decode batch (paper Section 3.3, "Multiplexing Toggle"; Section 4.1,
+ * running decode batch (paper Section 4.3, "Multiplexing Toggle"; Section 5.1,
  * chunked prefill with one chunk per iteration).  The engine keeps keys and
- * values in a paged cache (Section 4.1: the vLLM-based engine).  Every request
+ * values in a paged cache (Section 5.1: the vLLM-based engine).  Every request
  * is described by its phase, its new-token count, the number of tokens already
  * cached and its page table.
  *
@@ -157,9 +157,15 @@ mx_status mx_pack_weights(const mx_layer_cfg* cfg, const mx_layer_weights* canon
                           void* packed, size_t packed_bytes, hipStream_t stream);
 
 /*
- * KV append (the cache write of the new tokens): k_new, v_new [T][n_kv_heads]
- * [head_dim] are copied to the slots of the token map, k into k_pool's layout
- * and v into v_pool's transposed page layout.  A pure byte copy.
+ * KV append (the cache write of the new tokens).  The evaluation's serving
+ * engine keeps keys and values in a paged cache (paper Section 5.1, the
+ * vLLM-based engine and its baselines); the new tokens' keys and values enter
+ * it before attention reads them.  k_new, v_new [T][n_kv_heads][head_dim] are
+ * copied to the slots of the token map, k into k_pool's layout and v into
+ * v_pool's transposed page layout.  A pure byte copy: the pools are bit-equal
+ * to what a plain copy would leave.  Errors as every entry point: host checks
+ * first (MX_ERR_NULL for a NULL tensor, MX_ERR_INVALID for a misaligned one,
+ * MX_ERR_TOO_LARGE for a short workspace), nothing enqueued on error.
  */
 mx_status mx_kv_append(const mx_batch* batch, const mx_attn_shape* shape,
                        const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_pool,
@@ -167,7 +173,8 @@ mx_status mx_kv_append(const mx_batch* batch, const mx_attn_shape* shape,
 
 /*
  * Paged varlen attention over the mixed batch, one launch for prefill rows
- * and decode rows (paper Section 3.3, chunked prefill piggybacked on decodes):
+ * and decode rows (paper Section 4.2 and Section 4.3: prefill chunks
+ * piggybacked on decodes; Section 5.1: the paged cache of the vLLM-based engine):
  * q [T][n_q_heads][head_dim] -> out [T][n_q_heads][head_dim], bf16.  For token
  * t (request r, position p) and q head h, with g = h / (nq / nkv):
  *   out[t][h] = sum_{j <= p} softmax_j(scale * q[t][h] . K_r[j][g]) V_r[j][g],
@@ -182,7 +189,14 @@ mx_status mx_paged_attn(const mx_batch* batch, const mx_attn_shape* shape, const
                         void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
- * One multiplexed decoder-layer iteration (pre-norm Llama-style layer):
+ * One multiplexed decoder-layer iteration: a multiplexing worker's iteration
+ * in which the prefill chunks the toggle piggybacks onto the running decode
+ * batch (paper Section 4.2, "SLO-Aware Multiplexing", and Section 4.3,
+ * "Multiplexing Toggle"; one chunk per iteration, Section 5.1) pass through
+ * the layer together with the decodes.  Its latency as a function of the
+ * prefill tokens mixed in is the interference the toggle prices against the
+ * decodes' TPOT slack (Section 4.2).  The paper states no layer arithmetic; the
+ * layer is the pre-norm Llama-style layer of the benchmark shapes:
  *   h  = RMSNorm(x) * ln1_g
  *   q, k, v = h W_qkv^T;  RoPE (rotate-half, base rope_theta) on q and k at
  *             each token's position

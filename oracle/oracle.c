@@ -33,8 +33,8 @@ int orc_num_threads(void) {
 }
 
 /*
- * Mixed batch bookkeeping (Section 3.3: prefill chunks are piggybacked onto the
- * decode requests of a multiplexing worker; Section 4.1: the engine keeps a paged
+ * Mixed batch bookkeeping (Section 4.3: prefill chunks are piggybacked onto the
+ * decode requests of a multiplexing worker; Section 5.1: the engine keeps a paged
  * KV cache).  Tokens are concatenated in request order.
  */
 int orc_token_map(int32_t R, const int32_t* n_new, const int32_t* ctx_len,
@@ -233,7 +233,7 @@ static int attention_batch(int32_t R, const int32_t* n_new, const int32_t* ctx_l
   return failed ? -1 : 0;
 }
 
-/* Section 3.3 / Section 4.1: one attention launch serves the prefill rows and the
+/* Section 4.3 / Section 5.1: one attention launch serves the prefill rows and the
  * decode rows of the multiplexed batch. */
 void orc_attention_contig(int32_t R, const int32_t* n_new, const int32_t* ctx_len,
                           int32_t nq, int32_t nkv, int32_t d, double scale,
@@ -423,7 +423,7 @@ int orc_layer_step(const orc_layer_cfg* c, int32_t R, const int32_t* n_new,
   return 0;
 }
 
-/* KV append (vLLM-style paged cache, Section 4.1): a byte copy to the token slots. */
+/* KV append (vLLM-style paged cache, Section 5.1): a byte copy to the token slots. */
 int orc_kv_append(int32_t R, const int32_t* n_new, const int32_t* ctx_len,
                   const int64_t* page_off, const int32_t* pages, int32_t page_size,
                   int32_t nkv, int32_t d, const uint16_t* k_new, const uint16_t* v_new,

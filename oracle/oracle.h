@@ -8,8 +8,8 @@
  * leg of the benchmark do.  It shares no code, header, table or helper with the
  * HIP path.
  *
- * What the paper fixes and what it does not.  The paper (Section 3.3, "Multiplexing
- * Toggle", and Section 4.1, "Experimental Setup") describes a worker iteration in
+ * What the paper fixes and what it does not.  The paper (Section 4.3, "Multiplexing
+ * Toggle", and Section 5.1, "Experimental Setup") describes a worker iteration in
  * which chunked prefill requests are piggybacked onto the running decode batch,
  * served by a vLLM-style engine with a paged KV cache.  It states no layer
  * arithmetic.  The layer computed here is the textbook pre-norm decoder layer

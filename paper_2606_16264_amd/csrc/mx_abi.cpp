@@ -382,6 +382,20 @@ hipError_t close_group(DeviceState* ds, int last) {
   return hipSuccess;
 }
 
+// The metadata block [0, L.meta_end) of the workspace, as the kernels read it:
+// request records, page tables, attention work items, merge items, rotary
+// inverse frequencies.
+void pack_meta(const Plan& p, const Layout& L, const mx_attn_shape* s, float theta, char* h) {
+  memset(h, 0, L.meta_end);
+  if (!p.reqs.empty()) memcpy(h + L.reqs, p.reqs.data(), p.reqs.size() * sizeof(ReqDev));
+  if (!p.pages.empty()) memcpy(h + L.pages, p.pages.data(), p.pages.size() * sizeof(int32_t));
+  if (!p.items.empty()) memcpy(h + L.items, p.items.data(), p.items.size() * sizeof(AttnItem));
+  if (!p.merges.empty()) memcpy(h + L.merges, p.merges.data(), p.merges.size() * sizeof(MergeItem));
+  double* inv = (double*)(h + L.inv_freq);
+  const int d = s->head_dim;
+  for (int k = 0; k < d / 2; k++) inv[k] = std::pow((double)theta, -2.0 * k / d);
+}
+
 mx_status upload_meta(const Plan& p, const Layout& L, const mx_attn_shape* s, float theta,
                       void* ws, hipStream_t stream) {
   DeviceState* ds;
@@ -419,15 +433,7 @@ mx_status upload_meta(const Plan& p, const Layout& L, const mx_attn_shape* s, fl
     }
     ds->cap[i] = cap;
   }
-  char* h = (char*)ds->buf[i];
-  memset(h, 0, L.meta_end);
-  if (!p.reqs.empty()) memcpy(h + L.reqs, p.reqs.data(), p.reqs.size() * sizeof(ReqDev));
-  if (!p.pages.empty()) memcpy(h + L.pages, p.pages.data(), p.pages.size() * sizeof(int32_t));
-  if (!p.items.empty()) memcpy(h + L.items, p.items.data(), p.items.size() * sizeof(AttnItem));
-  if (!p.merges.empty()) memcpy(h + L.merges, p.merges.data(), p.merges.size() * sizeof(MergeItem));
-  double* inv = (double*)(h + L.inv_freq);
-  const int d = s->head_dim;
-  for (int k = 0; k < d / 2; k++) inv[k] = std::pow((double)theta, -2.0 * k / d);
+  pack_meta(p, L, s, theta, (char*)ds->buf[i]);
   e = launch_upload(ds->dbuf[i], ws, L.meta_end, stream);
   if (e != hipSuccess) return hip_fail(e, "metadata upload launch");
   ds->used[i] = true;

@@ -1,5 +1,5 @@
 """Iteration-latency predictor (the offline-profiled execution-time estimate
-the multiplexing toggle relies on, Section 3.3; prefill and decode execution
+the multiplexing toggle relies on, Section 4.3; prefill and decode execution
 times are taken as highly predictable there, which the fit's residuals test).
 
 A mixed iteration's latency is modelled as linear in the work its parts do:

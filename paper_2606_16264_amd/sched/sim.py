@@ -1,7 +1,7 @@
 """Discrete-event simulator of prefill/decode scheduling on a group of workers,
 driven by the iteration-latency model (per layer, times the model's layers).
 
-Policies (Section 3 and the baselines of Section 4.1):
+Policies (Section 4 and the baselines of Section 5.1):
   colocated      every worker mixes its running decodes with one prefill chunk
                  per iteration (non-disaggregated serving with chunked prefill);
                  new requests go to the worker with the fewest unfinished tokens.
@@ -313,7 +313,7 @@ def synthetic_requests(rate_per_s: float, n: int, seed: int, prompt_median: floa
 def light_load_slo(model: LatencyModel, layers: int, prompt_median: int, ctx_median: int,
                    factor: float = 5.0, **gates) -> SLO:
     """SLOs at `factor` times the light-load latency of each phase: the median
-    prompt's prefill alone, and one decode step of one request (Section 4.1
+    prompt's prefill alone, and one decode step of one request (Section 5.1
     sets them at five times the light-load latency)."""
     ttft = model.predict_batch([prompt_median], [0], [False]) * layers
     tpot = model.predict_batch([1], [ctx_median], [True]) * layers

@@ -5,14 +5,14 @@ time from its arrival to its first token is within TTFT_SLO, and its TPOT SLO
 when the total time of its decode iterations divided by its generation length
 L_r is within TPOT_SLO; attainment is the fraction of requests meeting both.
 
-TPOT slack (Sections 2.2 and 3.2): every decode iteration of a request that
+TPOT slack (Sections 2.2 and 4.2): every decode iteration of a request that
 takes less than TPOT_SLO adds the difference to the request's slack.  A
 prefill chunk may be piggybacked onto the next decode iteration of a
 multiplexing worker only if, for every decode request running there, the
 predicted iteration time with the chunk fits in one TPOT_SLO plus the slack
 the request has accumulated (so its running TPOT stays within the SLO), and
 only if the decode batch alone is not already close to the SLO and the
-worker's decode KV-cache use is under its HBM watermark (Section 3.3).
+worker's decode KV-cache use is under its HBM watermark (Section 4.3).
 """
 from __future__ import annotations
 

@@ -5,7 +5,7 @@ This module is shared by the oracle side (tests, CPU baseline) and the HIP side
 weights, activations, batch shapes, page tables and cached key/value contents.
 
 Inputs are shaped like the chat-style serving iterations the paper studies
-(Section 3.1: long-tailed prompt lengths; Section 4.1: chunked prefill with
+(Section 3.1: long-tailed prompt lengths; Section 5.1: chunked prefill with
 2048-token chunks, decode batches of running requests).  The paper measures on a
 production trace that is not available here; these synthetic batches stand in
 for the per-iteration shape of that trace and reproduce none of its records.
