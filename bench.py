@@ -59,26 +59,43 @@ def parse():
                          "latency model that `--predictor` printed (MODEL_JSON); prints one JSON line")
     ap.add_argument("--rates", type=float, nargs="+", default=[4, 8, 16, 24, 32, 48])
     ap.add_argument("--requests", type=int, default=800)
-    ap.add_argument("--summarize-stats", nargs=3, metavar=("STATS_CSV", "COMMAND", "OUT_MD"),
-                    help="write a markdown summary of a rocprofv3 --stats kernel_stats.csv "
+    ap.add_argument("--summarize-stats", nargs=4,
+                    metavar=("STATS_CSV", "COMMAND", "WORKLOAD", "OUT_MD"),
+                    help="write a markdown summary of a rocprofv3 --stats kernel_stats.csv of "
+                         "the step on WORKLOAD (e.g. c5_P8192) (no GPU needed)")
+    ap.add_argument("--summarize-traffic", nargs="+",
+                    metavar="ARG",
+                    help="FETCH_CSV WRITE_CSV COMMANDS_TXT WORKLOAD OUT_JSON [TAG KERNEL_NAME]: "
+                         "HBM bytes per launch of one kernel of the step (default: the attention; "
+                         "TAG a step tag such as gemm_gate_up and KERNEL_NAME the exact kernel "
+                         "name prefix in the trace) from two rocprofv3 --pmc runs (FETCH_SIZE, "
+                         "WRITE_SIZE), scaled by the 1 GiB copy calibration they contain "
                          "(no GPU needed)")
-    ap.add_argument("--summarize-traffic", nargs=5,
-                    metavar=("FETCH_CSV", "WRITE_CSV", "COMMANDS_TXT", "WORKLOAD", "OUT_JSON"),
-                    help="HBM bytes per launch of paged_attn_kernel from two rocprofv3 --pmc "
-                         "runs (FETCH_SIZE, WRITE_SIZE), scaled by the 1 GiB copy calibration "
-                         "they contain (no GPU needed)")
     return ap.parse_args()
 
 
-def summarize_stats(csv_path, command, out_md):
+def workload_text(workload):
+    """One line describing a sweep point such as c5_P8192."""
+    import workload as wl
+    key, P = workload.split("_P")
+    cfg = wl.CONFIGS[key]
+    b = wl.make_batch(key, int(P))
+    n_dec = int((b.phase == wl.DECODE).sum())
+    return (f"{cfg.name}-shaped layer: hidden {cfg.hidden}, {cfg.n_q_heads} query / "
+            f"{cfg.n_kv_heads} KV heads x {cfg.head_dim}, FFN {cfg.ffn}; {n_dec} decodes "
+            f"(contexts {int(b.ctx_len[b.phase == wl.DECODE].min())}.."
+            f"{int(b.ctx_len[b.phase == wl.DECODE].max())}) with {b.prefill_tokens} mixed prefill "
+            f"tokens, T = {b.T}")
+
+
+def summarize_stats(csv_path, command, workload, out_md):
     """Markdown table of a rocprofv3 --kernel-trace --stats summary."""
     import csv
     rows = list(csv.DictReader(open(csv_path)))
     total = sum(float(r["TotalDurationNs"]) for r in rows)
-    lines = ["# Kernel trace statistics: the layer step on the Llama-7B-shaped layer", "",
-             "Workload: hidden 4096, 32 x 128 MHA, FFN 11008; 64 decodes (contexts uniform in "
-             "[512, 2048]) with 512 mixed prefill tokens (the benchmark point, T = 576), including "
-             "setup (weight packing, pool fill) and the per-kernel timing steps.", "",
+    lines = [f"# Kernel trace statistics: the layer step, {workload}", "",
+             f"Workload: {workload_text(workload)}.  The run includes setup (weight packing, pool "
+             "fill) and the per-kernel timing steps.", "",
              "Command (one MI355X):", "", "```", command, "```", "",
              "Durations in microseconds (rocprofv3 kernel trace).  gemm_kernel<BM, BN, WM, WN, LDS stages, "
              "epilogue, split>: epilogue 0 store, 1 residual, 2 SwiGLU, 3 QKV.", "",
@@ -95,11 +112,21 @@ def summarize_stats(csv_path, command, out_md):
         f.write("\n".join(lines) + "\n")
 
 
+# step tag -> (algorithmic part, source file of its kernel)
+TRAFFIC_TAGS = {"paged_attn": ("attention", "paper_2606_16264_amd/csrc/attention.hip"),
+                "gemm_qkv": ("qkv", "paper_2606_16264_amd/csrc/gemm.hip"),
+                "gemm_o": ("o", "paper_2606_16264_amd/csrc/gemm.hip"),
+                "gemm_gate_up": ("gate_up", "paper_2606_16264_amd/csrc/gemm.hip"),
+                "gemm_down": ("down", "paper_2606_16264_amd/csrc/gemm.hip")}
+
+
 def summarize_traffic(fetch_csv, write_csv, commands_txt, workload, out_json,
-                      kernel="paged_attn_kernel", source="paper_2606_16264_amd/csrc/attention.hip"):
-    """HBM bytes per launch of `kernel`: FETCH_SIZE and WRITE_SIZE (KiB per
-    dispatch) scaled by what the same counters read for the 1 GiB device copy
-    (torch's copyBuffer) recorded in the same runs."""
+                      tag="paged_attn", kernel="paged_attn_kernel"):
+    """HBM bytes per launch of `kernel` (the kernel of step `tag`):
+    FETCH_SIZE and WRITE_SIZE (KiB per dispatch) scaled by what the same
+    counters read for the 1 GiB device copy (torch's copyBuffer) recorded in
+    the same runs."""
+    part, source = TRAFFIC_TAGS[tag]
     import csv
     calib = 1 << 30
 
@@ -109,7 +136,9 @@ def summarize_traffic(fetch_csv, write_csv, commands_txt, workload, out_json,
             if r["Counter_Name"] != counter:
                 continue
             v = float(r["Counter_Value"])
-            if kernel in r["Kernel_Name"]:
+            name = r["Kernel_Name"].replace("(anonymous namespace)::", "").replace("mx::", "")
+            name = name.replace("void ", "")
+            if name.startswith(kernel):
                 ks.append(v)
             elif "copyBuffer" in r["Kernel_Name"]:
                 cp.append(v)
@@ -122,7 +151,7 @@ def summarize_traffic(fetch_csv, write_csv, commands_txt, workload, out_json,
     key, P = workload.split("_P")
     import workload as wl
     parts = algorithmic(wl.CONFIGS[key], wl.make_batch(key, int(P)))
-    rec = {"kernel": kernel, "workload": workload,
+    rec = {"kernel": kernel, "tag": tag, "workload": workload,
            "commands": [l.strip() for l in open(commands_txt) if l.strip()],
            "copy_calibration": {"bytes": calib, "FETCH_SIZE_KiB": cf, "WRITE_SIZE_KiB": cw,
                                 "fetch_scale": round(fs, 4), "write_scale": round(ws_, 4)},
@@ -130,7 +159,7 @@ def summarize_traffic(fetch_csv, write_csv, commands_txt, workload, out_json,
            "WRITE_SIZE_KiB_mean": round(sum(kw) / len(kw), 1),
            "fetch_bytes_per_launch": int(fetch), "write_bytes_per_launch": int(write),
            "hbm_bytes_per_launch": int(fetch + write),
-           "algorithmic_bytes_per_launch": int(parts["attention"]["bytes"]),
+           "algorithmic_bytes_per_launch": int(parts[part]["bytes"]),
            "source_sha256": source_sha(source)}
     with open(out_json, "w") as f:
         json.dump(rec, f, indent=1)
@@ -456,7 +485,10 @@ def main():
         summarize_stats(*args.summarize_stats)
         return
     if args.summarize_traffic:
-        summarize_traffic(*args.summarize_traffic)
+        a = args.summarize_traffic
+        if len(a) not in (5, 7):
+            sys.exit("--summarize-traffic takes 5 or 7 arguments")
+        summarize_traffic(*a)
         return
     if args.simulate:
         from paper_2606_16264_amd.sched import LatencyModel, compare

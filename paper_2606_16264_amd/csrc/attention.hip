@@ -97,6 +97,26 @@ struct StepP {
 // is the softmax itself.
 constexpr float kLazyMax = 8.0f;
 
+// Max and sum of a query row's values over its four lane groups (lanes l,
+// l ^ 16, l ^ 32, l ^ 48).  v_permlane16_swap and v_permlane32_swap with both
+// operands equal to x leave, in every lane, the even-row (lower-half) value in
+// the first result and the odd-row (upper-half) value in the second: the lane's
+// own value and its partner's, in the same order in both lanes of a pair.  So
+// each step is one VALU swap and one VALU op, with no LDS permute, and the sum
+// is bit-identical in the four lanes of a row.
+__device__ __forceinline__ float lane_groups_max(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float lane_groups_sum(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 // Score block b of S^T = K Q^T (16 keys x 16 rows).
 template <int HD>
 __device__ __forceinline__ f32x4 score_block(const u32x4 (&kf)[HD / 32], const bf16x8 (&qf)[HD / 32]) {
@@ -123,9 +143,7 @@ __device__ __forceinline__ StepP softmax_step(const f32x4 (&s)[2], float& m, flo
       sv[b][i] = (!MASK || (pvalid && j <= row_pos)) ? s[b][i] : kNegBig;
       mx = fmaxf(mx, sv[b][i]);
     }
-  mx = fmaxf(mx, __shfl_xor(mx, 16));
-  mx = fmaxf(mx, __shfl_xor(mx, 32));
-  mx *= scale_log2;  // scale > 0: the max of the scaled scores
+  mx = lane_groups_max(mx) * scale_log2;  // scale > 0: the max of the scaled scores
   const bool raise = mx > m + kLazyMax;
   const float m_new = raise ? mx : m;
   const float alpha = raise ? exp2f(m - mx) : 1.f;
@@ -138,8 +156,7 @@ __device__ __forceinline__ StepP softmax_step(const f32x4 (&s)[2], float& m, flo
       pv[b][i] = exp2f(fmaf(sv[b][i], scale_log2, -m_new));
       ps += pv[b][i];
     }
-  ps += __shfl_xor(ps, 16);
-  ps += __shfl_xor(ps, 32);
+  ps = lane_groups_sum(ps);
   l = l * alpha + ps;
   m = m_new;
   u32x4 pb_bits;
