@@ -189,6 +189,25 @@ mx_status mx_paged_attn(const mx_batch* batch, const mx_attn_shape* shape, const
                         void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * mx_paged_attn without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same kernels and the same results, bit for bit, with
+ * the call's metadata and split partials in a static device array of
+ * mx_paged_attn_static_max_bytes() bytes (32 MiB) that the library holds on
+ * every GPU it runs on until the process ends.  Allocates no device or pinned
+ * host memory: the metadata is packed on the host and copied into the array
+ * with hipMemcpyAsync on the stream.  A batch whose metadata and partials
+ * need more than the array holds returns MX_ERR_TOO_LARGE before any device
+ * work.  All calls on one GPU share that GPU's array: calls that overlap on one
+ * GPU (different streams, or threads without ordering) race; calls ordered on
+ * one stream do not.  Other errors as mx_paged_attn.
+ */
+size_t mx_paged_attn_static_max_bytes(void);
+mx_status mx_paged_attn_static(const mx_batch* batch, const mx_attn_shape* shape, const uint16_t* q,
+                               const uint16_t* k_pool, const uint16_t* v_pool, uint16_t* out,
+                               hipStream_t stream);
+
+/*
  * One multiplexed decoder-layer iteration: a multiplexing worker's iteration
  * in which the prefill chunks the toggle piggybacks onto the running decode
  * batch (paper Section 4.2, "SLO-Aware Multiplexing", and Section 4.3,

@@ -30,7 +30,7 @@ EXPORTED = [
     "mx_paged_attn", "mx_layer_step", "mx_layer_workspace_offsets", "mx_debug_token_map",
     "mx_debug_gather", "mx_debug_gemm_ws_bytes", "mx_debug_gemm", "mx_debug_gemm_config",
     "mx_debug_gemm_tiled", "mx_debug_gemm_plan", "mx_debug_gemm_rows",
-    "mx_debug_reduce_residual_rmsnorm",
+    "mx_debug_reduce_residual_rmsnorm", "mx_paged_attn_static", "mx_paged_attn_static_max_bytes",
     "mx_profile_enable", "mx_profile_read",
 ]
 
@@ -92,6 +92,8 @@ def _load() -> ctypes.CDLL:
         "mx_kv_append": ([BP, SP, P, P, P, P, P, SZ, P], ctypes.c_int),
         "mx_paged_attn": ([BP, SP, P, P, P, P, P, SZ, P], ctypes.c_int),
         "mx_layer_step": ([BP, CP, P, P, P, P, P, P, SZ, P], ctypes.c_int),
+        "mx_paged_attn_static": ([BP, SP, P, P, P, P, P], ctypes.c_int),
+        "mx_paged_attn_static_max_bytes": ([], SZ),
         "mx_layer_workspace_offsets": ([BP, CP, ctypes.POINTER(SZ)], ctypes.c_int),
         "mx_debug_token_map": ([BP, SP, P, P, P, P, SZ, P], ctypes.c_int),
         "mx_debug_gather": ([BP, SP, I32, P, P, P, P, P, SZ, P], ctypes.c_int),
@@ -234,6 +236,18 @@ def mx_kv_append(batch: Batch, shape: AttnShape, k_new, v_new, k_pool, v_pool, w
 def mx_paged_attn(batch: Batch, shape: AttnShape, q, k_pool, v_pool, out, ws, stream=None) -> None:
     _check(_lib.mx_paged_attn(batch.ptr, ctypes.byref(shape), _ptr(q), _ptr(k_pool), _ptr(v_pool),
                               _ptr(out), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def mx_paged_attn_static(batch: Batch, shape: AttnShape, q, k_pool, v_pool, out,
+                         stream=None) -> None:
+    """mx_paged_attn with the library's static device scratch instead of a
+    workspace (no allocation); calls on one GPU must not overlap."""
+    _check(_lib.mx_paged_attn_static(batch.ptr, ctypes.byref(shape), _ptr(q), _ptr(k_pool),
+                                     _ptr(v_pool), _ptr(out), _stream(stream)))
+
+
+def mx_paged_attn_static_max_bytes() -> int:
+    return int(_lib.mx_paged_attn_static_max_bytes())
 
 
 def mx_layer_step(batch: Batch, cfg: LayerCfg, packed, x, y, k_pool, v_pool, ws,

@@ -723,6 +723,80 @@ MX_EXPORT mx_status mx_paged_attn(const mx_batch* batch, const mx_attn_shape* sh
   return MX_OK;
 }
 
+// ------------------------------------------------------------------ static scratch
+// Device memory of mx_paged_attn_static: the metadata block and the split
+// partials of one call, in a file-scope array of kStaticScratchBytes that
+// every GPU the library runs on holds until the process ends.  Host code uses
+// the array only through the device address hipGetSymbolAddress returns for
+// the current device (the array's name is a host-side stand-in, not a device
+// address); the address is taken once per device, on the entry point's first
+// call there, and kept.
+constexpr size_t kStaticScratchBytes = size_t(32) << 20;
+static __device__ __align__(256) char scratch[kStaticScratchBytes];
+
+std::mutex g_scratch_mu;
+std::map<int, void*> g_scratch_ptr;
+
+mx_status static_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  auto it = g_scratch_ptr.find(dev);
+  if (it != g_scratch_ptr.end()) {
+    *out = it->second;
+    return MX_OK;
+  }
+  void* ptr = nullptr;
+  e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+  if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress (static scratch)");
+  if (!ptr) return fail(MX_ERR_HIP, "hipGetSymbolAddress returned NULL for the static scratch");
+  g_scratch_ptr[dev] = ptr;
+  *out = ptr;
+  return MX_OK;
+}
+
+MX_EXPORT size_t mx_paged_attn_static_max_bytes(void) { return kStaticScratchBytes; }
+
+MX_EXPORT mx_status mx_paged_attn_static(const mx_batch* batch, const mx_attn_shape* shape,
+                                         const uint16_t* q, const uint16_t* k_pool,
+                                         const uint16_t* v_pool, uint16_t* out,
+                                         hipStream_t stream) {
+  g_err.clear();
+  int64_t T;
+  mx_status st = validate_batch(batch, shape, &T);
+  if (st != MX_OK) return st;
+  if (T == 0) return MX_OK;
+  if (!q || !k_pool || !v_pool || !out) return fail(MX_ERR_NULL, "tensor pointer is NULL");
+  if ((st = check_aligned({q, k_pool, v_pool, out})) != MX_OK) return st;
+  Plan p;
+  build_plan(batch, shape, true, p);
+  const Layout L = layout_for(p, shape, nullptr);
+  if (L.total > kStaticScratchBytes)
+    return fail(MX_ERR_TOO_LARGE,
+                "batch needs %zu bytes of scratch; the static scratch holds %zu (use mx_paged_attn "
+                "with a workspace)",
+                L.total, kStaticScratchBytes);
+  void* ws = nullptr;
+  if ((st = static_scratch(&ws)) != MX_OK) return st;
+  // the metadata block, packed on the host and copied into the scratch in
+  // stream order (nothing in the scratch needs to start at zero: every split
+  // partial is written by its item before the merge reads it)
+  thread_local std::vector<char> host;
+  if (host.size() < L.meta_end) host.resize(L.meta_end);
+  pack_meta(p, L, shape, 1e4f, host.data());
+  hipError_t e = hipMemcpyAsync(ws, host.data(), L.meta_end, hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (metadata)");
+  AttnParams a = attn_params(p, L, shape, ws, q, (int64_t)shape->n_q_heads * shape->head_dim,
+                             k_pool, v_pool, out);
+  e = timed("paged_attn", stream, [&] {
+    return launch_paged_attn(a, (int)p.items.size(), at<MergeItem>(ws, L.merges),
+                             (int)p.merges.size(), shape->head_dim, stream);
+  });
+  if (e != hipSuccess) return hip_fail(e, "attention launch");
+  return MX_OK;
+}
+
 MX_EXPORT mx_status mx_layer_step(const mx_batch* batch, const mx_layer_cfg* cfg,
                                   const void* packed_weights, const uint16_t* x, uint16_t* y,
                                   uint16_t* k_pool, uint16_t* v_pool, void* ws, size_t ws_bytes,
