@@ -370,28 +370,35 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   // DMA: instruction j (wave w issues j = w L .. w L + L - 1) fills rows
   // 16 j .. 16 j + 15 of the stacked A|B tile; lane l lands at row 16 j + l / 4,
   // stored chunk l % 4, which holds logical chunk (l % 4) ^ swz(row).
-  // (an instruction's 16 rows are all A or all B: BM is a multiple of 16)
-  const uint16_t* src[L];
-  int64_t kstep[L];
+  // (an instruction's 16 rows are all A or all B: BM is a multiple of 16, so
+  // which operand an instruction reads is wave-uniform.)  Each lane keeps a
+  // pointer to its 16 bytes of the next slice to issue, advanced by a scalar
+  // step after every issue (no per-slice address multiply), and the LDS
+  // destination is scalar arithmetic on the wave index.
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const uint16_t* dsrc[L];
+  int64_t dstep[L];
 #pragma unroll
   for (int i = 0; i < L; i++) {
-    const int row = (wave * L + i) * 16 + (lane >> 2);
+    const int row0 = (wave_s * L + i) * 16;  // first tile row of instruction i
+    const int row = row0 + (lane >> 2);
     const int c = (lane & 3) ^ swz(row);
-    if (row < BM) {
-      src[i] = a.A + (int64_t)min(m0 + row, a.M - 1) * a.lda + kbeg + c * 8;
-      kstep[i] = BKS;
+    if (row0 < BM) {
+      dsrc[i] = a.A + (int64_t)min(m0 + row, a.M - 1) * a.lda + kbeg + c * 8;
+      dstep[i] = BKS;
     } else {
       const int n = min(n0 + row - BM, a.N - 1);
-      src[i] = a.B + (int64_t)(n >> 4) * a.b_blk + (int64_t)(n & 15) * a.b_row +
-               (int64_t)(kbeg >> 5) * a.b_kstep + c * 8;
-      kstep[i] = a.b_kstep;
+      dsrc[i] = a.B + (int64_t)(n >> 4) * a.b_blk + (int64_t)(n & 15) * a.b_row +
+                (int64_t)(kbeg >> 5) * a.b_kstep + c * 8;
+      dstep[i] = a.b_kstep;
     }
   }
-  auto issue = [&](int st) {
-    const int kk = min(st, nk - 1);  // past the end: re-fetch the last slice (never read)
+  // DMA instruction i of slice st into its LDS slot; slices are issued in
+  // order, and past the end the last slice is fetched again (never read)
+  auto dma_one = [&](int i, int st) {
     const unsigned slot = sbase + (unsigned)((st % NS) * STAGE);
-#pragma unroll
-    for (int i = 0; i < L; i++) dma16(src[i] + kk * kstep[i], slot + (wave * L + i) * 1024);
+    dma16(dsrc[i], slot + (unsigned)((wave_s * L + i) * 1024));
+    if (st < nk - 1) dsrc[i] += dstep[i];
   };
 
   f32x16 acc[MB][NB];
@@ -417,33 +424,49 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   // k-step ks of a stage reads logical chunk 2 ks + fk; the XOR with the row
   // term commutes with the +2 (bit 1 only), so ks = 1 is the base ^ 32 bytes
   u32x4 fa[2][MB], fb[2][NB];
-  auto read_frags = [&](int buf, int st, int ks) {
+  // fragment read r (A rows first, then B) of k-step ks of stage st into buffer buf
+  auto read_one = [&](int buf, int st, int ks, int r) {
     const unsigned slot = sbase + (unsigned)((st % NS) * STAGE);
     const unsigned kx = ks ? 32u : 0u;
-#pragma unroll
-    for (int i = 0; i < MB; i++) fa[buf][i] = lds_read16(slot + (aoff[i] ^ kx));
-#pragma unroll
-    for (int j = 0; j < NB; j++) fb[buf][j] = lds_read16(slot + (boff[j] ^ kx));
+    if (r < MB)
+      fa[buf][r] = lds_read16(slot + (aoff[r] ^ kx));
+    else
+      fb[buf][r - MB] = lds_read16(slot + (boff[r - MB] ^ kx));
+  };
+  constexpr int NM = MB * NB;  // MFMAs per k-step
+  auto mfma_one = [&](int buf, int idx) {
+    const int i = idx / NB, j = idx % NB;
+    acc[i][j] = mfma32(as_bf16x8(fa[buf][i]), as_bf16x8(fb[buf][j]), acc[i][j]);
   };
 
-  // One slice: its two k-steps.  `more` issues the fragment reads of the next
-  // slice's first k-step behind the barrier.  The last slice must not: the
-  // compiler sees the result of a read that is never consumed as dead and may
-  // hand its registers to the epilogue while the read is still in flight, and
-  // the landing data would then overwrite them.
+  // One slice: its two k-steps.  The MFMAs of each k-step go out one at a
+  // time, with the slice's memory instructions spread between them (the DMA
+  // of slice kt + NS - 1 among the first k-step's, the next slice's first
+  // fragment reads among the second's), so that a wave keeps the matrix core
+  // fed while it issues them: with the instructions in bursts, the two waves
+  // of a SIMD, lined up by the barrier, issued theirs at the same time and
+  // the matrix core idled meanwhile.  `more` issues the fragment reads of the
+  // next slice's first k-step.  The last slice must not: the compiler sees the
+  // result of a read that is never consumed as dead and may hand its registers
+  // to the epilogue while the read is still in flight, and the landing data
+  // would then overwrite them.
   auto slice = [&](int kt, bool more) {
     __builtin_amdgcn_sched_barrier(0);
-    // slot (kt + NS - 1) % NS was last read in slice kt - 1, before its barrier
-    issue(kt + NS - 1);
-    read_frags(1, kt, 1);
+#pragma unroll
+    for (int r = 0; r < NREAD; r++) read_one(1, kt, 1, r);
     lgkm_wait<NREAD>();  // the k-step 0 fragments (older reads) have landed
     pin(fa[0]);
     pin(fb[0]);
+    // slot (kt + NS - 1) % NS was last read in slice kt - 1, before its barrier
 #pragma unroll
-    for (int i = 0; i < MB; i++)
+    for (int idx = 0; idx < NM; idx++) {
+      mfma_one(0, idx);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int j = 0; j < NB; j++) acc[i][j] = mfma32(as_bf16x8(fa[0][i]), as_bf16x8(fb[0][j]), acc[i][j]);
-    __builtin_amdgcn_sched_barrier(0);
+      for (int i = 0; i < L; i++)
+        if (i * NM / L == idx) dma_one(i, kt + NS - 1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
     // own DMA of stage kt + 1 landed, own reads of stage kt done; after the
     // barrier everyone's are, so stage kt + 1 is readable and slot kt % NS free
     vm_wait<VM_KEEP>();
@@ -451,19 +474,27 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
     pin(fa[1]);
     pin(fb[1]);
     wg_barrier();
-    if (more) read_frags(0, kt + 1, 0);
 #pragma unroll
-    for (int i = 0; i < MB; i++)
+    for (int idx = 0; idx < NM; idx++) {
+      mfma_one(1, idx);
+      __builtin_amdgcn_sched_barrier(0);
+      if (more) {
 #pragma unroll
-      for (int j = 0; j < NB; j++) acc[i][j] = mfma32(as_bf16x8(fa[1][i]), as_bf16x8(fb[1][j]), acc[i][j]);
-    __builtin_amdgcn_sched_barrier(0);
+        for (int r = 0; r < NREAD; r++)
+          if (r * NM / NREAD == idx) read_one(0, kt + 1, 0, r);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
   };
 
 #pragma unroll
-  for (int st = 0; st < NS - 1; st++) issue(st);
+  for (int st = 0; st < NS - 1; st++)
+#pragma unroll
+    for (int i = 0; i < L; i++) dma_one(i, st);
   vm_wait<VM_KEEP>();
   wg_barrier();
-  read_frags(0, 0, 0);
+#pragma unroll
+  for (int r = 0; r < NREAD; r++) read_one(0, 0, 0, r);
   for (int kt = 0; kt < nk - 1; kt++) slice(kt, true);
   slice(nk - 1, false);
   // drain: no DMA may still target this workgroup's LDS when it exits (no
