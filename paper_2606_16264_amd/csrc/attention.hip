@@ -117,6 +117,14 @@ __device__ __forceinline__ float lane_groups_sum(float x) {
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
+// 2^x with the hardware exponential alone (v_exp_f32).  exp2f adds a range
+// reduction that keeps results below 2^-126 as denormals (six instructions
+// instead of one); a softmax never needs them: every probability is
+// 2^(score - m) with the row's running max m at most 2^8 below its largest
+// score, so a term under 2^-126 is below 2^-134 of the row's sum and its
+// flush to zero changes nothing, and masked scores (-1e30) give exactly 0.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // Score block b of S^T = K Q^T (16 keys x 16 rows).
 template <int HD>
 __device__ __forceinline__ f32x4 score_block(const u32x4 (&kf)[HD / 32], const bf16x8 (&qf)[HD / 32]) {
@@ -146,14 +154,14 @@ __device__ __forceinline__ StepP softmax_step(const f32x4 (&s)[2], float& m, flo
   mx = lane_groups_max(mx) * scale_log2;  // scale > 0: the max of the scaled scores
   const bool raise = mx > m + kLazyMax;
   const float m_new = raise ? mx : m;
-  const float alpha = raise ? exp2f(m - mx) : 1.f;
+  const float alpha = raise ? fast_exp2(m - mx) : 1.f;
   float ps = 0.f;
   float pv[2][4];
 #pragma unroll
   for (int b = 0; b < 2; b++)
 #pragma unroll
     for (int i = 0; i < 4; i++) {
-      pv[b][i] = exp2f(fmaf(sv[b][i], scale_log2, -m_new));
+      pv[b][i] = fast_exp2(fmaf(sv[b][i], scale_log2, -m_new));
       ps += pv[b][i];
     }
   ps = lane_groups_sum(ps);

@@ -12,8 +12,10 @@
 //  - B is addressed through block, row and K-slice strides: row-major, or the
 //    packed weights' 16 x 32 tiles of 1 KB, where each DMA instruction reads
 //    one contiguous kilobyte;
-//  - fragment reads of the next k-step are issued before the MFMAs of the
-//    current one; one barrier per slice;
+//  - each k-step's MFMAs are issued one at a time, with the slice's DMA issues
+//    (first k-step) and the next slice's fragment reads (second k-step) spread
+//    between them, so that a wave keeps the matrix core fed while it issues
+//    its memory instructions; one barrier per slice;
 //  - LDS rows are 64 bytes (32 bf16 of K); the 16-byte chunk c of row r is
 //    stored at c ^ swz(r), which makes the fragment reads of 16 consecutive
 //    rows hit 16 distinct bank groups (the LDS serves a 16-byte read for 16
@@ -25,7 +27,10 @@
 //    64-wide K chunks [z C / S, (z + 1) C / S) of the C in K, so S need not
 //    divide C) and finishes in a deterministic reduce-and-epilogue kernel;
 //  - a cost model picks tile shape and K split per problem (a per-CU feed
-//    estimate for few rows, rounds of tile-units for more).
+//    estimate for few rows, rounds of tile-units for more), and may run the
+//    rows in two launches: the first in whole rounds of tiles, the rest as a
+//    GEMM of their own (split over K), so that a problem a little over a whole
+//    number of rounds does not pay for a mostly empty last round.
 #include <algorithm>
 #include <cmath>
 #include <map>
@@ -467,6 +472,10 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
         if (i * NM / L == idx) dma_one(i, kt + NS - 1);
       __builtin_amdgcn_sched_barrier(0);
     }
+    // (both fragment buffers stay live across each k-step, so that no read's
+    // destination is a register an MFMA of the k-step took as a source)
+    pin(fa[0]);
+    pin(fb[0]);
     // own DMA of stage kt + 1 landed, own reads of stage kt done; after the
     // barrier everyone's are, so stage kt + 1 is readable and slot kt % NS free
     vm_wait<VM_KEEP>();
@@ -485,6 +494,8 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
       }
       __builtin_amdgcn_sched_barrier(0);
     }
+    pin(fa[1]);
+    pin(fb[1]);
   };
 
 #pragma unroll
