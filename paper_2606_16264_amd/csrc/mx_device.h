@@ -24,8 +24,14 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
   return __builtin_bit_cast(uint16_t, (__bf16)f);
 }
 
+// Two floats to a pair of bf16 (lo in the low half), round-to-nearest-even
+// like f32_to_bf16: one v_cvt_pk_bf16_f32 (the conversion written per
+// element became two conversions, a shift and an or).
+typedef __bf16 mx_bf16x2 __attribute__((ext_vector_type(2)));
+typedef float mx_f32x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+  const mx_f32x2 f = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, mx_bf16x2));
 }
 
 // 16x16x32 bf16 matrix-core product, fp32 accumulate.
