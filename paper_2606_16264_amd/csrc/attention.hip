@@ -104,11 +104,15 @@ constexpr float kLazyMax = 8.0f;
 // own value and its partner's, in the same order in both lanes of a pair.  So
 // each step is one VALU swap and one VALU op, with no LDS permute, and the sum
 // is bit-identical in the four lanes of a row.
+// (The max as compare and select: fmaxf cannot tell that the swapped bits are
+// canonical and quiets both operands first, three instructions instead of two.
+// Scores are never NaN here: masked keys carry -1e30.)
+__device__ __forceinline__ float max_pair(float a, float b) { return a > b ? a : b; }
 __device__ __forceinline__ float lane_groups_max(float x) {
   const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  x = max_pair(__uint_as_float(a[0]), __uint_as_float(a[1]));
   const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+  return max_pair(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 __device__ __forceinline__ float lane_groups_sum(float x) {
   const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
