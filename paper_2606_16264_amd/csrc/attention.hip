@@ -79,15 +79,16 @@ __device__ __forceinline__ void load_chunk(Chunk<HD>& c, const AttnParams& p, in
   }
 }
 
-// One 32-key step of the online softmax for this lane's query row, in two
-// parts: the scores and the softmax update from the key fragments, then the
-// value product.  Lane group g4 owns keys pi0 * 16 + 8 * g4 + i' (i' = 4 b + i
-// for score block b, row i).
-struct StepP {
-  bf16x8 pb;     // P^T as the B operand: k index i' = 4 b + i <-> key j0 + i'
-  float alpha;   // rescale of the running output (1 where the max was kept)
-  bool rescale;  // some row of the wave raised its max (wave-uniform)
+// Online-softmax state of this lane's query row.  m is the running max of the
+// scaled scores (log2 units) that every probability of the row refers to, thr
+// the raw score above which m has to be raised (m + kLazyMax, unscaled), and
+// l this lane's share of the row's sum: the probabilities of the lane's own
+// keys only.  The four lanes of a row share m and every rescale, so the row's
+// sum is the sum of their shares, taken once at the end.
+struct RowState {
+  float m, thr, l;
 };
+__device__ __forceinline__ RowState row_start() { return RowState{kNegBig, kNegBig, 0.f}; }
 
 // A row's running max m (log2 units) is raised only when a score exceeds it by
 // more than this: the probabilities exp2(x - m) then stay below 2^8, which bf16
@@ -138,14 +139,13 @@ __device__ __forceinline__ f32x4 score_block(const u32x4 (&kf)[HD / 32], const b
   return s;
 }
 
-// Online-softmax update of this lane's row from its two score blocks (raw
-// scores; the softmax scale, in log2 units, is applied inside the exponent).
+// This lane's eight raw scores of the step (keys past the range or after the
+// row's position masked to kNegBig by select) and their max.
 template <bool MASK>
-__device__ __forceinline__ StepP softmax_step(const f32x4 (&s)[2], float& m, float& l, int pi0,
-                                              int page_end, int row_pos, float scale_log2, int g4) {
+__device__ __forceinline__ float masked_scores(const f32x4 (&s)[2], float (&sv)[2][4], int pi0,
+                                               int page_end, int row_pos, int g4) {
   const bool pvalid = (pi0 + (g4 >> 1)) < page_end;
   const int j0 = pi0 * 16 + 8 * g4;
-  float sv[2][4];
   float mx = kNegBig;
 #pragma unroll
   for (int b = 0; b < 2; b++)
@@ -155,28 +155,51 @@ __device__ __forceinline__ StepP softmax_step(const f32x4 (&s)[2], float& m, flo
       sv[b][i] = (!MASK || (pvalid && j <= row_pos)) ? s[b][i] : kNegBig;
       mx = fmaxf(mx, sv[b][i]);
     }
-  mx = lane_groups_max(mx) * scale_log2;  // scale > 0: the max of the scaled scores
-  const bool raise = mx > m + kLazyMax;
-  const float m_new = raise ? mx : m;
-  const float alpha = raise ? fast_exp2(m - mx) : 1.f;
-  float ps = 0.f;
+  return mx;
+}
+
+// Called by the whole wave when some lane holds a score above its row's
+// threshold: each row takes its max over its four lane groups and raises m to
+// it if that exceeds m by more than kLazyMax, rescaling its output and sum.
+// The first step of every row comes here (thr starts at kNegBig and every row
+// has a key in its first step).
+template <int NO>
+__device__ __forceinline__ void raise_max(RowState& r, float mx, float scale_log2, float inv_scale,
+                                          f32x4 (&o)[NO]) {
+  const float rmx = lane_groups_max(mx) * scale_log2;  // scale > 0: the max of the scaled scores
+  const bool raise = rmx > r.m + kLazyMax;
+  const float m_new = raise ? rmx : r.m;
+  const float alpha = raise ? fast_exp2(r.m - m_new) : 1.f;
+#pragma unroll
+  for (int e = 0; e < NO; e++) o[e] = o[e] * alpha;
+  r.l *= alpha;
+  r.m = m_new;
+  r.thr = (m_new + kLazyMax) * inv_scale;
+}
+
+// The step's probabilities of this lane's keys, exp2(score * scale - m), as
+// the value product's B operand (k index i' = 4 b + i <-> key j0 + i'), and
+// their sum into the lane's share of the row's sum: two at a time with the
+// bf16 dot instruction, from the same rounded values the value product uses.
+__device__ __forceinline__ bf16x8 probs(const float (&sv)[2][4], RowState& r, float scale_log2) {
   float pv[2][4];
 #pragma unroll
   for (int b = 0; b < 2; b++)
 #pragma unroll
-    for (int i = 0; i < 4; i++) {
-      pv[b][i] = fast_exp2(fmaf(sv[b][i], scale_log2, -m_new));
-      ps += pv[b][i];
-    }
-  ps = lane_groups_sum(ps);
-  l = l * alpha + ps;
-  m = m_new;
-  u32x4 pb_bits;
-  pb_bits[0] = pack_bf16x2(pv[0][0], pv[0][1]);
-  pb_bits[1] = pack_bf16x2(pv[0][2], pv[0][3]);
-  pb_bits[2] = pack_bf16x2(pv[1][0], pv[1][1]);
-  pb_bits[3] = pack_bf16x2(pv[1][2], pv[1][3]);
-  return StepP{as_bf16x8(pb_bits), alpha, __any(raise) != 0};
+    for (int i = 0; i < 4; i++) pv[b][i] = fast_exp2(fmaf(sv[b][i], scale_log2, -r.m));
+  // Four separate words, put together only for the return: with the words
+  // taken out of a four-word vector, this compiler's dot instructions all
+  // read its first word.
+  const uint32_t w0 = pack_bf16x2(pv[0][0], pv[0][1]);
+  const uint32_t w1 = pack_bf16x2(pv[0][2], pv[0][3]);
+  const uint32_t w2 = pack_bf16x2(pv[1][0], pv[1][1]);
+  const uint32_t w3 = pack_bf16x2(pv[1][2], pv[1][3]);
+  const mx_bf16x2 ones = __builtin_bit_cast(mx_bf16x2, 0x3F803F80u);
+  r.l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(mx_bf16x2, w0), ones, r.l, false);
+  r.l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(mx_bf16x2, w1), ones, r.l, false);
+  r.l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(mx_bf16x2, w2), ones, r.l, false);
+  r.l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(mx_bf16x2, w3), ones, r.l, false);
+  return as_bf16x8(u32x4{w0, w1, w2, w3});
 }
 
 // Which of this lane group's eight keys hold values (bf16 lanes of each
@@ -195,15 +218,11 @@ __device__ __forceinline__ void value_keep(int pi0, int page_end, int kv_len, in
   }
 }
 
-// O^T = alpha O^T + V^T P^T over the output blocks DB0 .. DB0 + NDB - 1 (16
-// head dims each), V^T as the A operand.
+// O^T += V^T P^T over the output blocks DB0 .. DB0 + NDB - 1 (16 head dims
+// each), V^T as the A operand.
 template <int HD, int DB0, int NDB, bool MASK>
-__device__ __forceinline__ void values_part(const u32x4 (&vf)[NDB], f32x4 (&o)[HD / 16], StepP sp,
+__device__ __forceinline__ void values_part(const u32x4 (&vf)[NDB], f32x4 (&o)[HD / 16], bf16x8 pb,
                                             const uint32_t (&keep)[4]) {
-  if (sp.rescale) {
-#pragma unroll
-    for (int e = 0; e < NDB; e++) o[DB0 + e] = o[DB0 + e] * sp.alpha;
-  }
 #pragma unroll
   for (int e = 0; e < NDB; e++) {
     u32x4 va = vf[e];
@@ -211,7 +230,7 @@ __device__ __forceinline__ void values_part(const u32x4 (&vf)[NDB], f32x4 (&o)[H
 #pragma unroll
       for (int h = 0; h < 4; h++) va[h] &= keep[h];
     }
-    o[DB0 + e] = mfma16(as_bf16x8(va), sp.pb, o[DB0 + e]);
+    o[DB0 + e] = mfma16(as_bf16x8(va), pb, o[DB0 + e]);
   }
 }
 
@@ -219,14 +238,17 @@ __device__ __forceinline__ void values_part(const u32x4 (&vf)[NDB], f32x4 (&o)[H
 // g4 owns keys pi0 * 16 + 8 * g4 + i' (i' = 4 b + i for score block b, row i).
 template <int HD, bool MASK = true>
 __device__ __forceinline__ void process_chunk(const Chunk<HD>& c, const bf16x8 (&qf)[HD / 32],
-                                              f32x4 (&o)[HD / 16], float& m, float& l,
-                                              int pi0, int page_end, int row_pos, int kv_len,
-                                              float scale_log2, int g4) {
+                                              f32x4 (&o)[HD / 16], RowState& r, int pi0,
+                                              int page_end, int row_pos, int kv_len,
+                                              float scale_log2, float inv_scale, int g4) {
   const f32x4 s[2] = {score_block<HD>(c.k[0], qf), score_block<HD>(c.k[1], qf)};
-  const StepP sp = softmax_step<MASK>(s, m, l, pi0, page_end, row_pos, scale_log2, g4);
+  float sv[2][4];
+  const float mx = masked_scores<MASK>(s, sv, pi0, page_end, row_pos, g4);
+  if (__any(mx > r.thr)) raise_max(r, mx, scale_log2, inv_scale, o);
+  const bf16x8 pb = probs(sv, r, scale_log2);
   uint32_t keep[4];
   value_keep(pi0, page_end, kv_len, g4, keep);
-  values_part<HD, 0, HD / 16, MASK>(c.v, o, sp, keep);
+  values_part<HD, 0, HD / 16, MASK>(c.v, o, pb, keep);
 }
 
 // Keys pi0 * 16 .. pi0 * 16 + 31 all count for every row of the wave (both
@@ -282,7 +304,8 @@ __device__ __forceinline__ void prefill_item(const AttnParams& p, const AttnItem
   const int last_row = min(row0 + 31, rq.n_new - 1);
   const int page_end = row0 < rq.n_new ? (rq.ctx_len + last_row) / 16 + 1 : 0;
 
-  float m = kNegBig, l = 0.f, m2 = kNegBig, l2 = 0.f;
+  RowState r1 = row_start(), r2 = row_start();
+  const float inv_scale = 1.f / p.scale_log2;
   f32x4 o[HD / 16], o2[HD / 16];
 #pragma unroll
   for (int db = 0; db < HD / 16; db++) o[db] = o2[db] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -380,21 +403,28 @@ __device__ __forceinline__ void prefill_item(const AttnParams& p, const AttnItem
           s1[b] = score_block<HD>(kf, qf);
           s2[b] = score_block<HD>(kf, qf2);
         }
-        const StepP sp1 = softmax_step<MASK>(s1, m, l, pi0, page_end, row_pos, p.scale_log2, g4);
-        const StepP sp2 = softmax_step<MASK>(s2, m2, l2, pi0, page_end, row_pos2, p.scale_log2, g4);
+        float sv1[2][4], sv2[2][4];
+        const float mx1 = masked_scores<MASK>(s1, sv1, pi0, page_end, row_pos, g4);
+        const float mx2 = masked_scores<MASK>(s2, sv2, pi0, page_end, row_pos2, g4);
+        if (__any(mx1 > r1.thr || mx2 > r2.thr)) {
+          raise_max(r1, mx1, p.scale_log2, inv_scale, o);
+          raise_max(r2, mx2, p.scale_log2, inv_scale, o2);
+        }
+        const bf16x8 pb1 = probs(sv1, r1, p.scale_log2);
+        const bf16x8 pb2 = probs(sv2, r2, p.scale_log2);
         uint32_t keep[4];
         value_keep(pi0, page_end, rq.kv_len, g4, keep);
         {
           u32x4 vf[HD / 32];
           vread(slot, 0, vf);
-          values_part<HD, 0, HD / 32, MASK>(vf, o, sp1, keep);
-          values_part<HD, 0, HD / 32, MASK>(vf, o2, sp2, keep);
+          values_part<HD, 0, HD / 32, MASK>(vf, o, pb1, keep);
+          values_part<HD, 0, HD / 32, MASK>(vf, o2, pb2, keep);
         }
         {
           u32x4 vf[HD / 32];
           vread(slot, HD / 32, vf);
-          values_part<HD, HD / 32, HD / 32, MASK>(vf, o, sp1, keep);
-          values_part<HD, HD / 32, HD / 32, MASK>(vf, o2, sp2, keep);
+          values_part<HD, HD / 32, HD / 32, MASK>(vf, o, pb1, keep);
+          values_part<HD, HD / 32, HD / 32, MASK>(vf, o2, pb2, keep);
         }
       };
       if (chunk_interior(pi0, page_end, wave_first_pos))
@@ -426,8 +456,10 @@ __device__ __forceinline__ void prefill_item(const AttnParams& p, const AttnItem
     if (kt + 1 >= n_chunks) break;
     step(kt + 1, stb, sta);
   }
+  // the rows' sums over their four lane groups (every lane takes part)
+  const float l1 = lane_groups_sum(r1.l), l2 = lane_groups_sum(r2.l);
   if (row_valid) {
-    const float inv = 1.f / l;
+    const float inv = 1.f / l1;
     uint16_t* op = p.out + qtok * p.out_tok_stride + (int64_t)qhead * HD + 4 * g4;
 #pragma unroll
     for (int db = 0; db < HD / 16; db++) {
@@ -469,7 +501,8 @@ __device__ __forceinline__ void decode_item(const AttnParams& p, const AttnItem&
   const int chunk_first = it.start + 2 * wave;
   constexpr int chunk_step = 8;
 
-  float m = kNegBig, l = 0.f;
+  RowState r = row_start();
+  const float inv_scale = 1.f / p.scale_log2;
   f32x4 o[HD / 16];
 #pragma unroll
   for (int db = 0; db < HD / 16; db++) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -497,9 +530,11 @@ __device__ __forceinline__ void decode_item(const AttnParams& p, const AttnItem&
   };
   auto proc = [&](const Chunk<HD>& c, int pi0) {
     if (chunk_interior(pi0, page_end, row_pos))
-      process_chunk<HD, false>(c, qf, o, m, l, pi0, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
+      process_chunk<HD, false>(c, qf, o, r, pi0, page_end, row_pos, rq.kv_len, p.scale_log2,
+                               inv_scale, g4);
     else
-      process_chunk<HD>(c, qf, o, m, l, pi0, page_end, row_pos, rq.kv_len, p.scale_log2, g4);
+      process_chunk<HD>(c, qf, o, r, pi0, page_end, row_pos, rq.kv_len, p.scale_log2, inv_scale,
+                        g4);
   };
   Chunk<HD> ca, cb;
   int pi = chunk_first;
@@ -541,8 +576,9 @@ __device__ __forceinline__ void decode_item(const AttnParams& p, const AttnItem&
   for (int db = 0; db < HD / 16; db++)
 #pragma unroll
     for (int i = 0; i < 4; i++) s_o[wave][col][db * 16 + 4 * g4 + i] = o[db][i];
+  const float l = lane_groups_sum(r.l);
   if (g4 == 0) {
-    s_m[wave][col] = m;
+    s_m[wave][col] = r.m;
     s_l[wave][col] = l;
   }
   __syncthreads();
