@@ -258,13 +258,17 @@ __device__ __forceinline__ bool chunk_interior(int pi0, int page_end, int first_
   return pi0 + 1 < page_end && pi0 * 16 + 31 <= first_row_pos;
 }
 
-// Prefill tiles share every 32-key chunk through LDS: the four waves load it
-// once, a quarter each (waves 0 and 1 the keys of the chunk's two pages, waves
-// 2 and 3 their values), and every wave reads its matrix-core fragments from
-// there.  Keys are stored [32][HD] with the 16-byte chunk c of key row j at
-// c ^ ksw(j); values [HD][32 keys] with the 16-byte chunk c of dim row d at
+// Prefill tiles share every 32-key chunk through LDS.  The four waves copy it
+// there with the DMA path (global_load_lds, 16 bytes per lane), a quarter each
+// (waves 0 and 1 the keys of the chunk's two pages, waves 2 and 3 their
+// values), and every wave reads its matrix-core fragments from there.  Keys
+// are stored [32][HD] with the 16-byte chunk c of key row j at c ^ ksw(j);
+// values [HD][32 keys] with the 16-byte chunk c of dim row d at
 // c ^ ((d >> 2) & 3).  Both make the fragment reads (16 key rows, or 16 dim
-// rows, at one logical chunk) and the stores hit distinct bank groups.
+// rows, at one logical chunk) hit distinct bank groups.  A DMA instruction
+// writes 1 KB of LDS in lane order, so each lane fetches the 16 bytes that
+// belong at its position: a permutation within the page's rows, which keeps
+// every copy a run of whole 64-byte (or longer) segments.
 template <int HD>
 __device__ __forceinline__ int ksw(int key) {
   if constexpr (HD == 128) return (key & 3) | ((key >> 3) << 2);
@@ -274,22 +278,51 @@ template <int HD>
 struct SharedChunk {
   static constexpr int KBYTES = 32 * HD * 2;
   static constexpr int BYTES = 2 * KBYTES;  // keys + values
+  static constexpr int SLOTS = 4;           // chunks kt .. kt + 3: copies run three ahead
+  static constexpr int NLD = BYTES / 4096;  // 1 KB copies per wave per chunk
 };
 template <int HD>
 constexpr int smem_bytes() {
-  constexpr int ring = 2 * SharedChunk<HD>::BYTES;
+  constexpr int ring = SharedChunk<HD>::SLOTS * SharedChunk<HD>::BYTES;
   constexpr int combine = (4 * 16 * (HD + 4) + 2 * 4 * 16) * 4;
   return ring > combine ? ring : combine;
 }
 
+// v[e] = the 16 bytes at LDS address addr + OFF0 + e * STEP, e = E .. N - 1.
+template <int E, int N, int OFF0, int STEP>
+__device__ __forceinline__ void lds_read_run(unsigned addr, u32x4 (&v)[N]) {
+  if constexpr (E < N) {
+    v[E] = lds_read16_at<OFF0 + E * STEP>(addr);
+    lds_read_run<E + 1, N, OFF0, STEP>(addr, v);
+  }
+}
+
 // Prefill item: one q head, rows it.start .. it.start + 127 of the chunk; wave
 // w owns two blocks of 16 consecutive rows, it.start + 32 w + (0 | 16) + col.
+//
+// Iteration kt of the chunk loop reads the keys of chunk kt + 1 for the score
+// products while the exponentials of chunk kt (whose scores the previous
+// iteration left) run on the vector units, then takes the value products of
+// chunk kt, and raises the rows' running max for chunk kt + 1 where needed:
+// the scores of the next chunk and the softmax of the current one are
+// independent, so they share a basic block and the matrix cores have work
+// while the exponentials run.  The copies of chunk kt + 3 go out at the top of
+// iteration kt into the slot chunk kt - 1 used, after the barrier that ends
+// every wave's reads of it; page ids are loaded one iteration before their
+// copies.  Every iteration issues the same copies (chunks past the tile's last
+// one copy the request's first page into the free slot and are never read),
+// and they are the only vector-memory operations of the loop (page ids are
+// scalar loads), so one vmcnt value fits every wait: at the top of iteration
+// kt the copies of iteration kt - 1 may still be in flight, every earlier one
+// (chunk kt + 1) has landed.
 static_assert(kPrefillTileRows == 4 * 32, "four waves of two 16-row blocks");
 template <int HD>
 __device__ __forceinline__ void prefill_item(const AttnParams& p, const AttnItem& it,
                                              const ReqDev& rq, char* smem) {
+  using SC = SharedChunk<HD>;
+  constexpr int KB = SC::KBYTES, CB = SC::BYTES, NLD = SC::NLD, ND = HD / 32;
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int col = lane & 15;  // query row of this lane within each block
   const int g4 = lane >> 4;   // lane group
   const int qhead = it.head;
@@ -304,158 +337,212 @@ __device__ __forceinline__ void prefill_item(const AttnParams& p, const AttnItem
   const int last_row = min(row0 + 31, rq.n_new - 1);
   const int page_end = row0 < rq.n_new ? (rq.ctx_len + last_row) / 16 + 1 : 0;
 
-  RowState r1 = row_start(), r2 = row_start();
-  const float inv_scale = 1.f / p.scale_log2;
-  f32x4 o[HD / 16], o2[HD / 16];
-#pragma unroll
-  for (int db = 0; db < HD / 16; db++) o[db] = o2[db] = f32x4{0.f, 0.f, 0.f, 0.f};
-  bf16x8 qf[HD / 32], qf2[HD / 32];
+  bf16x8 qf[ND], qf2[ND];
   {
     const uint16_t* qp = p.q + qtok * p.q_tok_stride + (int64_t)qhead * HD + 8 * g4;
     const uint16_t* qp2 = p.q + qtok2 * p.q_tok_stride + (int64_t)qhead * HD + 8 * g4;
 #pragma unroll
-    for (int ds = 0; ds < HD / 32; ds++) {
+    for (int ds = 0; ds < ND; ds++) {
       u32x4 v = row_valid ? *reinterpret_cast<const u32x4*>(qp + ds * 32) : u32x4{0, 0, 0, 0};
       u32x4 v2 = row_valid2 ? *reinterpret_cast<const u32x4*>(qp2 + ds * 32) : u32x4{0, 0, 0, 0};
       qf[ds] = as_bf16x8(v);
       qf2[ds] = as_bf16x8(v2);
     }
   }
+  RowState r1 = row_start(), r2 = row_start();
+  const float inv_scale = 1.f / p.scale_log2;
+  f32x4 o[HD / 16], o2[HD / 16];
+#pragma unroll
+  for (int db = 0; db < HD / 16; db++) o[db] = o2[db] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // the tile's last row bounds the pages every wave helps to load
+  // the tile's last row bounds the pages every wave helps to copy
   const int tile_last = min(it.start + kPrefillTileRows - 1, rq.n_new - 1);
   const int item_pages = (rq.ctx_len + tile_last) / 16 + 1;
   const int n_chunks = (item_pages + 1) / 2;
   const int wave_chunks = (page_end + 1) / 2;  // 0 for a wave without valid rows
   const int wave_first_pos = rq.ctx_len + it.start + 32 * wave;  // the wave's first row
-  const int safe = p.pages[rq.page_start];
-  auto pid = [&](int pi) -> int {
-    const int v = p.pages[rq.page_start + min(pi, rq.n_pages - 1)];
-    return pi < item_pages ? v : -1;
-  };
-  constexpr int KB = SharedChunk<HD>::KBYTES, CB = SharedChunk<HD>::BYTES;
-  constexpr int NLD = HD / 32;  // 16-byte loads per lane for a quarter chunk
-  // waves 0 / 1: keys of the chunk's first / second page; 2 / 3: values
-  auto gload = [&](u32x4 (&st)[NLD], int pid0, int pid1) {
-    const int pg0 = (wave & 1) ? pid1 : pid0;
-    const int pg = pg0 >= 0 ? pg0 : safe;  // past the end: masked, like the decode path
-    const uint16_t* base = (wave < 2 ? p.k_pool : p.v_pool) + ((int64_t)pg * p.nkv + kvh) * (16 * HD);
+  // page ids through the constant address space: uniform reads of a table
+  // nothing writes during the launch, so they are scalar loads, whose
+  // results the compiler waits for with lgkmcnt when it uses them (vector
+  // loads would put the compiler's own vmcnt waits among the copies)
+  const __attribute__((address_space(4))) int32_t* ptab =
+      (const __attribute__((address_space(4))) int32_t*)(p.pages + rq.page_start);
+  const int last_page = rq.n_pages - 1;
+  const int safe = ptab[0];
+
+  // This lane's share of the wave's 1 KB copies: copy i fills LDS kilobyte
+  // kb = NLD * wave + i of the slot (keys first, then values) with the 16 bytes
+  // at element offset off[i] of the chunk's first (sel[i] false) or second page.
+  int off[NLD];
+  bool sel[NLD];
 #pragma unroll
-    for (int i = 0; i < NLD; i++) st[i] = *reinterpret_cast<const u32x4*>(base + (i * 64 + lane) * 8);
-  };
-  auto swrite = [&](char* slot, const u32x4 (&st)[NLD]) {
-#pragma unroll
-    for (int i = 0; i < NLD; i++) {
-      const int c = i * 64 + lane;
-      char* dst;
-      if (wave < 2) {
-        const int key = 16 * (wave & 1) + c / (HD / 8), lc = c % (HD / 8);
-        dst = slot + key * (HD * 2) + ((lc ^ ksw<HD>(key)) << 4);
-      } else {
-        const int d = c >> 1, lc = 2 * (wave & 1) + (c & 1);
-        dst = slot + KB + d * 64 + ((lc ^ ((d >> 2) & 3)) << 4);
-      }
-      *reinterpret_cast<u32x4*>(dst) = st[i];
+  for (int i = 0; i < NLD; i++) {
+    const int kb = NLD * wave + i;
+    if (wave < 2) {
+      constexpr int lanes_per_row = HD / 8;  // 16-byte pieces of a key row
+      const int j = kb * (64 / lanes_per_row) + lane / lanes_per_row;
+      const int lc = (lane % lanes_per_row) ^ ksw<HD>(j);
+      sel[i] = j >= 16;
+      off[i] = (j & 15) * HD + lc * 8;
+    } else {
+      const int d = (kb - KB / 1024) * 16 + (lane >> 2);
+      const int c = (lane & 3) ^ ((d >> 2) & 3);  // logical 8-key piece: page c / 2
+      sel[i] = c >= 2;
+      off[i] = d * 16 + (c & 1) * 8;
     }
-  };
-  // fragments of score block b (keys), or of output blocks DB0 .. (values)
-  auto kread = [&](const char* slot, int b, u32x4 (&kf)[HD / 32]) {
+  }
+  const uint16_t* pool = wave < 2 ? p.k_pool : p.v_pool;
+  const unsigned lds0 = (unsigned)(size_t)(MX_LDS char*)smem;
+  auto copy = [&](int c, int ra, int rb) {  // ra, rb: page ids of pages 2c, 2c + 1
+    const int pa = 2 * c < item_pages ? ra : safe;
+    const int pb = 2 * c + 1 < item_pages ? rb : safe;
+    const uint16_t* ba = pool + ((int64_t)pa * p.nkv + kvh) * (16 * HD);
+    const uint16_t* bb = pool + ((int64_t)pb * p.nkv + kvh) * (16 * HD);
+    const unsigned dst = lds0 + (unsigned)((c & 3) * CB + NLD * wave * 1024);
 #pragma unroll
-    for (int ds = 0; ds < HD / 32; ds++) {
-      const int key = 16 * (col >> 3) + 8 * ((col >> 2) & 1) + (col & 3) + 4 * b;
-      kf[ds] = *reinterpret_cast<const u32x4*>(slot + key * (HD * 2) +
-                                               (((4 * ds + g4) ^ ksw<HD>(key)) << 4));
-    }
+    for (int i = 0; i < NLD; i++) dma16((sel[i] ? bb : ba) + off[i], dst + i * 1024);
   };
-  auto vread = [&](const char* slot, int db0, u32x4 (&vf)[HD / 32]) {
+  auto page_of = [&](int pi) { return ptab[min(pi, last_page)]; };
+
+  // fragment addresses within a slot: key rows kappa_0(col) (score block 1 is
+  // four key rows further, same swizzle), value dim rows 16 e + col
+  const int key0 = 16 * (col >> 3) + 8 * ((col >> 2) & 1) + (col & 3);
+  unsigned kaddr[ND];
 #pragma unroll
-    for (int e = 0; e < HD / 32; e++) {
-      const int d = 16 * (db0 + e) + col;
-      vf[e] = *reinterpret_cast<const u32x4*>(slot + KB + d * 64 + ((g4 ^ ((d >> 2) & 3)) << 4));
-    }
-  };
-  // Two register stagings used in turn: the loads of chunk kt + 2 are issued
-  // while chunk kt is processed, and chunk kt + 1 (loaded during the previous
-  // step) is then stored into the other LDS slot, which everyone finished
-  // reading before the previous step's barrier; one barrier per chunk.  Page
-  // ids are read one step ahead of their loads and issued before the step's
-  // chunk loads: one counter tracks both, in order, so a wait for a page id
-  // never waits for a chunk in flight.  Chunks past the tile's last one read
-  // the request's first page and are never processed, so every step issues
-  // the same loads.
-  u32x4 sta[NLD], stb[NLD];
-  int f0 = pid(4), f1 = pid(5);  // pages of the chunk the next step loads
-  auto process = [&](int kt) {
-    if (kt < wave_chunks) {
-      // both row blocks from one read of the chunk's fragments, half a
-      // chunk's keys (or values) at a time, each half applied to both
-      // blocks before the next is read.  The wave's first row bounds both
-      // blocks: the second block's rows come later.
-      const char* slot = smem + (kt & 1) * CB;
-      const int pi0 = 2 * kt;
-      auto both = [&](auto mask) {
-        constexpr bool MASK = decltype(mask)::value;
-        f32x4 s1[2], s2[2];
+  for (int ds = 0; ds < ND; ds++)
+    kaddr[ds] = (unsigned)(key0 * (HD * 2) + (((4 * ds + g4) ^ ksw<HD>(key0)) << 4));
+  const unsigned vaddr = (unsigned)(KB + col * 64 + ((g4 ^ ((col >> 2) & 3)) << 4));
+
+  // scores of chunk c from its keys in LDS: this lane's masked raw scores, their
+  // max, and whether some lane of the wave is above its row's threshold
+  float sv1[2][4], sv2[2][4], mx1 = kNegBig, mx2 = kNegBig;
+  auto scores = [&](auto mask, int c) -> bool {
+    constexpr bool MASK = decltype(mask)::value;
+    const unsigned sb = lds0 + (unsigned)((c & 3) * CB);
+    u32x4 k0[ND], k1[ND];
 #pragma unroll
-        for (int b = 0; b < 2; b++) {
-          u32x4 kf[HD / 32];
-          kread(slot, b, kf);
-          s1[b] = score_block<HD>(kf, qf);
-          s2[b] = score_block<HD>(kf, qf2);
-        }
-        float sv1[2][4], sv2[2][4];
-        const float mx1 = masked_scores<MASK>(s1, sv1, pi0, page_end, row_pos, g4);
-        const float mx2 = masked_scores<MASK>(s2, sv2, pi0, page_end, row_pos2, g4);
-        if (__any(mx1 > r1.thr || mx2 > r2.thr)) {
-          raise_max(r1, mx1, p.scale_log2, inv_scale, o);
-          raise_max(r2, mx2, p.scale_log2, inv_scale, o2);
-        }
-        const bf16x8 pb1 = probs(sv1, r1, p.scale_log2);
-        const bf16x8 pb2 = probs(sv2, r2, p.scale_log2);
-        uint32_t keep[4];
-        value_keep(pi0, page_end, rq.kv_len, g4, keep);
-        {
-          u32x4 vf[HD / 32];
-          vread(slot, 0, vf);
-          values_part<HD, 0, HD / 32, MASK>(vf, o, pb1, keep);
-          values_part<HD, 0, HD / 32, MASK>(vf, o2, pb2, keep);
-        }
-        {
-          u32x4 vf[HD / 32];
-          vread(slot, HD / 32, vf);
-          values_part<HD, HD / 32, HD / 32, MASK>(vf, o, pb1, keep);
-          values_part<HD, HD / 32, HD / 32, MASK>(vf, o2, pb2, keep);
-        }
-      };
-      if (chunk_interior(pi0, page_end, wave_first_pos))
-        both(std::integral_constant<bool, false>{});
-      else
-        both(std::integral_constant<bool, true>{});
-    }
+    for (int ds = 0; ds < ND; ds++) k0[ds] = lds_read16(sb + kaddr[ds]);
+#pragma unroll
+    for (int ds = 0; ds < ND; ds++) k1[ds] = lds_read16_at<4 * HD * 2>(sb + kaddr[ds]);
+    f32x4 s1[2], s2[2];
+    lgkm_wait<ND>();
+    pin(k0);
+    s1[0] = score_block<HD>(k0, qf);
+    s2[0] = score_block<HD>(k0, qf2);
+    __builtin_amdgcn_sched_barrier(0);  // these products go before the second wait
+    lgkm_wait<0>();
+    pin(k1);
+    s1[1] = score_block<HD>(k1, qf);
+    s2[1] = score_block<HD>(k1, qf2);
+    mx1 = masked_scores<MASK>(s1, sv1, 2 * c, page_end, row_pos, g4);
+    mx2 = masked_scores<MASK>(s2, sv2, 2 * c, page_end, row_pos2, g4);
+    return __any(mx1 > r1.thr || mx2 > r2.thr) != 0;
   };
-  auto step = [&](int kt, u32x4 (&fill)[NLD], const u32x4 (&store)[NLD]) {
-    const int g0 = pid(2 * kt + 6), g1 = pid(2 * kt + 7);  // for the next step
-    __builtin_amdgcn_sched_barrier(0);
-    gload(fill, f0, f1);  // chunk kt + 2
-    __builtin_amdgcn_sched_barrier(0);
-    f0 = g0;
-    f1 = g1;
-    process(kt);
-    swrite(smem + ((kt + 1) & 1) * CB, store);  // chunk kt + 1
-    __syncthreads();
+  // value products of chunk c (values past the request's keys zeroed when
+  // MASK: only the chunk that holds the request's last key has such values)
+  auto values = [&](auto mask, int c, bf16x8 pb1, bf16x8 pb2) {
+    constexpr bool MASK = decltype(mask)::value;
+    const unsigned va = lds0 + (unsigned)((c & 3) * CB) + vaddr;
+    u32x4 v0[ND], v1[ND];
+    lds_read_run<0, ND, 0, 1024>(va, v0);
+    lds_read_run<0, ND, ND * 1024, 1024>(va, v1);
+    uint32_t keep[4] = {~0u, ~0u, ~0u, ~0u};
+    if constexpr (MASK) value_keep(2 * c, page_end, rq.kv_len, g4, keep);
+    lgkm_wait<ND>();
+    pin(v0);
+    values_part<HD, 0, ND, MASK>(v0, o, pb1, keep);
+    values_part<HD, 0, ND, MASK>(v0, o2, pb2, keep);
+    __builtin_amdgcn_sched_barrier(0);  // these products go before the second wait
+    lgkm_wait<0>();
+    pin(v1);
+    values_part<HD, ND, ND, MASK>(v1, o, pb1, keep);
+    values_part<HD, ND, ND, MASK>(v1, o2, pb2, keep);
   };
+  auto raise_rows = [&]() {
+    raise_max(r1, mx1, p.scale_log2, inv_scale, o);
+    raise_max(r2, mx2, p.scale_log2, inv_scale, o2);
+  };
+  using Masked = std::integral_constant<bool, true>;
+  using Unmasked = std::integral_constant<bool, false>;
+
+  // prologue: page ids of chunks 0 .. 3, the copies of chunks 0 .. 2
+  int ua, ub, fa = 0, fb = 0;  // page ids of the chunk the next copy is for, and the one after
   {
-    const int a0 = pid(0), a1 = pid(1), b0 = pid(2), b1 = pid(3);
-    gload(sta, a0, a1);
-    gload(stb, b0, b1);
+    const int a0 = page_of(0), b0 = page_of(1), a1 = page_of(2), b1 = page_of(3);
+    const int a2 = page_of(4), b2 = page_of(5);
+    copy(0, a0, b0);
+    copy(1, a1, b1);
+    ua = page_of(6);
+    ub = page_of(7);
+    copy(2, a2, b2);
   }
-  swrite(smem, sta);
-  __syncthreads();
-  for (int kt = 0; kt < n_chunks; kt += 2) {
-    step(kt, sta, stb);
-    if (kt + 1 >= n_chunks) break;
-    step(kt + 1, stb, sta);
+  // top of iteration kt: this wave's copies of chunk kt + 1 have landed, then
+  // everyone's, and every read of chunk kt - 1 is done; chunk kt + 3 goes out
+  auto top = [&](int kt, int& use_a, int& use_b, int& fill_a, int& fill_b) {
+    vm_wait<NLD>();
+    wg_barrier();
+    fill_a = page_of(2 * (kt + 4));
+    fill_b = page_of(2 * (kt + 4) + 1);
+    copy(kt + 3, use_a, use_b);
+  };
+  auto run = [&](int kt0, int kt1, auto body) {  // iterations kt0 .. kt1 - 1
+    for (int kt = kt0; kt < kt1; kt += 2) {
+      top(kt, ua, ub, fa, fb);
+      body(kt);
+      if (kt + 1 >= kt1) {  // an odd count: the next iteration uses fa, fb
+        const int ta = ua, tb = ub;
+        ua = fa;
+        ub = fb;
+        fa = ta;
+        fb = tb;
+        break;
+      }
+      top(kt + 1, fa, fb, ua, ub);
+      body(kt + 1);
+    }
+  };
+
+  if (row0 >= rq.n_new) {
+    // no rows here: this wave only copies its quarter of every chunk
+    vm_wait<2 * NLD>();
+    wg_barrier();
+    run(0, n_chunks, [](int) {});
+    vm_wait<0>();  // no copy may land in LDS after the workgroup has ended
+    return;
   }
+
+  vm_wait<2 * NLD>();  // chunk 0 has landed; chunks 1 and 2 may be in flight
+  wg_barrier();
+  if (scores(Masked{}, 0)) raise_rows();  // the first step raises every row's max
+
+  // Chunks 0 .. n_int - 1 are inside every wave's range and at or before
+  // every row of the tile: no masks.  The last chunk of the tile is the only
+  // one that can hold keys past the request's end, so n_main <= n_chunks - 1.
+  const int first_pos = rq.ctx_len + it.start;
+  const int page_end0 = (rq.ctx_len + min(it.start + 31, rq.n_new - 1)) / 16 + 1;  // wave 0's
+  const int n_int = first_pos >= 31 ? min((first_pos - 31) / 32 + 1, page_end0 / 2) : 0;
+  const int n_main = max(0, n_int - 1);
+  // main loop: the scores of chunk kt + 1 and the softmax of chunk kt in one
+  // basic block, then the values of chunk kt; no masks, no per-wave bounds
+  run(0, n_main, [&](int kt) {
+    const bf16x8 pb1 = probs(sv1, r1, p.scale_log2);
+    const bf16x8 pb2 = probs(sv2, r2, p.scale_log2);
+    const bool raise = scores(Unmasked{}, kt + 1);
+    values(Unmasked{}, kt, pb1, pb2);
+    if (raise) raise_rows();
+  });
+  // the chunks around the diagonal and the tile's end, with masks and bounds
+  run(n_main, n_chunks, [&](int kt) {
+    const bool sc = kt + 1 < wave_chunks;  // scores of chunk kt + 1
+    if (kt < wave_chunks) {
+      const bf16x8 pb1 = probs(sv1, r1, p.scale_log2);
+      const bf16x8 pb2 = probs(sv2, r2, p.scale_log2);
+      values(Masked{}, kt, pb1, pb2);
+    }
+    if (sc && scores(Masked{}, kt + 1)) raise_rows();
+  });
+  vm_wait<0>();  // no copy may land in LDS after the workgroup has ended
+
   // the rows' sums over their four lane groups (every lane takes part)
   const float l1 = lane_groups_sum(r1.l), l2 = lane_groups_sum(r2.l);
   if (row_valid) {

@@ -48,37 +48,9 @@ constexpr int BK = 64;    // K granularity of a split (and of the problem)
 constexpr int BKS = 32;   // K per LDS stage
 constexpr int kGroupM = 8;
 
-// LDS ring discipline.  The K slices are copied global -> LDS by the DMA path
-// (global_load_lds, 16 bytes per lane), which the hardware tracks with vmcnt
-// only, and the MFMA fragments are read with ds_read_b128 issued from inline
-// assembly, so that every wait is placed here by hand rather than inferred
-// (the compiler would otherwise wait for all DMA in flight before any LDS
-// read).  pin() ties fragment registers to the preceding wait so that no
-// consumer is scheduled above it.
-template <int N>
-__device__ __forceinline__ void lgkm_wait() {
-  static_assert(N >= 0 && N <= 15, "lgkmcnt range");
-  asm volatile("s_waitcnt lgkmcnt(%0)" ::"i"(N) : "memory");
-}
-template <int N>
-__device__ __forceinline__ void vm_wait() {
-  static_assert(N >= 0 && N <= 63, "vmcnt range");
-  asm volatile("s_waitcnt vmcnt(%0)" ::"i"(N) : "memory");
-}
-__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
-template <int K>
-__device__ __forceinline__ void pin(u32x4 (&f)[K]) {
-#pragma unroll
-  for (int i = 0; i < K; i++) asm volatile("" : "+v"(f[i]));
-}
-__device__ __forceinline__ u32x4 lds_read16(unsigned addr) {
-  u32x4 v;
-  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr));
-  return v;
-}
-__device__ __forceinline__ void dma16(const void* g, unsigned lds_addr) {
-  __builtin_amdgcn_global_load_lds(g, (MX_LDS void*)(size_t)lds_addr, 16, 0, 0);
-}
+// LDS ring discipline: the K slices are copied global -> LDS by the DMA path
+// and the MFMA fragments read by inline-assembly ds_read_b128, with every wait
+// placed by hand (the helpers in mx_device.h).
 
 // Chunk swizzle of LDS row r: 16-byte chunk c is stored at c ^ swz(r).  A
 // 16-lane phase of a fragment read (rows r0 .. r0 + 15, one logical chunk)

@@ -52,6 +52,47 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+// Hand-placed waits and LDS traffic for kernels that copy global -> LDS with
+// the DMA path (global_load_lds, 16 bytes per lane; the hardware tracks it with
+// vmcnt only) and read their matrix-core fragments with ds_read_b128 issued
+// from inline assembly, so that every wait is placed by hand rather than
+// inferred (the compiler would otherwise wait for all DMA in flight before any
+// LDS read).  The compiler takes an inline-assembly read's result as available
+// at once: pin() ties fragment registers to the preceding wait so that no
+// consumer is scheduled above it, and the registers must stay live until then.
+template <int N>
+__device__ __forceinline__ void lgkm_wait() {
+  static_assert(N >= 0 && N <= 15, "lgkmcnt range");
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"i"(N) : "memory");
+}
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"i"(N) : "memory");
+}
+__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
+template <int K>
+__device__ __forceinline__ void pin(u32x4 (&f)[K]) {
+#pragma unroll
+  for (int i = 0; i < K; i++) asm volatile("" : "+v"(f[i]));
+}
+__device__ __forceinline__ u32x4 lds_read16(unsigned addr) {
+  u32x4 v;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr));
+  return v;
+}
+// the same with a constant byte offset added by the instruction
+template <int OFF>
+__device__ __forceinline__ u32x4 lds_read16_at(unsigned addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+  u32x4 v;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
+  return v;
+}
+__device__ __forceinline__ void dma16(const void* g, unsigned lds_addr) {
+  __builtin_amdgcn_global_load_lds(g, (MX_LDS void*)(size_t)lds_addr, 16, 0, 0);
+}
+
 // Request record uploaded by the host planner.
 struct ReqDev {
   int32_t tok_start;  // first row of the request in the batch
