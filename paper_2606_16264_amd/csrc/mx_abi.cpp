@@ -131,6 +131,7 @@ struct Plan {
   int64_t n_parts = 0;
   int split_pages = 16;
   int group = 1;
+  bool has_prefill = false;  // some work item is a prefill tile
 };
 
 // Decode splits: about 1024 work items (the chip holds 512 attention
@@ -259,6 +260,7 @@ void build_plan(const mx_batch* b, const mx_attn_shape* s, bool with_items, Plan
   // values through one L2 instead of all eight, which leaves more of the
   // fabric to the decode stream beside them: the 70B launch at P = 8192 took
   // 2.10 ms against 2.24 ms with one list for all XCDs (same at P <= 4096).
+  p.has_prefill = !p.items.empty();
   const std::vector<AttnItem> pre(std::move(p.items));
   const size_t nP = pre.size(), nD = dsorted.size();
   p.items.clear();
@@ -518,6 +520,7 @@ AttnParams attn_params(const Plan& p, const Layout& L, const mx_attn_shape* s, v
   a.group = p.group;
   a.split_pages = p.split_pages;
   a.scale_log2 = eff_scale(s) * 1.4426950408889634f;
+  a.decode_only = p.has_prefill ? 0 : 1;
   return a;
 }
 

@@ -22,6 +22,7 @@ struct AttnParams {
   float* part_ml;          // [parts][2] running max (log2 units) and sum
   int32_t nq, nkv, group, split_pages;
   float scale_log2;        // softmax scale * log2(e)
+  int32_t decode_only;     // no prefill items: decode keys and values are read non-temporally
 };
 
 hipError_t launch_paged_attn(const AttnParams& p, int n_items, const MergeItem* merges,
