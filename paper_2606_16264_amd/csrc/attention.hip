@@ -49,13 +49,18 @@ struct Chunk {
 // consecutive keys 8g .. 8g+7, all in page g / 2.  Those eight keys are then
 // one 16-byte run of a transposed value page, and they are exactly the k
 // indices the second product expects from this lane group.
-// NT: the loads are non-temporal (streamed past the caches' retention): a
-// launch of decode splits alone reads every key and value once, and so marked
-// the decode attention moved its bytes 3-12% faster on the four layer shapes
-// (7B 70.4 -> 78.2% of the HBM peak, 13B 69.5 -> 75.8%, Llama-3-8B 70.6 ->
-// 78.6%, 70B 78.2 -> 80.4%).  Beside prefill tiles, whose keys and values are
-// re-read from the caches, the same marking made the launch slower (70B at
-// P = 4096 2.19 ms against 1.88 ms), so there the loads are ordinary.
+// Non-temporal loads (streamed past the caches' retention): every key and
+// value of a decode split is read once.  A value load reads whole 128-byte
+// lines (16 dim rows x 32 bytes of a page, contiguous), so its values are
+// always loaded non-temporally.  A key load reads 64 bytes of each of its 16
+// key rows, and the other half of each line comes with the next load: beside
+// prefill tiles, whose key/value copies keep the L2 busy, a line marked
+// non-temporal was evidently dropped between the two, and the launch got
+// slower (70B at P = 4096: 2.19 ms against 1.88 ms); so keys are non-temporal
+// (NT) only in launches of decode splits alone.  Measured: decode-only
+// attention 3-11% faster on the four layer shapes (7B 70.0 -> 78.1% of the
+// HBM peak, 13B 70.6 -> 75.8%, Llama-3-8B 70.8 -> 78.8%, 70B 78.2 -> 80.3%);
+// non-temporal values in mixed launches 1-3.5% faster (70B, P = 1024 .. 8192).
 template <int HD, bool NT>
 __device__ __forceinline__ u32x4 stream_load(const uint16_t* ptr) {
   const u32x4* q = reinterpret_cast<const u32x4*>(ptr);
@@ -89,7 +94,7 @@ __device__ __forceinline__ void load_chunk(Chunk<HD>& c, const AttnParams& p, in
     const uint16_t* vb_ptr = p.v_pool + ((int64_t)page * p.nkv + kvh) * (int64_t)(16 * HD) + 8 * (g4 & 1);
 #pragma unroll
     for (int db = 0; db < HD / 16; db++)
-      c.v[db] = stream_load<HD, NT>(vb_ptr + (db * 16 + col) * 16);
+      c.v[db] = stream_load<HD, true>(vb_ptr + (db * 16 + col) * 16);
   }
 }
 
