@@ -150,24 +150,10 @@ __device__ __forceinline__ void rmsnorm_row(const uint16_t* __restrict__ x,
 // cost one memory round trip, not one each; further planes are summed one by
 // one.
 
-// Rows below split_row were completed by the GEMM itself (a row split of the
-// projection): their blocks read x1 and only normalise it.
-__device__ __forceinline__ float norm_complete_row(const u32x4* __restrict__ xrow, int nchunk,
-                                                   u32x4 (&v)[kNormChunks]) {
-  float ss = 0.f;
-#pragma unroll
-  for (int k = 0; k < kNormChunks; k++) {
-    const int c = threadIdx.x + k * kNormThreads;
-    v[k] = c < nchunk ? xrow[c] : u32x4{0, 0, 0, 0};
-    ss += sum_squares(v[k]);
-  }
-  return ss;
-}
-
 __global__ __launch_bounds__(kNormThreads) void reduce_residual_rmsnorm_kernel(
     const float* __restrict__ partial, int ksplit, const uint16_t* __restrict__ R,
     uint16_t* __restrict__ x1, const uint16_t* __restrict__ g, uint16_t* __restrict__ h, int M,
-    int H, float eps, int split_row) {
+    int H, float eps) {
   __shared__ float red[kNormThreads / 64];
   const int64_t row = blockIdx.x;
   const int nchunk = H / 8;
@@ -175,31 +161,8 @@ __global__ __launch_bounds__(kNormThreads) void reduce_residual_rmsnorm_kernel(
   u32x4* xrow = reinterpret_cast<u32x4*>(x1 + row * H);
   u32x4* hrow = reinterpret_cast<u32x4*>(h + row * H);
   u32x4 gv[kNormChunks], v[kNormChunks];
-  if (row < split_row) {
-#pragma unroll
-    for (int k = 0; k < kNormChunks; k++) {
-      const int c = threadIdx.x + k * kNormThreads;
-      gv[k] = c < nchunk ? gr[c] : u32x4{0, 0, 0, 0};
-    }
-    float ss = norm_complete_row(xrow, nchunk, v);
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
-    __syncthreads();
-    float tot = 0.f;
-#pragma unroll
-    for (int w = 0; w < kNormThreads / 64; w++) tot += red[w];
-    const float inv = 1.0f / sqrtf(tot / (float)H + eps);
-#pragma unroll
-    for (int k = 0; k < kNormChunks; k++) {
-      const int c = threadIdx.x + k * kNormThreads;
-      if (c < nchunk) rms_scale_store(v[k], gv[k], inv, hrow + c);
-    }
-    return;
-  }
-  const int64_t prow_idx = row - split_row;                  // row within the planes
-  const int64_t plane4 = (int64_t)(M - split_row) * H / 4;   // one plane in f32x4
-  const f32x4* prow = reinterpret_cast<const f32x4*>(partial + prow_idx * H);
+  const int64_t plane4 = (int64_t)M * H / 4;  // one plane in f32x4
+  const f32x4* prow = reinterpret_cast<const f32x4*>(partial + row * H);
   const u32x4* rrow = reinterpret_cast<const u32x4*>(R + row * H);
   f32x4 pl[kNormChunks][kNormPlanes][2];
   u32x4 r[kNormChunks];
@@ -433,8 +396,19 @@ hipError_t launch_reduce_residual_rmsnorm(const float* partial, int ksplit, cons
   if (M == 0) return hipSuccess;
   if (H % 8 != 0 || H > kFusedNormMaxH || ksplit < 1 || split_row < 0 || split_row > M)
     return hipErrorInvalidValue;
-  reduce_residual_rmsnorm_kernel<<<M, kNormThreads, 0, stream>>>(partial, ksplit, R, x1, g, h, M,
-                                                                 H, eps, split_row);
+  // Rows below split_row were completed by the GEMM itself (a row split of
+  // the projection): they only need the RMSNorm of x1, which the plain norm
+  // kernel does at its own occupancy (the fused kernel's plane registers,
+  // 166 VGPRs, leave one 512-thread block per CU: as one launch the 70B
+  // iteration's 8448 rows took 86 us).  The planes cover rows [split_row, M).
+  if (split_row > 0) rmsnorm_kernel<<<split_row, 256, 0, stream>>>(x1, g, h, H, eps);
+  const int tail = M - split_row;
+  if (tail > 0) {
+    const int64_t off = (int64_t)split_row * H;
+    reduce_residual_rmsnorm_kernel<<<tail, kNormThreads, 0, stream>>>(partial, ksplit, R + off,
+                                                                      x1 + off, g, h + off, tail,
+                                                                      H, eps);
+  }
   return hipGetLastError();
 }
 
