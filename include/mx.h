@@ -21,7 +21,15 @@
  *  - Page size is 16 tokens.  The KV slot of position p of a request is
  *    pages[p / 16] * 16 + p % 16.
  *  - Pools (one for keys, one for values), per layer, bf16:
- *      k_pool[pool_pages][n_kv_heads][16][head_dim]   (token-major within a page)
+ *      k_pool[pool_pages][n_kv_heads][head_dim / 32][16][32]
+ *                                                    (each page blocked by 32
+ *                                                     dims: element (slot s,
+ *                                                     dim e) of a page at
+ *                                                     (e / 32) * 512 + s * 32
+ *                                                     + e % 32, so that four
+ *                                                     consecutive slots of a
+ *                                                     32-dim block are one
+ *                                                     contiguous 256-byte run)
  *      v_pool[pool_pages][n_kv_heads][head_dim][16]   (each page stored transposed,
  *                                                     so that the matrix-core
  *                                                     operands load contiguously)

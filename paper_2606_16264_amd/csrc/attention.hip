@@ -52,15 +52,16 @@ struct Chunk {
 // Non-temporal loads (streamed past the caches' retention): every key and
 // value of a decode split is read once.  A value load reads whole 128-byte
 // lines (16 dim rows x 32 bytes of a page, contiguous), so its values are
-// always loaded non-temporally.  A key load reads 64 bytes of each of its 16
-// key rows, and the other half of each line comes with the next load: beside
-// prefill tiles, whose key/value copies keep the L2 busy, a line marked
-// non-temporal was evidently dropped between the two, and the launch got
-// slower (70B at P = 4096: 2.19 ms against 1.88 ms); so keys are non-temporal
-// (NT) only in launches of decode splits alone.  Measured: decode-only
-// attention 3-11% faster on the four layer shapes (7B 70.0 -> 78.1% of the
-// HBM peak, 13B 70.6 -> 75.8%, Llama-3-8B 70.8 -> 78.8%, 70B 78.2 -> 80.3%);
-// non-temporal values in mixed launches 1-3.5% faster (70B, P = 1024 .. 8192).
+// always loaded non-temporally.  Keys are non-temporal (NT) only in launches
+// of decode splits alone.  With token-major key pages a key load read half
+// lines, and beside prefill tiles (whose copies keep the L2 busy) non-temporal
+// keys made the launch slower (70B at P = 4096: 2.19 ms against 1.88 ms); with
+// the blocked key pages every key load reads whole lines, and non-temporal
+// keys in mixed launches measured no better than ordinary ones.  Measured:
+// decode-only attention 3-11% faster on the four layer shapes (7B 70.0 ->
+// 78.1% of the HBM peak, 13B 70.6 -> 75.8%, Llama-3-8B 70.8 -> 78.8%, 70B
+// 78.2 -> 80.3%); non-temporal values in mixed launches 1-3.5% faster (70B,
+// P = 1024 .. 8192).
 template <int HD, bool NT>
 __device__ __forceinline__ u32x4 stream_load(const uint16_t* ptr) {
   const u32x4* q = reinterpret_cast<const u32x4*>(ptr);
@@ -75,7 +76,11 @@ __device__ __forceinline__ void load_chunk(Chunk<HD>& c, const AttnParams& p, in
   // instead: those keys and values are masked out by select in
   // process_chunk, and every load stays unconditional, which keeps the
   // count of loads in flight the same on every path.
-  // keys: lane row m = col; its key kappa_b(col) lives in page col / 8
+  // keys: lane row m = col; its key kappa_b(col) lives in page col / 8.  A key
+  // page is blocked by 32 dims ([d / 32][16 slots][32]), so the four
+  // consecutive slots that rows 4i .. 4i + 3 read of a 32-dim block in one
+  // load are one contiguous 256-byte run: every load moves whole 128-byte
+  // lines.
   {
     const int page0 = (col < 8) ? pid0 : pid1;
     const int page = page0 >= 0 ? page0 : safe;
@@ -85,7 +90,7 @@ __device__ __forceinline__ void load_chunk(Chunk<HD>& c, const AttnParams& p, in
     for (int b = 0; b < 2; b++)
 #pragma unroll
       for (int ds = 0; ds < HD / 32; ds++)
-        c.k[b][ds] = stream_load<HD, NT>(kb_ptr + (slot0 + 4 * b) * HD + ds * 32 + 8 * g4);
+        c.k[b][ds] = stream_load<HD, NT>(kb_ptr + ds * 512 + (slot0 + 4 * b) * 32 + 8 * g4);
   }
   // values: lane group g reads keys 8 (g % 2) .. +7 of page g / 2 at d = 16 db + col
   {
@@ -286,8 +291,9 @@ __device__ __forceinline__ bool chunk_interior(int pi0, int page_end, int first_
 // c ^ ((d >> 2) & 3).  Both make the fragment reads (16 key rows, or 16 dim
 // rows, at one logical chunk) hit distinct bank groups.  A DMA instruction
 // writes 1 KB of LDS in lane order, so each lane fetches the 16 bytes that
-// belong at its position: a permutation within the page's rows, which keeps
-// every copy a run of whole 64-byte (or longer) segments.
+// belong at its position: a permutation within the page's rows (and, for
+// keys, within its 32-dim blocks), which keeps every copy a run of whole
+// 128-byte lines.
 template <int HD>
 __device__ __forceinline__ int ksw(int key) {
   if constexpr (HD == 128) return (key & 3) | ((key >> 3) << 2);
@@ -402,7 +408,7 @@ __device__ __forceinline__ void prefill_item(const AttnParams& p, const AttnItem
       const int j = kb * (64 / lanes_per_row) + lane / lanes_per_row;
       const int lc = (lane % lanes_per_row) ^ ksw<HD>(j);
       sel[i] = j >= 16;
-      off[i] = (j & 15) * HD + lc * 8;
+      off[i] = (lc >> 2) * 512 + (j & 15) * 32 + (lc & 3) * 8;
     } else {
       const int d = (kb - KB / 1024) * 16 + (lane >> 2);
       const int c = (lane & 3) ^ ((d >> 2) & 3);  // logical 8-key piece: page c / 2

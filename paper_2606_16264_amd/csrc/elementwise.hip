@@ -268,11 +268,11 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const uint16_t* __restri
   const int n = nkv * d;
   const uint16_t* ks = k_new + t * n;
   const uint16_t* vs = v_new + t * n;
-  // keys: 16-byte chunks, token-major within the page
+  // keys: 16-byte chunks; a key page is blocked by 32 dims, [d / 32][16][32]
   for (int c = threadIdx.x; c < n / 8; c += blockDim.x) {
     const int g = (c * 8) / d, e = (c * 8) % d;
-    *reinterpret_cast<u32x4*>(k_pool + ((page * nkv + g) * 16 + s_in) * d + e) =
-        *reinterpret_cast<const u32x4*>(ks + c * 8);
+    *reinterpret_cast<u32x4*>(k_pool + (page * nkv + g) * 16 * d + (e / 32) * 512 + s_in * 32 +
+                              e % 32) = *reinterpret_cast<const u32x4*>(ks + c * 8);
   }
   for (int u = threadIdx.x; u < n; u += blockDim.x) {
     const int g = u / d, e = u % d;
@@ -292,7 +292,7 @@ __global__ __launch_bounds__(256) void gather_kernel(const uint16_t* __restrict_
   const int n = nkv * d;
   for (int u = threadIdx.x; u < n; u += blockDim.x) {
     const int g = u / d, e = u % d;
-    k_out[j * n + u] = k_pool[((page * nkv + g) * 16 + s_in) * d + e];
+    k_out[j * n + u] = k_pool[(page * nkv + g) * 16 * d + (e / 32) * 512 + s_in * 32 + e % 32];
     v_out[j * n + u] = v_pool[((page * nkv + g) * d + e) * 16 + s_in];
   }
 }

@@ -105,14 +105,19 @@ __device__ __forceinline__ void qkv_pair_store(uint16_t* __restrict__ q_out,
     const float rlo = lo * cs.x - hi * cs.y;
     const float rhi = hi * cs.x + lo * cs.y;
     uint16_t* dst;
+    int step;  // element distance from dim d_lo to dim d_lo + hd/2
     if (head < nq) {
-      dst = q_out + ((int64_t)t * nq + head) * hd;
+      dst = q_out + ((int64_t)t * nq + head) * hd + d_lo;
+      step = hd / 2;
     } else {
+      // key pages blocked by 32 dims: [d / 32][16 slots][32]
       const int64_t page = slot / 16;
-      dst = k_pool + ((page * nkv + (head - nq)) * 16 + slot % 16) * hd;
+      dst = k_pool + (page * nkv + (head - nq)) * 16 * hd + (d_lo / 32) * 512 + (slot % 16) * 32 +
+            d_lo % 32;
+      step = 8 * hd;
     }
-    dst[d_lo] = f32_to_bf16(rlo);
-    dst[d_lo + hd / 2] = f32_to_bf16(rhi);
+    dst[0] = f32_to_bf16(rlo);
+    dst[step] = f32_to_bf16(rhi);
   } else {
     const int64_t page = slot / 16;
     uint16_t* dst = v_pool + ((page * nkv + (head - nq - nkv)) * hd) * 16 + slot % 16;
@@ -217,7 +222,8 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MB][NB], int M,
             const float2 c = cs[jj][jp][ii];
             val[jj][jp][ii] = pack_bf16x2(lo[ii] * c.x - hi[ii] * c.y, hi[ii] * c.x + lo[ii] * c.y);
             dst[jj][jp][ii] = head < nq ? ((int64_t)t * nq + head) * hd + d_lo
-                                        : (((sl >> 4) * nkv + (head - nq)) * 16 + (sl & 15)) * hd + d_lo;
+                                        : ((sl >> 4) * nkv + (head - nq)) * 16 * hd +
+                                              (d_lo >> 5) * 512 + (sl & 15) * 32 + (d_lo & 31);
           } else {
             val[jj][jp][ii] = pack_bf16x2(lo[ii], hi[ii]);
             dst[jj][jp][ii] = (((sl >> 4) * nkv + (head - nq - nkv)) * hd + within) * 16 + (sl & 15);
@@ -256,7 +262,7 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MB][NB], int M,
             q_out[dst[jj][jp][ii] + hd / 2] = vhi;
           } else if (head < nq + nkv) {
             k_pool[dst[jj][jp][ii]] = vlo;
-            k_pool[dst[jj][jp][ii] + hd / 2] = vhi;
+            k_pool[dst[jj][jp][ii] + 8 * hd] = vhi;  // dim d_lo + hd/2: hd/64 blocks on
           } else {
             v_pool[dst[jj][jp][ii]] = vlo;
             v_pool[dst[jj][jp][ii] + 32 * 16] = vhi;

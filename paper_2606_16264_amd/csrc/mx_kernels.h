@@ -96,7 +96,7 @@ struct QkvEpilogue {
   const float2* rope_cs;   // [T][head_dim / 2] (cos, sin)
   const int64_t* tok_slot; // [T] KV slot of each token
   uint16_t* q_out;         // [T][nq][head_dim]
-  uint16_t* k_pool;        // [pages][nkv][16][head_dim]
+  uint16_t* k_pool;        // [pages][nkv][head_dim / 32][16][32]
   uint16_t* v_pool;        // [pages][nkv][head_dim][16]
   int nq, nkv, head_dim;
 };

@@ -49,7 +49,7 @@ def test_device_pool_fill_matches_host():
     wdev.fill_pools(k, v, cfg, b, 1000, poison=True)
     sync()
     hk, hv = wl.host_pool(cfg, b, 1000, poison=True)
-    np.testing.assert_array_equal(host_bits(k), hk)
+    np.testing.assert_array_equal(wdev.k_pool_canonical(k), hk)
     np.testing.assert_array_equal(wdev.v_pool_canonical(v), hv)
 
 
@@ -94,7 +94,7 @@ def test_kv_append_bit_exact(nkv, d):
     k, v = wdev.alloc_pools(cfg, b.pool_pages)
     wdev.fill_pools(k, v, cfg, b, 7, poison=True)
     sync()
-    k0, v0 = host_bits(k).copy(), wdev.v_pool_canonical(v)
+    k0, v0 = wdev.k_pool_canonical(k), wdev.v_pool_canonical(v)
     kn = rng.integers(0, 65536, (b.T, nkv, d), dtype=np.uint16)
     vn = rng.integers(0, 65536, (b.T, nkv, d), dtype=np.uint16)
     mb = mx_batch(mx, b)
@@ -103,7 +103,7 @@ def test_kv_append_bit_exact(nkv, d):
     mx.mx_kv_append(mb, shape, dev(kn), dev(vn), k, v, ws)
     sync()
     ek, ev = oracle.kv_append(b.n_new, b.ctx_len, b.page_tables, kn, vn, k0, v0)
-    np.testing.assert_array_equal(host_bits(k), ek)
+    np.testing.assert_array_equal(wdev.k_pool_canonical(k), ek)
     np.testing.assert_array_equal(wdev.v_pool_canonical(v), ev)
 
 
@@ -158,12 +158,12 @@ def attention_case(cfg, b, seed, rng, needle=False):
                 qf[t:t + int(b.n_new[r]), g * (nq // nkv):(g + 1) * (nq // nkv)] = qd
                 kp[pstart[r] + j, g] = wl.f32_to_bf16_bits(20.0 * qd / np.linalg.norm(qd) * math.sqrt(d) / 4)
         # write the needle keys into the device pool
-        kh = host_bits(k).copy()
+        kh = wdev.k_pool_canonical(k)
         for r in range(b.R):
             for j in range(int(b.ctx_len[r])):
                 page = b.page_tables[r][j // 16]
                 kh[page, :, j % 16] = kp[pstart[r] + j]
-        k.copy_(torch.from_numpy(kh).cuda())
+        k.copy_(torch.from_numpy(wdev.k_pool_blocked(kh)).cuda())
     q = wl.f32_to_bf16_bits(qf)
     mb = mx_batch(mx, b)
     shape = mx_shape(mx, cfg, b.pool_pages)
@@ -482,7 +482,7 @@ def check_pool_rows(cfg, b, got, exp_k, exp_v, tok_idx):
     pg = torch.from_numpy(slots // 16).cuda()
     sl = torch.from_numpy(slots % 16).cuda()
     # uint16 tensors cannot be gathered on the device; gather their int16 view
-    kk = got["k"].view(torch.int16)[pg, :, sl].view(torch.uint16)
+    kk = got["k"].view(torch.int16)[pg, :, :, sl].view(torch.uint16)  # [n][nkv][d/32][32]
     vv = got["v"].view(torch.int16)[pg, :, :, sl].view(torch.uint16)
     assert_rows_close(bits_to_f64(kk).reshape(-1, cfg.head_dim),
                       exp_k.reshape(-1, cfg.head_dim), what="appended k")
@@ -540,8 +540,11 @@ def small_weights(rng, cfg):
 def changed_slots(before, after, transposed):
     """Slots (page * 16 + s) where a pool differs bitwise between two images."""
     diff = before.view(torch.int16) != after.view(torch.int16)
-    # keys [page][kv head][16][d], values [page][kv head][d][16]
-    per_slot = diff.any(dim=3).any(dim=1) if not transposed else diff.any(dim=2).any(dim=1)
+    # keys [page][kv head][d/32][16][32], values [page][kv head][d][16]
+    if transposed:
+        per_slot = diff.any(dim=2).any(dim=1)
+    else:
+        per_slot = diff.any(dim=4).any(dim=2).any(dim=1)
     pg, sl = torch.nonzero(per_slot, as_tuple=True)
     return set((pg.cpu().numpy().astype(np.int64) * 16 + sl.cpu().numpy()).tolist())
 

@@ -6,9 +6,10 @@
 // (Steele, Lea and Flood 2014):
 //   z = mix64(key + (c + 1) * 0x9E3779B97F4A7C15)
 //   v = float((int)(z >> 40) - 2^23) * 2^-23 * 1.7320508f  -> bf16 (round to nearest even)
-// Pages whose `owned` flag is 0 are filled with bf16 NaN instead.  The V pool
-// is written in the transposed page layout [page][head][dim][slot] that the
-// attention kernels read.
+// Pages whose `owned` flag is 0 are filled with bf16 NaN instead.  The pools
+// are written in the page layouts the attention kernels read: K pages blocked
+// by 32 dims, [page][head][dim / 32][slot][32], V pages transposed,
+// [page][head][dim][slot].
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -59,7 +60,9 @@ __global__ void fill_pool_kernel(uint16_t* k_pool, uint16_t* v_pool, int64_t pag
     w.y = kv[2] | ((uint32_t)kv[3] << 16);
     w.z = kv[4] | ((uint32_t)kv[5] << 16);
     w.w = kv[6] | ((uint32_t)kv[7] << 16);
-    *reinterpret_cast<uint4*>(k_pool + e0) = w;
+    // key pages blocked by 32 dims: [d / 32][16 slots][32]
+    *reinterpret_cast<uint4*>(k_pool + (page * nkv + g) * (int64_t)(16 * d) + (dim0 / 32) * 512 +
+                              s * 32 + dim0 % 32) = w;
     uint16_t* vb = v_pool + (page * nkv + g) * (int64_t)(16 * d);
 #pragma unroll
     for (int i = 0; i < 8; i++) vb[(dim0 + i) * 16 + s] = vv[i];
@@ -76,7 +79,7 @@ __global__ void poison_slots_kernel(uint16_t* k_pool, uint16_t* v_pool, const in
     const int g = (int)((idx % per) / d), e = (int)(idx % d);
     const int64_t page = slot / 16;
     const int s = (int)(slot % 16);
-    k_pool[((page * nkv + g) * 16 + s) * d + e] = 0x7FC0;
+    k_pool[(page * nkv + g) * (int64_t)(16 * d) + (e / 32) * 512 + s * 32 + e % 32] = 0x7FC0;
     v_pool[((page * nkv + g) * d + e) * 16 + s] = 0x7FC0;
   }
 }

@@ -32,8 +32,9 @@ def lib():
 
 def alloc_pools(cfg: wl.LayerConfig, pool_pages: int, device="cuda"):
     import torch
-    k = torch.empty((pool_pages, cfg.n_kv_heads, 16, cfg.head_dim), dtype=torch.uint16,
-                    device=device)
+    # keys: each page blocked by 32 dims, [page][head][dim / 32][slot][32]
+    k = torch.empty((pool_pages, cfg.n_kv_heads, cfg.head_dim // 32, 16, 32),
+                    dtype=torch.uint16, device=device)
     # values: each page stored transposed, [page][head][dim][slot]
     v = torch.empty((pool_pages, cfg.n_kv_heads, cfg.head_dim, 16), dtype=torch.uint16,
                     device=device)
@@ -44,7 +45,7 @@ def fill_pools(k_pool, v_pool, cfg: wl.LayerConfig, batch: wl.Batch, seed: int,
                poison: bool = True) -> None:
     """Hash values everywhere; bf16 NaN on pages no request owns and on slots at
     or beyond each request's ctx_len (when ``poison``).  V is written in the
-    transposed page layout."""
+    transposed page layout and K in the blocked one."""
     import torch
     stream = torch.cuda.current_stream().cuda_stream
     owned = None
@@ -65,6 +66,26 @@ def fill_pools(k_pool, v_pool, cfg: wl.LayerConfig, batch: wl.Batch, seed: int,
             if rc != 0:
                 raise RuntimeError(f"mxgen_poison_slots failed ({rc})")
             torch.cuda.current_stream().synchronize()
+
+
+def _host(t) -> np.ndarray:
+    a = t.cpu().numpy() if hasattr(t, "cpu") else np.asarray(t)
+    return a.view(np.uint16)
+
+
+def k_pool_canonical(k_pool_b):
+    """Device K pool [pages][nkv][d/32][16][32] (blocked pages) -> numpy uint16
+    [pages][nkv][16][d]."""
+    a = _host(k_pool_b)
+    p, g, nb = a.shape[:3]
+    return np.ascontiguousarray(a.transpose(0, 1, 3, 2, 4).reshape(p, g, 16, nb * 32))
+
+
+def k_pool_blocked(k_canon: np.ndarray) -> np.ndarray:
+    """Canonical [pages][nkv][16][d] -> the device's blocked K page layout
+    [pages][nkv][d/32][16][32]."""
+    p, g, s, d = k_canon.shape
+    return np.ascontiguousarray(k_canon.reshape(p, g, s, d // 32, 32).transpose(0, 1, 3, 2, 4))
 
 
 def v_pool_canonical(v_pool_t):
