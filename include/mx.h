@@ -245,7 +245,13 @@ mx_status mx_layer_step(const mx_batch* batch, const mx_layer_cfg* cfg, const vo
 /* Byte offsets, inside the workspace of mx_layer_step for this batch, of the
  * intermediate tensors the call leaves behind (bf16):
  *   off[0] h / h2 [T][H] (h2 overwrites h), off[1] q [T][nq][d] (post-RoPE),
- *   off[2] o [T][nq][d], off[3] x1 [T][H], off[4] a [T][F].
+ *   off[2] o [T][nq * d], off[3] x1 [T][H], off[4] a [T][F].
+ * q and x1 are row-major.  h, o and a, the inputs of the projections, are in
+ * the projection-input tile layout: a T x K matrix stored as
+ * [ceil(T / 16)][K / 32][16][32], element (t, c) at
+ *   (t / 16) * 16 * K + (c / 32) * 512 + (t % 16) * 32 + c % 32,
+ * so that each 16-row x 32-column tile is one contiguous kilobyte (the GEMMs
+ * copy whole kilobytes, as they do from the packed weights).
  * (The new keys and values of the iteration are in the pools.) */
 mx_status mx_layer_workspace_offsets(const mx_batch* batch, const mx_layer_cfg* cfg,
                                      size_t off[5]);
@@ -298,10 +304,15 @@ mx_status mx_debug_gemm(int32_t M, int32_t N, int32_t K, const uint16_t* A, cons
 mx_status mx_debug_gemm_config(int32_t M, int32_t N, int32_t K, const uint16_t* A, const uint16_t* B,
                                uint16_t* C, const uint16_t* R, int32_t epilogue, int32_t tile_cfg,
                                int32_t ksplit, void* ws, size_t ws_bytes, hipStream_t stream);
-/* The same with B in the layer step's packed-weight tile layout: element (n, k) at
- * ((n / 16) * (K / 32) + k / 32) * 512 + (n % 16) * 32 + k % 32, i.e. 16 x 32 tiles of
- * 1 KB ordered [N / 16][K / 32].  N % 16 == 0 and K % 32 == 0 (else MX_ERR_UNSUPPORTED).
- * For tests and tuning sweeps of the layer's own operand layout. */
+/* The same with every operand in the layer step's own layout: B in the packed-weight
+ * tile layout, element (n, k) at ((n / 16) * (K / 32) + k / 32) * 512 + (n % 16) * 32
+ * + k % 32, i.e. 16 x 32 tiles of 1 KB ordered [N / 16][K / 32]; A in the same tile
+ * layout over its M rows (ceil(M / 16) * 16 * K elements; the padding rows of the last
+ * tile row are never read); C row-major [M][N], except the SwiGLU output, which is in
+ * the tile layout too (ceil(M / 16) * 16 * N / 2 elements; the padding rows are never
+ * written), as the layer's down projection reads it.  R row-major.  N % 16 == 0 and
+ * K % 32 == 0 (else MX_ERR_UNSUPPORTED).  For tests and tuning sweeps of the layer's
+ * own operand layout. */
 mx_status mx_debug_gemm_tiled(int32_t M, int32_t N, int32_t K, const uint16_t* A,
                               const uint16_t* B_tiled, uint16_t* C, const uint16_t* R,
                               int32_t epilogue, int32_t tile_cfg, int32_t ksplit, void* ws,
@@ -314,11 +325,12 @@ mx_status mx_debug_gemm_tiled(int32_t M, int32_t N, int32_t K, const uint16_t* A
  * tile shape plan[3] and K split plan[4] (plan[2] == M: one launch, plan[3] = -1).
  * K must be a multiple of 64.  For tests that must know which path a shape takes. */
 mx_status mx_debug_gemm_plan(int32_t M, int32_t N, int32_t K, int32_t plan[5]);
-/* A forced row split with B in the packed tile layout (as mx_debug_gemm_tiled):
- * rows [0, m_main) with tile shape main_cfg and no K split, then rows
- * [m_main, M) as a GEMM of their own with tile shape tail_cfg and K split
+/* A forced row split with the operands in the layer's layouts (as
+ * mx_debug_gemm_tiled): rows [0, m_main) with tile shape main_cfg and no K split,
+ * then rows [m_main, M) as a GEMM of their own with tile shape tail_cfg and K split
  * tail_ksplit (ws holds tail_ksplit * (M - m_main) * N floats when it is > 1).
- * 1 <= m_main < M, N % 16 == 0, K % 64 == 0.  For tests of the row split. */
+ * 1 <= m_main < M with m_main % 16 == 0 (the second GEMM starts a tile row),
+ * N % 16 == 0, K % 64 == 0.  For tests of the row split. */
 mx_status mx_debug_gemm_rows(int32_t M, int32_t N, int32_t K, const uint16_t* A,
                              const uint16_t* B_tiled, uint16_t* C, const uint16_t* R,
                              int32_t epilogue, int32_t m_main, int32_t main_cfg, int32_t tail_cfg,
@@ -327,8 +339,10 @@ mx_status mx_debug_gemm_rows(int32_t M, int32_t N, int32_t K, const uint16_t* A,
  * own: for rows r >= split_row, x1[r] = bf16(sum_z partial[z][r - split_row] + R[r])
  * (partial: ksplit fp32 planes [M - split_row][H], summed in plane order, then
  * the residual); rows r < split_row hold x1 already.  Then h[r] = RMSNorm(x1[r]) * g
- * for every row, from the rounded x1.  R, x1, h [M][H] bf16, g [H] bf16;
- * H % 8 == 0 and H <= 8192.  For tests of the kernel the layer step runs. */
+ * for every row, from the rounded x1.  R, x1 [M][H] bf16 row-major, g [H] bf16, h
+ * in the projection-input tile layout (mx_layer_workspace_offsets; ceil(M / 16) * 16
+ * * H elements); H % 32 == 0 and H <= 8192.  For tests of the kernel the layer step
+ * runs. */
 mx_status mx_debug_reduce_residual_rmsnorm(const float* partial, int32_t ksplit, const uint16_t* R,
                                            uint16_t* x1, const uint16_t* g, uint16_t* h, int32_t M,
                                            int32_t H, float eps, int32_t split_row,

@@ -283,16 +283,18 @@ def mx_debug_gemm_ws_bytes(M: int, N: int, K: int) -> int:
 
 
 def mx_debug_gemm(A, B, C, R=None, epilogue: int = EPI_STORE, ws=None, stream=None,
-                  tile_cfg: int = -1, ksplit: int = 0, b_tiled: bool = False, N: int = None) -> None:
+                  tile_cfg: int = -1, ksplit: int = 0, tiled: bool = False, M: int = None,
+                  N: int = None, K: int = None) -> None:
     """C = epi(A B^T); A [M][K], B [N][K], C [M][N] (or [M][N/2] for SwiGLU).
-    tile_cfg >= 0 forces a tile shape and K split (tuning).  b_tiled: B holds
-    the N x K weights in the packed 16 x 32 tile layout (any shape; pass N)."""
-    M, K = A.shape
-    if b_tiled:
-        if N is None:
-            raise ValueError("b_tiled needs N")
+    tile_cfg >= 0 forces a tile shape and K split (tuning).  tiled: the
+    operands in the layer step's layouts (mx_debug_gemm_tiled: A and B in the
+    16 x 32 tile layout, the SwiGLU output too; any tensor shapes, pass M, N, K)."""
+    if tiled:
+        if M is None or N is None or K is None:
+            raise ValueError("tiled needs M, N and K")
         fn = _lib.mx_debug_gemm_tiled
     else:
+        M, K = A.shape
         N = B.shape[0]
         fn = _lib.mx_debug_gemm_config
     _check(fn(M, N, K, _ptr(A), _ptr(B), _ptr(C), _ptr(R), epilogue, tile_cfg, ksplit, _ptr(ws),
@@ -307,11 +309,12 @@ def mx_debug_gemm_plan(M: int, N: int, K: int) -> dict:
             "tail_ksplit": out[4]}
 
 
-def mx_debug_gemm_rows(A, B_tiled, C, R, epilogue: int, N: int, m_main: int, main_cfg: int,
-                       tail_cfg: int, tail_ksplit: int, ws=None, stream=None) -> None:
-    """A forced row split (B in the packed tile layout): rows [0, m_main) with
-    tile shape main_cfg, the rest with tail_cfg split tail_ksplit ways over K."""
-    M, K = A.shape
+def mx_debug_gemm_rows(A, B_tiled, C, R, epilogue: int, M: int, N: int, K: int, m_main: int,
+                       main_cfg: int, tail_cfg: int, tail_ksplit: int, ws=None,
+                       stream=None) -> None:
+    """A forced row split (operands in the layer's layouts, as mx_debug_gemm
+    with tiled=True): rows [0, m_main) with tile shape main_cfg, the rest with
+    tail_cfg split tail_ksplit ways over K."""
     _check(_lib.mx_debug_gemm_rows(M, N, K, _ptr(A), _ptr(B_tiled), _ptr(C), _ptr(R), epilogue,
                                    m_main, main_cfg, tail_cfg, tail_ksplit, _ptr(ws),
                                    0 if ws is None else ws.numel(), _stream(stream)))

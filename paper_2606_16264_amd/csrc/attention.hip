@@ -37,6 +37,12 @@ namespace {
 
 constexpr float kNegBig = -1.0e30f;
 
+// Element (token t, column c = head * HD + dim) of the attention output:
+// [T][nq][HD] row-major, or the projection-input tile layout when out_tiled.
+__device__ __forceinline__ uint16_t* out_ptr(const AttnParams& p, int64_t t, int64_t c) {
+  return p.out + (p.out_tiled ? tile_index(t, c, p.out_tok_stride) : t * p.out_tok_stride + c);
+}
+
 template <int HD>
 struct Chunk {
   u32x4 k[2][HD / 32];  // keys: 16 B per lane per (score block, d-step)
@@ -570,26 +576,28 @@ __device__ __forceinline__ void prefill_item(const AttnParams& p, const AttnItem
 
   // the rows' sums over their four lane groups (every lane takes part)
   const float l1 = lane_groups_sum(r1.l), l2 = lane_groups_sum(r2.l);
+  // dims 16 db + 4 g4 .. + 3 of the row: (db / 2) 32-column steps plus 16 (db % 2)
+  const int64_t step32 = p.out_tiled ? 512 : 32;
   if (row_valid) {
     const float inv = 1.f / l1;
-    uint16_t* op = p.out + qtok * p.out_tok_stride + (int64_t)qhead * HD + 4 * g4;
+    uint16_t* op = out_ptr(p, qtok, qhead * HD + 4 * g4);
 #pragma unroll
     for (int db = 0; db < HD / 16; db++) {
       u32x2 w;
       w[0] = pack_bf16x2(o[db][0] * inv, o[db][1] * inv);
       w[1] = pack_bf16x2(o[db][2] * inv, o[db][3] * inv);
-      *reinterpret_cast<u32x2*>(op + db * 16) = w;
+      *reinterpret_cast<u32x2*>(op + (db >> 1) * step32 + (db & 1) * 16) = w;
     }
   }
   if (row_valid2) {
     const float inv = 1.f / l2;
-    uint16_t* op = p.out + qtok2 * p.out_tok_stride + (int64_t)qhead * HD + 4 * g4;
+    uint16_t* op = out_ptr(p, qtok2, qhead * HD + 4 * g4);
 #pragma unroll
     for (int db = 0; db < HD / 16; db++) {
       u32x2 w;
       w[0] = pack_bf16x2(o2[db][0] * inv, o2[db][1] * inv);
       w[1] = pack_bf16x2(o2[db][2] * inv, o2[db][3] * inv);
-      *reinterpret_cast<u32x2*>(op + db * 16) = w;
+      *reinterpret_cast<u32x2*>(op + (db >> 1) * step32 + (db & 1) * 16) = w;
     }
   }
 }
@@ -717,7 +725,7 @@ __device__ __forceinline__ void decode_item(const AttnParams& p, const AttnItem&
   const int h = it.head + row;
   if (rq.n_split == 1) {
     const float inv = 1.f / L;
-    uint16_t* op = p.out + qtok * p.out_tok_stride + (int64_t)h * HD + dseg;
+    uint16_t* op = out_ptr(p, qtok, h * HD + dseg);  // HD / 16 dims within a 32-column block
 #pragma unroll
     for (int e = 0; e < HD / 16; e += 2)
       *reinterpret_cast<uint32_t*>(op + e) = pack_bf16x2(acc[e] * inv, acc[e + 1] * inv);
@@ -764,7 +772,7 @@ __global__ __launch_bounds__(HD) void attn_merge_kernel(AttnParams p, const Merg
     L += p.part_ml[(base + s) * 2 + 1] * w;
     acc += p.part_o[(base + s) * HD + d] * w;
   }
-  p.out[(int64_t)rq.tok_start * p.out_tok_stride + (int64_t)h * HD + d] = f32_to_bf16(acc / L);
+  *out_ptr(p, rq.tok_start, h * HD + d) = f32_to_bf16(acc / L);
 }
 
 }  // namespace

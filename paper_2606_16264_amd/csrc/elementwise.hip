@@ -80,11 +80,17 @@ __device__ __forceinline__ float block_sum_256(float v, float* red) {
   return red[0] + red[1] + red[2] + red[3];
 }
 
-// One row per block of 256 threads.  Rows of up to 8192 elements are held in
-// registers between the sum of squares and the scaling (with the gains, read
-// in the same first pass), so the row is read from memory once; longer rows
-// are read twice.
-constexpr int kRowChunks = 4;  // 16-byte chunks per thread held in registers
+// Two rows per block of 256 threads, written in the tile layout.  Thread t
+// works on row 2j + (t / 4) % 2 and on its chunks (8 columns each)
+// i = 4 (t / 8) + t % 4 + 128 k: the eight threads 8 s .. 8 s + 7 hold the same
+// 32 columns of both rows, which are one 128-byte line of a 16 x 32 tile
+// (rows 2j and 2j + 1 are adjacent in it), so every store instruction writes
+// whole lines; with one row per block each store covered half a line, and the
+// 70B-shaped norms took 70-77 us instead of 52-58 us.  Rows of up to 8192
+// elements are held in registers between the sum of squares and the scaling
+// (with the gains, read in the same first pass), so a row is read from memory
+// once; longer rows are read twice.
+constexpr int kPairChunks = 8;  // 16-byte chunks per thread held in registers
 
 __device__ __forceinline__ void rms_scale_store(u32x4 v, u32x4 gv, float inv, u32x4* dst) {
   u32x4 w;
@@ -107,44 +113,64 @@ __device__ __forceinline__ float sum_squares(u32x4 v) {
   return ss;
 }
 
-__device__ __forceinline__ void rmsnorm_row(const uint16_t* __restrict__ x,
-                                            const uint16_t* __restrict__ g,
-                                            uint16_t* __restrict__ out, int H, float eps,
-                                            int64_t row, float* red) {
-  const u32x4* xr = reinterpret_cast<const u32x4*>(x + row * H);
+// Sum over the block's threads of one row (par = (t / 4) % 2); red holds 8 floats.
+__device__ __forceinline__ float pair_sum_256(float v, float* red, int par) {
+  // every lane offset but 4, which would cross to the other row
+  v += __shfl_xor(v, 1);
+  v += __shfl_xor(v, 2);
+  v += __shfl_xor(v, 8);
+  v += __shfl_xor(v, 16);
+  v += __shfl_xor(v, 32);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (lane == 0 || lane == 4) red[2 * wave + (lane >> 2)] = v;
+  __syncthreads();
+  return red[par] + red[2 + par] + red[4 + par] + red[6 + par];
+}
+
+__device__ __forceinline__ void rmsnorm_pair(const uint16_t* __restrict__ x,
+                                             const uint16_t* __restrict__ g,
+                                             uint16_t* __restrict__ out, int H, float eps,
+                                             int64_t pair, int64_t T, float* red) {
+  const int t = threadIdx.x;
+  const int par = (t >> 2) & 1;
+  const int64_t row = 2 * pair + par;
+  const bool live = row < T;  // the second row of the last pair may not exist
+  const int i0 = 4 * (t >> 3) + (t & 3);
+  const u32x4* xr = reinterpret_cast<const u32x4*>(x + (live ? row : 2 * pair) * H);
   const u32x4* gr = reinterpret_cast<const u32x4*>(g);
-  u32x4* outr = reinterpret_cast<u32x4*>(out + row * H);
+  auto outc = [&](int c) { return reinterpret_cast<u32x4*>(out + tile_index(row, 8 * c, H)); };
   const int nchunk = H / 8;
-  if (nchunk <= kRowChunks * 256) {
-    u32x4 v[kRowChunks], gv[kRowChunks];
+  if (nchunk <= kPairChunks * 128) {
+    u32x4 v[kPairChunks], gv[kPairChunks];
     float ss = 0.f;
 #pragma unroll
-    for (int k = 0; k < kRowChunks; k++) {
-      const int c = threadIdx.x + k * 256;
-      const bool in = c < nchunk;
-      v[k] = in ? xr[c] : u32x4{0, 0, 0, 0};
-      gv[k] = in ? gr[c] : u32x4{0, 0, 0, 0};
+    for (int k = 0; k < kPairChunks; k++) {
+      const int c = i0 + k * 128;
+      v[k] = live && c < nchunk ? xr[c] : u32x4{0, 0, 0, 0};
+      gv[k] = c < nchunk ? gr[c] : u32x4{0, 0, 0, 0};
       ss += sum_squares(v[k]);
     }
-    const float inv = 1.0f / sqrtf(block_sum_256(ss, red) / (float)H + eps);
+    const float inv = 1.0f / sqrtf(pair_sum_256(ss, red, par) / (float)H + eps);
 #pragma unroll
-    for (int k = 0; k < kRowChunks; k++) {
-      const int c = threadIdx.x + k * 256;
-      if (c < nchunk) rms_scale_store(v[k], gv[k], inv, outr + c);
+    for (int k = 0; k < kPairChunks; k++) {
+      const int c = i0 + k * 128;
+      if (live && c < nchunk) rms_scale_store(v[k], gv[k], inv, outc(c));
     }
     return;
   }
   float ss = 0.f;
-  for (int c = threadIdx.x; c < nchunk; c += 256) ss += sum_squares(xr[c]);
-  const float inv = 1.0f / sqrtf(block_sum_256(ss, red) / (float)H + eps);
-  for (int c = threadIdx.x; c < nchunk; c += 256) rms_scale_store(xr[c], gr[c], inv, outr + c);
+  if (live)
+    for (int c = i0; c < nchunk; c += 128) ss += sum_squares(xr[c]);
+  const float inv = 1.0f / sqrtf(pair_sum_256(ss, red, par) / (float)H + eps);
+  if (live)
+    for (int c = i0; c < nchunk; c += 128) rms_scale_store(xr[c], gr[c], inv, outc(c));
 }
 
 // The split-K reduce of a residual GEMM fused with the RMSNorm of its output,
 // one row per block of 512 threads: x1 = bf16(sum_z partial[z] + R), the sums
 // taken in split order and then the residual, exactly as the stand-alone
 // reduce does, and h = RMSNorm(x1, g) from the rounded x1, exactly as
-// rmsnorm_row does; the row stays in registers between the two (rows of up to
+// rmsnorm_pair does; the row stays in registers between the two (rows of up to
 // kFusedNormMaxH elements).  Every plane's loads of a thread (up to
 // kNormPlanes of them) are issued before the first sum, so that the planes
 // cost one memory round trip, not one each; further planes are summed one by
@@ -152,17 +178,17 @@ __device__ __forceinline__ void rmsnorm_row(const uint16_t* __restrict__ x,
 
 __global__ __launch_bounds__(kNormThreads) void reduce_residual_rmsnorm_kernel(
     const float* __restrict__ partial, int ksplit, const uint16_t* __restrict__ R,
-    uint16_t* __restrict__ x1, const uint16_t* __restrict__ g, uint16_t* __restrict__ h, int M,
-    int H, float eps) {
+    uint16_t* __restrict__ x1, const uint16_t* __restrict__ g, uint16_t* __restrict__ h,
+    int row0, int rows, int H, float eps) {
+  // block b: row row0 + b of R, x1 and h; row b of the planes ([rows][H] each)
   __shared__ float red[kNormThreads / 64];
-  const int64_t row = blockIdx.x;
+  const int64_t row = row0 + (int64_t)blockIdx.x;
   const int nchunk = H / 8;
   const u32x4* gr = reinterpret_cast<const u32x4*>(g);
   u32x4* xrow = reinterpret_cast<u32x4*>(x1 + row * H);
-  u32x4* hrow = reinterpret_cast<u32x4*>(h + row * H);
   u32x4 gv[kNormChunks], v[kNormChunks];
-  const int64_t plane4 = (int64_t)M * H / 4;  // one plane in f32x4
-  const f32x4* prow = reinterpret_cast<const f32x4*>(partial + row * H);
+  const int64_t plane4 = (int64_t)rows * H / 4;  // one plane in f32x4
+  const f32x4* prow = reinterpret_cast<const f32x4*>(partial + (int64_t)blockIdx.x * H);
   const u32x4* rrow = reinterpret_cast<const u32x4*>(R + row * H);
   f32x4 pl[kNormChunks][kNormPlanes][2];
   u32x4 r[kNormChunks];
@@ -226,21 +252,24 @@ __global__ __launch_bounds__(kNormThreads) void reduce_residual_rmsnorm_kernel(
 #pragma unroll
   for (int k = 0; k < kNormChunks; k++) {
     const int c = threadIdx.x + k * kNormThreads;
-    if (c < nchunk) rms_scale_store(v[k], gv[k], inv, hrow + c);
+    // h in the tile layout, like rmsnorm_pair's output (one row per block: each
+    // store covers half a line; this kernel runs on the split rows only)
+    if (c < nchunk)
+      rms_scale_store(v[k], gv[k], inv, reinterpret_cast<u32x4*>(h + tile_index(row, 8 * c, H)));
   }
 }
 
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict__ x,
                                                       const uint16_t* __restrict__ g,
-                                                      uint16_t* __restrict__ out, int H,
+                                                      uint16_t* __restrict__ out, int T, int H,
                                                       float eps) {
-  __shared__ float red[4];
-  rmsnorm_row(x, g, out, H, eps, blockIdx.x, red);
+  __shared__ float red[8];
+  rmsnorm_pair(x, g, out, H, eps, blockIdx.x, T, red);
 }
 
 // The first kernel of a layer step: the token map (blocks 0 .. map_blocks - 1)
-// and the first RMSNorm (one block per row after them), which do not depend on
-// each other, in one launch.
+// and the first RMSNorm (one block per pair of rows after them), which do not
+// depend on each other, in one launch.
 __global__ __launch_bounds__(256) void prologue_kernel(TokenMapArgs a, int map_blocks,
                                                        const uint16_t* __restrict__ x,
                                                        const uint16_t* __restrict__ g,
@@ -250,8 +279,8 @@ __global__ __launch_bounds__(256) void prologue_kernel(TokenMapArgs a, int map_b
   if ((int)blockIdx.x < map_blocks)
     token_map_block(a, blockIdx.x, s_start);
   else
-    rmsnorm_row(x, g, out, H, eps, (int64_t)blockIdx.x - map_blocks,
-                reinterpret_cast<float*>(s_start));
+    rmsnorm_pair(x, g, out, H, eps, (int64_t)blockIdx.x - map_blocks, a.T,
+                 reinterpret_cast<float*>(s_start));
 }
 
 // ---------------------------------------------------------------- KV append
@@ -378,15 +407,15 @@ hipError_t launch_prologue(const ReqDev* reqs, int R, int T, const int32_t* page
   if (R == 0 || T == 0) return hipSuccess;
   const int64_t map_blocks = ((int64_t)T * half + 255) / 256;
   const TokenMapArgs a{reqs, R, T, pages, tok_req, tok_pos, tok_slot, inv_freq, rope_cs, half};
-  prologue_kernel<<<(unsigned)(map_blocks + T), 256, 0, stream>>>(a, (int)map_blocks, x, g, out, H,
-                                                                  eps);
+  prologue_kernel<<<(unsigned)(map_blocks + (T + 1) / 2), 256, 0, stream>>>(a, (int)map_blocks, x,
+                                                                            g, out, H, eps);
   return hipGetLastError();
 }
 
 hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* g, uint16_t* out, int T, int H,
                           float eps, hipStream_t stream) {
   if (T == 0) return hipSuccess;
-  rmsnorm_kernel<<<T, 256, 0, stream>>>(x, g, out, H, eps);
+  rmsnorm_kernel<<<(T + 1) / 2, 256, 0, stream>>>(x, g, out, T, H, eps);
   return hipGetLastError();
 }
 
@@ -394,21 +423,18 @@ hipError_t launch_reduce_residual_rmsnorm(const float* partial, int ksplit, cons
                                           uint16_t* x1, const uint16_t* g, uint16_t* h, int M,
                                           int H, float eps, int split_row, hipStream_t stream) {
   if (M == 0) return hipSuccess;
-  if (H % 8 != 0 || H > kFusedNormMaxH || ksplit < 1 || split_row < 0 || split_row > M)
+  if (H % 32 != 0 || H > kFusedNormMaxH || ksplit < 1 || split_row < 0 || split_row > M)
     return hipErrorInvalidValue;
   // Rows below split_row were completed by the GEMM itself (a row split of
   // the projection): they only need the RMSNorm of x1, which the plain norm
   // kernel does at its own occupancy (the fused kernel's plane registers,
   // 166 VGPRs, leave one 512-thread block per CU: as one launch the 70B
   // iteration's 8448 rows took 86 us).  The planes cover rows [split_row, M).
-  if (split_row > 0) rmsnorm_kernel<<<split_row, 256, 0, stream>>>(x1, g, h, H, eps);
+  if (split_row > 0) rmsnorm_kernel<<<(split_row + 1) / 2, 256, 0, stream>>>(x1, g, h, split_row, H, eps);
   const int tail = M - split_row;
-  if (tail > 0) {
-    const int64_t off = (int64_t)split_row * H;
-    reduce_residual_rmsnorm_kernel<<<tail, kNormThreads, 0, stream>>>(partial, ksplit, R + off,
-                                                                      x1 + off, g, h + off, tail,
-                                                                      H, eps);
-  }
+  if (tail > 0)
+    reduce_residual_rmsnorm_kernel<<<tail, kNormThreads, 0, stream>>>(partial, ksplit, R, x1, g, h,
+                                                                      split_row, tail, H, eps);
   return hipGetLastError();
 }
 

@@ -361,14 +361,21 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
   const uint16_t* dsrc[L];
   int64_t dstep[L];
+  // A element (m, k) at A + (m / 16) 16 lda + (m % 16) a_row + (k / 32) a_kstep
+  // + k % 32: row-major (lda, 32) or the activation tiles (32, 512), where the
+  // 16 rows of an instruction are one contiguous kilobyte
+  const int a_row = a.a_tiled ? 32 : a.lda;
+  const int a_kstep = a.a_tiled ? 512 : BKS;
 #pragma unroll
   for (int i = 0; i < L; i++) {
     const int row0 = (wave_s * L + i) * 16;  // first tile row of instruction i
     const int row = row0 + (lane >> 2);
     const int c = (lane & 3) ^ swz(row);
     if (row0 < BM) {
-      dsrc[i] = a.A + (int64_t)min(m0 + row, a.M - 1) * a.lda + kbeg + c * 8;
-      dstep[i] = BKS;
+      const int m = min(m0 + row, a.M - 1);
+      dsrc[i] = a.A + (int64_t)(m >> 4) * 16 * a.lda + (int64_t)(m & 15) * a_row +
+                (int64_t)(kbeg >> 5) * a_kstep + c * 8;
+      dstep[i] = a_kstep;
     } else {
       const int n = min(n0 + row - BM, a.N - 1);
       dsrc[i] = a.B + (int64_t)(n >> 4) * a.b_blk + (int64_t)(n & 15) * a.b_row +
@@ -521,7 +528,9 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
           const int colg = n0 + wave_n * WN + jp * 64;  // first packed column of the pair
           if (colg >= a.N) continue;
           const float gt = acc[i][2 * jp][r], up = acc[i][2 * jp + 1][r];
-          a.C[(int64_t)row * a.ldc + colg / 2 + ccol] = f32_to_bf16(silu(gt) * up);
+          const int col = colg / 2 + ccol;
+          a.C[a.c_tiled ? tile_index(row, col, a.ldc) : (int64_t)row * a.ldc + col] =
+              f32_to_bf16(silu(gt) * up);
         }
       }
     }
@@ -586,7 +595,8 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int kspl
         g += a.partial[z * plane + gi];
         u += a.partial[z * plane + ui];
       }
-      a.C[(int64_t)row * a.ldc + col] = f32_to_bf16(silu(g) * u);
+      a.C[a.c_tiled ? tile_index(row, col, a.ldc) : (int64_t)row * a.ldc + col] =
+          f32_to_bf16(silu(g) * u);
     } else {
       const int64_t pi = (int64_t)row * a.N + col;
       float v = 0.f;
@@ -741,7 +751,9 @@ size_t plan_scratch(const Plan& p, int M, int N) {
 
 // The GEMM of rows [m0, M) of a: every row-indexed operand moves by m0 rows
 // (A, C, R and, for the QKV epilogue, the rotary table, the token slots and
-// q_out; the pools are addressed through the slots).
+// q_out; the pools are addressed through the slots).  In the tile layout row
+// m0 starts a tile row only when m0 % 16 == 0, which the callers ensure; it
+// then sits m0 * K elements in, as in a row-major matrix.
 GemmArgs rows_from(const GemmArgs& a, int m0) {
   GemmArgs t = a;
   t.M = a.M - m0;
@@ -906,6 +918,7 @@ hipError_t launch_gemm_rows(const GemmArgs& a, size_t ws_floats, int m_main, int
   if (m_main < 1 || m_main >= a.M || cfg < 0 || cfg >= kNumShapes || tail_cfg < 0 ||
       tail_cfg >= kNumShapes || tail_ksplit < 1 || a.K / BK < tail_ksplit)
     return hipErrorInvalidValue;
+  if ((a.a_tiled || a.c_tiled) && m_main % 16) return hipErrorInvalidValue;
   const Plan p{cfg, 1, m_main, tail_cfg, tail_ksplit};
   if (plan_scratch(p, a.M, a.N) > ws_floats) return hipErrorInvalidValue;
   return launch_plan(a, p, true, stream);

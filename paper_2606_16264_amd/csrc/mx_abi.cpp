@@ -331,12 +331,14 @@ Layout make_layout(int64_t R, int64_t T, int64_t n_pages, int64_t n_items, int64
   L.part_ml = o; o = align_up(o + n_parts * 8);
   if (c) {
     const int64_t H = c->hidden, F = c->ffn, nq = s->n_q_heads;
+    // h, o and a are projection inputs in the tile layout: whole 16-row tiles
+    const int64_t T16 = (T + 15) / 16 * 16;
     L.rope_cs = o; o = align_up(o + T * (d / 2) * 8);
-    L.h = o; o = align_up(o + T * H * 2);
+    L.h = o; o = align_up(o + T16 * H * 2);
     L.q = o; o = align_up(o + T * nq * d * 2);
-    L.o = o; o = align_up(o + T * nq * d * 2);
+    L.o = o; o = align_up(o + T16 * nq * d * 2);
     L.x1 = o; o = align_up(o + T * H * 2);
-    L.a = o; o = align_up(o + T * F * 2);
+    L.a = o; o = align_up(o + T16 * F * 2);
     L.scratch = o; o = align_up(o + scratch_floats * 4);
     L.scratch_floats = scratch_floats;
   }
@@ -510,6 +512,7 @@ AttnParams attn_params(const Plan& p, const Layout& L, const mx_attn_shape* s, v
   a.v_pool = vp;
   a.out = out;
   a.out_tok_stride = (int64_t)s->n_q_heads * s->head_dim;
+  a.out_tiled = 0;
   a.reqs = at<ReqDev>(ws, L.reqs);
   a.pages = at<int32_t>(ws, L.pages);
   a.items = at<AttnItem>(ws, L.items);
@@ -892,12 +895,14 @@ MX_EXPORT mx_status mx_layer_step(const mx_batch* batch, const mx_layer_cfg* cfg
     GemmArgs g{h, (const uint16_t*)(P + W.qkv), nullptr, nullptr, scratch, M, Nqkv, H, H, H, 0, 0, EPI_QKV,
                QkvEpilogue{rope_cs, at<int64_t>(ws, L.tok_slot), q, k_pool, v_pool, nq, nkv, d}};
     set_b_tiled(g);
+    g.a_tiled = 1;
     MX_CK(timed("gemm_qkv", stream, [&] { return launch_gemm(g, L.scratch_floats, stream); }),
           "qkv gemm launch")
   }
   // a6: paged attention, prefill and decode rows in one launch (+ split merge)
   {
     AttnParams a = attn_params(p, L, s, ws, q, (int64_t)nq * d, k_pool, v_pool, o);
+    a.out_tiled = 1;  // o feeds the output projection
     MX_CK(timed("paged_attn", stream, [&] {
             return launch_paged_attn(a, (int)p.items.size(), at<MergeItem>(ws, L.merges),
                                      (int)p.merges.size(), d, stream);
@@ -910,6 +915,7 @@ MX_EXPORT mx_status mx_layer_step(const mx_batch* batch, const mx_layer_cfg* cfg
   {
     GemmArgs g{o, (const uint16_t*)(P + W.o), x1, x, scratch, M, H, nq * d, nq * d, nq * d, H, H, EPI_RESIDUAL, {}};
     set_b_tiled(g);
+    g.a_tiled = 1;
     const uint16_t* g2 = (const uint16_t*)(P + W.g2);
     const bool fuse = H <= kFusedNormMaxH;  // the fused kernel holds a row in registers
     int split_row = M, ks = 1;
@@ -927,6 +933,8 @@ MX_EXPORT mx_status mx_layer_step(const mx_batch* batch, const mx_layer_cfg* cfg
   {
     GemmArgs g{h, (const uint16_t*)(P + W.gu), act, nullptr, scratch, M, 2 * F, H, H, H, F, 0, EPI_SWIGLU, {}};
     set_b_tiled(g);
+    g.a_tiled = 1;
+    g.c_tiled = 1;  // act feeds the down projection
     MX_CK(timed("gemm_gate_up", stream, [&] { return launch_gemm(g, L.scratch_floats, stream); }),
           "gate/up gemm launch")
   }
@@ -934,6 +942,7 @@ MX_EXPORT mx_status mx_layer_step(const mx_batch* batch, const mx_layer_cfg* cfg
   {
     GemmArgs g{act, (const uint16_t*)(P + W.down), y, x1, scratch, M, H, F, F, F, H, H, EPI_RESIDUAL, {}};
     set_b_tiled(g);
+    g.a_tiled = 1;
     MX_CK(timed("gemm_down", stream, [&] { return launch_gemm(g, L.scratch_floats, stream); }),
           "down gemm launch")
   }
@@ -1051,10 +1060,13 @@ mx_status debug_gemm(int32_t M, int32_t N, int32_t K, const uint16_t* A, const u
   if (st != MX_OK) return st;
   const int ldc = epilogue == EPI_SWIGLU ? N / 2 : N;
   GemmArgs g{A, B, C, R, (float*)ws, M, N, K, K, K, ldc, N, epilogue, {}};
-  if (b_tiled)
+  if (b_tiled) {  // the layer step's operand layouts
     set_b_tiled(g);
-  else
+    g.a_tiled = 1;
+    g.c_tiled = epilogue == EPI_SWIGLU;
+  } else {
     set_b_row_major(g);
+  }
   hipError_t e = launch_gemm_config(g, ws ? ws_bytes / 4 : 0, tile_cfg, ksplit, stream);
   if (e != hipSuccess) return hip_fail(e, "gemm launch");
   return MX_OK;
@@ -1094,7 +1106,8 @@ MX_EXPORT mx_status mx_debug_gemm_rows(int32_t M, int32_t N, int32_t K, const ui
   g_err.clear();
   if (M < 2 || N <= 0 || K <= 0) return fail(MX_ERR_INVALID, "bad GEMM shape %d x %d x %d", M, N, K);
   if (N % 16 || K % 64) return fail(MX_ERR_UNSUPPORTED, "tiled weights need N %% 16 == 0 and K %% 64 == 0");
-  if (m_main < 1 || m_main >= M) return fail(MX_ERR_INVALID, "m_main %d not in [1, M)", m_main);
+  if (m_main < 1 || m_main >= M || m_main % 16)
+    return fail(MX_ERR_INVALID, "m_main %d not a multiple of 16 in [1, M)", m_main);
   if (main_cfg < 0 || main_cfg >= gemm_num_configs() || tail_cfg < 0 || tail_cfg >= gemm_num_configs())
     return fail(MX_ERR_INVALID, "tile config out of range");
   if (tail_ksplit < 1 || tail_ksplit > 64 || K / 64 < tail_ksplit)
@@ -1117,6 +1130,8 @@ MX_EXPORT mx_status mx_debug_gemm_rows(int32_t M, int32_t N, int32_t K, const ui
   const int ldc = epilogue == EPI_SWIGLU ? N / 2 : N;
   GemmArgs g{A, B_tiled, C, R, (float*)ws, M, N, K, K, K, ldc, N, epilogue, {}};
   set_b_tiled(g);
+  g.a_tiled = 1;
+  g.c_tiled = epilogue == EPI_SWIGLU;
   hipError_t e = launch_gemm_rows(g, ws ? ws_bytes / 4 : 0, m_main, main_cfg, tail_cfg, tail_ksplit,
                                   stream);
   if (e != hipSuccess) return hip_fail(e, "gemm launch");
@@ -1129,7 +1144,7 @@ MX_EXPORT mx_status mx_debug_reduce_residual_rmsnorm(const float* partial, int32
                                                      int32_t H, float eps, int32_t split_row,
                                                      hipStream_t stream) {
   g_err.clear();
-  if (M < 0 || H <= 0 || H % 8) return fail(MX_ERR_INVALID, "bad shape %d x %d", M, H);
+  if (M < 0 || H <= 0 || H % 32) return fail(MX_ERR_INVALID, "bad shape %d x %d", M, H);
   if (H > kFusedNormMaxH) return fail(MX_ERR_UNSUPPORTED, "H %d > %d", H, kFusedNormMaxH);
   if (ksplit < 1) return fail(MX_ERR_INVALID, "ksplit %d < 1", ksplit);
   if (split_row < 0 || split_row > M) return fail(MX_ERR_INVALID, "split_row %d not in [0, M]", split_row);

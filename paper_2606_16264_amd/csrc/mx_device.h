@@ -15,6 +15,16 @@ typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
 
 #define MX_LDS __attribute__((address_space(3)))
 
+// Activations that feed a projection (the RMSNorm outputs, the attention
+// output, the SwiGLU output) are stored in the GEMM operand tile layout: an
+// M x K matrix as [ceil(M / 16)][K / 32][16][32], each 16-row x 32-column tile
+// one contiguous kilobyte (K a multiple of 32), the layout of the packed
+// weights.  A GEMM copy instruction then reads one whole kilobyte instead of
+// sixteen 64-byte row pieces.  Element offset of (row r, column c):
+__host__ __device__ __forceinline__ int64_t tile_index(int64_t r, int64_t c, int64_t K) {
+  return (r >> 4) * 16 * K + (c >> 5) * 512 + (r & 15) * 32 + (c & 31);
+}
+
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
   return __uint_as_float(((uint32_t)b) << 16);
 }

@@ -14,7 +14,8 @@ struct AttnParams {
   const uint16_t* k_pool;
   const uint16_t* v_pool;
   uint16_t* out;
-  int64_t out_tok_stride;  // elements between consecutive tokens of out
+  int64_t out_tok_stride;  // elements between consecutive tokens of out (nq * head_dim)
+  int32_t out_tiled;       // out in the tile layout (tile_index) instead of [T][nq][head_dim]
   const ReqDev* reqs;
   const int32_t* pages;
   const AttnItem* items;
@@ -51,13 +52,17 @@ hipError_t launch_prologue(const ReqDev* reqs, int R, int T, const int32_t* page
                            hipStream_t stream);
 
 // RMSNorm: out[t] = x[t] / sqrt(mean(x[t]^2) + eps) * g, bf16 in/out, fp32 math.
+// x is row-major [T][H]; out, a projection's input, is in the tile layout
+// (tile_index, ceil(T / 16) * 16 rows), H % 32 == 0.  The same holds for the
+// RMSNorm outputs of the two launches around it.
 hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* g, uint16_t* out, int T, int H,
                           float eps, hipStream_t stream);
 
 // The residual split-K reduce fused with the RMSNorm of its result:
 // x1 = bf16(sum_z partial[z] + R) over [M][H] fp32 planes (R, x1 [M][H] bf16),
-// then h = RMSNorm(x1, g).  One row per block of kNormThreads threads, each
-// holding kNormChunks 16-byte chunks of the row in registers, so H % 8 == 0 and
+// then h = RMSNorm(x1, g) (h in the tile layout).  One row per block of
+// kNormThreads threads, each holding kNormChunks 16-byte chunks of the row in
+// registers, so H % 32 == 0 and
 // H <= kFusedNormMaxH; the first kNormPlanes planes are loaded ahead of the
 // first sum, any further ones are summed as they arrive.
 constexpr int kNormThreads = 512;
@@ -117,6 +122,10 @@ struct GemmArgs {
   // so that each DMA instruction reads one contiguous kilobyte
   int64_t b_blk, b_kstep;
   int b_row;
+  // a_tiled: A in the activation tile layout (tile_index, K = lda) instead of
+  // row-major; c_tiled: the SwiGLU output likewise (K = ldc).  Zero (the
+  // default of an aggregate initialisation) is row-major.
+  int a_tiled, c_tiled;
 };
 
 inline void set_b_row_major(GemmArgs& g) {

@@ -57,6 +57,27 @@ def bits_to_f64(t) -> np.ndarray:
     return wl.bf16_bits_to_f64(host_bits(t))
 
 
+def to_tiles(a, pad=0x7FC0) -> np.ndarray:
+    """[M][K] uint16 -> the projection-input tile layout [ceil(M/16)][K/32][16][32]
+    (flat); the padding rows of the last tile row are filled with `pad` (a NaN:
+    a kernel that read them would show it)."""
+    a = np.asarray(a, np.uint16)
+    M, K = a.shape
+    M16 = -(-M // 16) * 16
+    p = np.full((M16, K), pad, np.uint16)
+    p[:M] = a
+    return np.ascontiguousarray(p.reshape(M16 // 16, 16, K // 32, 32).transpose(0, 2, 1, 3)).reshape(-1)
+
+
+def from_tiles(t, M, K) -> np.ndarray:
+    """The inverse of to_tiles for M rows (a multiple of 16 when the padding
+    rows are wanted too): tile layout (device tensor or array) -> [M][K] uint16."""
+    a = (host_bits(t) if hasattr(t, "cpu") else np.asarray(t).view(np.uint16)).reshape(-1)
+    M16 = -(-M // 16) * 16
+    a = a[:M16 * K].reshape(M16 // 16, K // 32, 16, 32).transpose(0, 2, 1, 3).reshape(M16, K)
+    return np.ascontiguousarray(a[:M])
+
+
 def sample_rows(b: wl.Batch, rng, n_decode=16, n_prefill_random=62):
     """All decode rows of n_decode random decode requests, plus the first, the
     last and n_prefill_random random rows of every prefill chunk."""

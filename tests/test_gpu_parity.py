@@ -14,8 +14,8 @@ import pytest
 import oracle
 import workload as wl
 from helpers import (TOL, assert_rows_close, bf16_half_ulp, bits_to_f64, branch_err_rows, dev,
-                     host_bits, mx_batch, mx_cfg, mx_shape, rel_err_rows, sample_rows,
-                     truncated_subbatch)
+                     from_tiles, host_bits, mx_batch, mx_cfg, mx_shape, rel_err_rows,
+                     sample_rows, to_tiles, truncated_subbatch)
 
 pytestmark = pytest.mark.gpu
 
@@ -279,15 +279,25 @@ def gemm_case(M, N, K, epi, tile_cfg=-1, ksplit=0, b_tiled=False):
         (ksplit * M * N * 4 if ksplit > 1 else 0)
     ws = ws_tensor(max(need, 256))
     if b_tiled:
+        # the layer's layouts: A (NaN padding rows, never read) and the SwiGLU
+        # output in the tile layout, over whole 16-row tiles
         wt = np.ascontiguousarray(w.reshape(N // 16, 16, K // 32, 32).transpose(0, 2, 1, 3))
-        mx.mx_debug_gemm(dev(a), dev(wt.reshape(-1)), C, dev(r) if epi == 1 else None, epi, ws,
-                         tile_cfg=tile_cfg, ksplit=ksplit, b_tiled=True, N=N)
+        c_rows = -(-M // 16) * 16 if epi == 2 else M
+        buf16 = torch.full((lead + (c_rows + 2) * ncol,), CANARY, dtype=torch.int16, device="cuda")
+        C = buf16.view(torch.uint16)[lead:lead + c_rows * ncol].view(c_rows, ncol)
+        mx.mx_debug_gemm(dev(to_tiles(a)), dev(wt.reshape(-1)), C, dev(r) if epi == 1 else None,
+                         epi, ws, tile_cfg=tile_cfg, ksplit=ksplit, tiled=True, M=M, N=N, K=K)
     else:
+        c_rows = M
         mx.mx_debug_gemm(dev(a), dev(w), C, dev(r) if epi == 1 else None, epi, ws,
                          tile_cfg=tile_cfg, ksplit=ksplit)
     sync()
-    guard = torch.cat([buf16[:lead], buf16[lead + M * ncol:]]).cpu().numpy()
+    guard = torch.cat([buf16[:lead], buf16[lead + c_rows * ncol:]]).cpu().numpy()
     assert (guard == CANARY).all(), "GEMM wrote outside C"
+    if b_tiled and epi == 2:
+        full = from_tiles(C, c_rows, ncol)
+        assert (full[M:].view(np.int16) == CANARY).all(), "GEMM wrote a padding row of C"
+        C = torch.from_numpy(np.ascontiguousarray(full[:M]))
     # every row at small shapes, sampled rows keep the fp64 reference cheap at large ones
     if M * N * K <= (1 << 31):
         rows = np.arange(M)
@@ -386,8 +396,14 @@ def run_layer(cfg, b, w, x, seed, reps=1, keep_before=False):
         o = off[name]
         return ws[o:o + T * cols * 2].view(torch.uint16).reshape(T, cols)
 
-    return dict(y=y, k=k, v=v, q=view("q", nqd), o=view("o", nqd), x1=view("x1", H),
-                a=view("a", F), h2=view("h", H), **before)
+    def view_tiled(name, cols):  # a projection input: [ceil(T/16)][cols/32][16][32]
+        o = off[name]
+        T16 = -(-T // 16) * 16
+        t = ws[o:o + T16 * cols * 2].view(torch.int16).reshape(T16 // 16, cols // 32, 16, 32)
+        return t.permute(0, 2, 1, 3).reshape(T16, cols)[:T].contiguous().view(torch.uint16)
+
+    return dict(y=y, k=k, v=v, q=view("q", nqd), o=view_tiled("o", nqd), x1=view("x1", H),
+                a=view_tiled("a", F), h2=view_tiled("h", H), **before)
 
 
 def staged_attention(cfg, sub, x_sub, w, kp, vp, sub_rows):
@@ -752,15 +768,20 @@ def test_gemm_row_split(M, N, K, epi, m_main, main_cfg, tail_cfg, tail_ks):
     r = wl.f32_to_bf16_bits(rng.standard_normal((M, N), dtype=np.float32))
     ncol = N // 2 if epi == 2 else N
     lead = -(-2 * ncol // 8) * 8
-    buf16 = torch.full((lead + (M + 2) * ncol,), CANARY, dtype=torch.int16, device="cuda")
-    C = buf16.view(torch.uint16)[lead:lead + M * ncol].view(M, ncol)
+    c_rows = -(-M // 16) * 16 if epi == 2 else M  # the SwiGLU output in the tile layout
+    buf16 = torch.full((lead + (c_rows + 2) * ncol,), CANARY, dtype=torch.int16, device="cuda")
+    C = buf16.view(torch.uint16)[lead:lead + c_rows * ncol].view(c_rows, ncol)
     ws = ws_tensor(max(tail_ks * (M - m_main) * N * 4 if tail_ks > 1 else 0, 256))
     wt = np.ascontiguousarray(w.reshape(N // 16, 16, K // 32, 32).transpose(0, 2, 1, 3))
-    mx.mx_debug_gemm_rows(dev(a), dev(wt.reshape(-1)), C, dev(r) if epi == 1 else None, epi, N,
-                          m_main, main_cfg, tail_cfg, tail_ks, ws)
+    mx.mx_debug_gemm_rows(dev(to_tiles(a)), dev(wt.reshape(-1)), C, dev(r) if epi == 1 else None,
+                          epi, M, N, K, m_main, main_cfg, tail_cfg, tail_ks, ws)
     sync()
-    guard = torch.cat([buf16[:lead], buf16[lead + M * ncol:]]).cpu().numpy()
+    guard = torch.cat([buf16[:lead], buf16[lead + c_rows * ncol:]]).cpu().numpy()
     assert (guard == CANARY).all(), "GEMM wrote outside C"
+    if epi == 2:
+        full = from_tiles(C, c_rows, ncol)
+        assert (full[M:].view(np.int16) == CANARY).all(), "GEMM wrote a padding row of C"
+        C = torch.from_numpy(np.ascontiguousarray(full[:M]))
     acc = oracle.linear(wl.bf16_bits_to_f64(a), w)
     if epi == 1:
         exp = acc + wl.bf16_bits_to_f64(r)
@@ -805,7 +826,7 @@ def test_reduce_residual_rmsnorm(H, ks, split_row):
     x1_done = wl.f32_to_bf16_bits(rng.standard_normal((M, H), dtype=np.float32))
     g = wl.f32_to_bf16_bits(1 + 0.1 * rng.standard_normal(H, dtype=np.float32))
     x1 = dev(x1_done)
-    h = torch.empty((M, H), dtype=torch.uint16, device="cuda")
+    h = torch.empty((-(-M // 16) * 16 * H,), dtype=torch.uint16, device="cuda")  # tile layout
     mx.mx_debug_reduce_residual_rmsnorm(torch.from_numpy(planes).cuda(), ks, dev(r), x1, dev(g), h,
                                         eps=1e-5, split_row=split_row)
     sync()
@@ -819,7 +840,7 @@ def test_reduce_residual_rmsnorm(H, ks, split_row):
     bound = bf16_half_ulp(tail) + (ks + 1) * mag * 2.0 ** -24 + 1e-30
     assert (np.abs(tail - exact) <= bound).all(), "x1 off by more than one rounding"
     exp_h = oracle.rmsnorm(got_x1, wl.bf16_bits_to_f64(g), 1e-5)
-    assert_rows_close(bits_to_f64(h), exp_h, what="h")
+    assert_rows_close(wl.bf16_bits_to_f64(from_tiles(h, M, H)), exp_h, what="h")
 
 
 # ----------------------------------------------------------------------- row split in the layer
