@@ -247,11 +247,13 @@ mx_status mx_layer_step(const mx_batch* batch, const mx_layer_cfg* cfg, const vo
  *   off[0] h / h2 [T][H] (h2 overwrites h), off[1] q [T][nq][d] (post-RoPE),
  *   off[2] o [T][nq * d], off[3] x1 [T][H], off[4] a [T][F].
  * q and x1 are row-major.  h, o and a, the inputs of the projections, are in
- * the projection-input tile layout: a T x K matrix stored as
- * [ceil(T / 16)][K / 32][16][32], element (t, c) at
- *   (t / 16) * 16 * K + (c / 32) * 512 + (t % 16) * 32 + c % 32,
- * so that each 16-row x 32-column tile is one contiguous kilobyte (the GEMMs
- * copy whole kilobytes, as they do from the packed weights).
+ * the projection-input tile layout: a T x K matrix stored as ceil(T / 16) tile
+ * rows, each K / 32 tiles of 16 rows x 32 columns (one contiguous kilobyte)
+ * followed by one unused tile, element (t, c) at
+ *   (t / 16) * (16 * K + 512) + (c / 32) * 512 + (t % 16) * 32 + c % 32,
+ * ceil(T / 16) * (16 * K + 512) elements in all (the GEMMs copy whole
+ * kilobytes, as they do from the packed weights; the unused tile keeps tile
+ * rows off power-of-two distances).
  * (The new keys and values of the iteration are in the pools.) */
 mx_status mx_layer_workspace_offsets(const mx_batch* batch, const mx_layer_cfg* cfg,
                                      size_t off[5]);
@@ -306,11 +308,12 @@ mx_status mx_debug_gemm_config(int32_t M, int32_t N, int32_t K, const uint16_t* 
                                int32_t ksplit, void* ws, size_t ws_bytes, hipStream_t stream);
 /* The same with every operand in the layer step's own layout: B in the packed-weight
  * tile layout, element (n, k) at ((n / 16) * (K / 32) + k / 32) * 512 + (n % 16) * 32
- * + k % 32, i.e. 16 x 32 tiles of 1 KB ordered [N / 16][K / 32]; A in the same tile
- * layout over its M rows (ceil(M / 16) * 16 * K elements; the padding rows of the last
- * tile row are never read); C row-major [M][N], except the SwiGLU output, which is in
- * the tile layout too (ceil(M / 16) * 16 * N / 2 elements; the padding rows are never
- * written), as the layer's down projection reads it.  R row-major.  N % 16 == 0 and
+ * + k % 32, i.e. 16 x 32 tiles of 1 KB ordered [N / 16][K / 32]; A in the projection-input
+ * tile layout of mx_layer_workspace_offsets over its M rows (ceil(M / 16) * (16 * K + 512)
+ * elements; the padding rows of the last tile row and the unused tiles are never read);
+ * C row-major [M][N], except the SwiGLU output, which is in that tile layout too (with
+ * N / 2 columns; the padding rows and unused tiles are never written), as the layer's
+ * down projection reads it.  R row-major.  N % 16 == 0 and
  * K % 32 == 0 (else MX_ERR_UNSUPPORTED).  For tests and tuning sweeps of the layer's
  * own operand layout. */
 mx_status mx_debug_gemm_tiled(int32_t M, int32_t N, int32_t K, const uint16_t* A,
@@ -340,8 +343,8 @@ mx_status mx_debug_gemm_rows(int32_t M, int32_t N, int32_t K, const uint16_t* A,
  * (partial: ksplit fp32 planes [M - split_row][H], summed in plane order, then
  * the residual); rows r < split_row hold x1 already.  Then h[r] = RMSNorm(x1[r]) * g
  * for every row, from the rounded x1.  R, x1 [M][H] bf16 row-major, g [H] bf16, h
- * in the projection-input tile layout (mx_layer_workspace_offsets; ceil(M / 16) * 16
- * * H elements); H % 32 == 0 and H <= 8192.  For tests of the kernel the layer step
+ * in the projection-input tile layout (mx_layer_workspace_offsets; ceil(M / 16) *
+ * (16 * H + 512) elements); H % 32 == 0 and H <= 8192.  For tests of the kernel the layer step
  * runs. */
 mx_status mx_debug_reduce_residual_rmsnorm(const float* partial, int32_t ksplit, const uint16_t* R,
                                            uint16_t* x1, const uint16_t* g, uint16_t* h, int32_t M,

@@ -361,9 +361,11 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
   const uint16_t* dsrc[L];
   int64_t dstep[L];
-  // A element (m, k) at A + (m / 16) 16 lda + (m % 16) a_row + (k / 32) a_kstep
-  // + k % 32: row-major (lda, 32) or the activation tiles (32, 512), where the
-  // 16 rows of an instruction are one contiguous kilobyte
+  // A element (m, k) at A + (m / 16) a_blk + (m % 16) a_row + (k / 32) a_kstep
+  // + k % 32: row-major (16 lda, lda, 32) or the activation tiles
+  // (tile_row_pitch(lda), 32, 512), where the 16 rows of an instruction are one
+  // contiguous kilobyte
+  const int64_t a_blk = a.a_tiled ? tile_row_pitch(a.lda) : 16 * (int64_t)a.lda;
   const int a_row = a.a_tiled ? 32 : a.lda;
   const int a_kstep = a.a_tiled ? 512 : BKS;
 #pragma unroll
@@ -373,7 +375,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
     const int c = (lane & 3) ^ swz(row);
     if (row0 < BM) {
       const int m = min(m0 + row, a.M - 1);
-      dsrc[i] = a.A + (int64_t)(m >> 4) * 16 * a.lda + (int64_t)(m & 15) * a_row +
+      dsrc[i] = a.A + (int64_t)(m >> 4) * a_blk + (int64_t)(m & 15) * a_row +
                 (int64_t)(kbeg >> 5) * a_kstep + c * 8;
       dstep[i] = a_kstep;
     } else {
@@ -752,13 +754,13 @@ size_t plan_scratch(const Plan& p, int M, int N) {
 // The GEMM of rows [m0, M) of a: every row-indexed operand moves by m0 rows
 // (A, C, R and, for the QKV epilogue, the rotary table, the token slots and
 // q_out; the pools are addressed through the slots).  In the tile layout row
-// m0 starts a tile row only when m0 % 16 == 0, which the callers ensure; it
-// then sits m0 * K elements in, as in a row-major matrix.
+// m0 starts a tile row only when m0 % 16 == 0, which the callers ensure.
 GemmArgs rows_from(const GemmArgs& a, int m0) {
   GemmArgs t = a;
   t.M = a.M - m0;
-  t.A = a.A + (int64_t)m0 * a.lda;
-  if (t.C) t.C = a.C + (int64_t)m0 * a.ldc;
+  t.A = a.A + (a.a_tiled ? (int64_t)(m0 / 16) * tile_row_pitch(a.lda) : (int64_t)m0 * a.lda);
+  if (t.C)
+    t.C = a.C + (a.c_tiled ? (int64_t)(m0 / 16) * tile_row_pitch(a.ldc) : (int64_t)m0 * a.ldc);
   if (t.R) t.R = a.R + (int64_t)m0 * a.ldr;
   if (a.epilogue == EPI_QKV) {
     t.qkv.rope_cs = a.qkv.rope_cs + (int64_t)m0 * (a.qkv.head_dim / 2);

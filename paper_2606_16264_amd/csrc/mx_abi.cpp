@@ -331,14 +331,13 @@ Layout make_layout(int64_t R, int64_t T, int64_t n_pages, int64_t n_items, int64
   L.part_ml = o; o = align_up(o + n_parts * 8);
   if (c) {
     const int64_t H = c->hidden, F = c->ffn, nq = s->n_q_heads;
-    // h, o and a are projection inputs in the tile layout: whole 16-row tiles
-    const int64_t T16 = (T + 15) / 16 * 16;
+    // h, o and a are projection inputs in the tile layout (whole tile rows)
     L.rope_cs = o; o = align_up(o + T * (d / 2) * 8);
-    L.h = o; o = align_up(o + T16 * H * 2);
+    L.h = o; o = align_up(o + tile_elems(T, H) * 2);
     L.q = o; o = align_up(o + T * nq * d * 2);
-    L.o = o; o = align_up(o + T16 * nq * d * 2);
+    L.o = o; o = align_up(o + tile_elems(T, nq * d) * 2);
     L.x1 = o; o = align_up(o + T * H * 2);
-    L.a = o; o = align_up(o + T16 * F * 2);
+    L.a = o; o = align_up(o + tile_elems(T, F) * 2);
     L.scratch = o; o = align_up(o + scratch_floats * 4);
     L.scratch_floats = scratch_floats;
   }

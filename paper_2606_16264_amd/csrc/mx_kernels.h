@@ -53,7 +53,7 @@ hipError_t launch_prologue(const ReqDev* reqs, int R, int T, const int32_t* page
 
 // RMSNorm: out[t] = x[t] / sqrt(mean(x[t]^2) + eps) * g, bf16 in/out, fp32 math.
 // x is row-major [T][H]; out, a projection's input, is in the tile layout
-// (tile_index, ceil(T / 16) * 16 rows), H % 32 == 0.  The same holds for the
+// (tile_index, tile_elems(T, H) elements), H % 32 == 0.  The same holds for the
 // RMSNorm outputs of the two launches around it.
 hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* g, uint16_t* out, int T, int H,
                           float eps, hipStream_t stream);

@@ -57,25 +57,39 @@ def bits_to_f64(t) -> np.ndarray:
     return wl.bf16_bits_to_f64(host_bits(t))
 
 
+def tile_elems(M, K) -> int:
+    """Elements of an M x K matrix in the projection-input tile layout: ceil(M/16)
+    tile rows of K/32 one-kilobyte tiles plus one unused tile each."""
+    return -(-M // 16) * (16 * K + 512)
+
+
 def to_tiles(a, pad=0x7FC0) -> np.ndarray:
-    """[M][K] uint16 -> the projection-input tile layout [ceil(M/16)][K/32][16][32]
-    (flat); the padding rows of the last tile row are filled with `pad` (a NaN:
-    a kernel that read them would show it)."""
+    """[M][K] uint16 -> the projection-input tile layout (flat): tile rows of
+    [K/32 + 1][16][32], the last tile of each unused; the padding rows of the
+    last tile row and the unused tiles are filled with `pad` (a NaN: a kernel
+    that read them would show it)."""
     a = np.asarray(a, np.uint16)
     M, K = a.shape
     M16 = -(-M // 16) * 16
-    p = np.full((M16, K), pad, np.uint16)
-    p[:M] = a
-    return np.ascontiguousarray(p.reshape(M16 // 16, 16, K // 32, 32).transpose(0, 2, 1, 3)).reshape(-1)
+    p = np.full((M16, K + 32), pad, np.uint16)
+    p[:M, :K] = a
+    return np.ascontiguousarray(p.reshape(M16 // 16, 16, K // 32 + 1, 32).transpose(0, 2, 1, 3)).reshape(-1)
 
 
 def from_tiles(t, M, K) -> np.ndarray:
-    """The inverse of to_tiles for M rows (a multiple of 16 when the padding
-    rows are wanted too): tile layout (device tensor or array) -> [M][K] uint16."""
+    """The inverse of to_tiles: tile layout (device tensor or array) -> [M][K] uint16."""
     a = (host_bits(t) if hasattr(t, "cpu") else np.asarray(t).view(np.uint16)).reshape(-1)
     M16 = -(-M // 16) * 16
-    a = a[:M16 * K].reshape(M16 // 16, K // 32, 16, 32).transpose(0, 2, 1, 3).reshape(M16, K)
-    return np.ascontiguousarray(a[:M])
+    a = a[:tile_elems(M, K)].reshape(M16 // 16, K // 32 + 1, 16, 32)[:, :K // 32]
+    return np.ascontiguousarray(a.transpose(0, 2, 1, 3).reshape(M16, K)[:M])
+
+
+def tiles_unwritten(t, M, K) -> np.ndarray:
+    """The elements of a tile-layout buffer that hold no matrix element (padding
+    rows, unused tiles), as uint16."""
+    a = (host_bits(t) if hasattr(t, "cpu") else np.asarray(t).view(np.uint16)).reshape(-1)
+    real = to_tiles(np.ones((M, K), np.uint16), pad=0).astype(bool)
+    return a[:len(real)][~real]
 
 
 def sample_rows(b: wl.Batch, rng, n_decode=16, n_prefill_random=62):

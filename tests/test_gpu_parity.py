@@ -15,7 +15,7 @@ import oracle
 import workload as wl
 from helpers import (TOL, assert_rows_close, bf16_half_ulp, bits_to_f64, branch_err_rows, dev,
                      from_tiles, host_bits, mx_batch, mx_cfg, mx_shape, rel_err_rows,
-                     sample_rows, to_tiles, truncated_subbatch)
+                     sample_rows, tile_elems, tiles_unwritten, to_tiles, truncated_subbatch)
 
 pytestmark = pytest.mark.gpu
 
@@ -278,26 +278,28 @@ def gemm_case(M, N, K, epi, tile_cfg=-1, ksplit=0, b_tiled=False):
     need = mx.mx_debug_gemm_ws_bytes(M, N, K) if tile_cfg < 0 else \
         (ksplit * M * N * 4 if ksplit > 1 else 0)
     ws = ws_tensor(max(need, 256))
+    n_c = M * ncol
     if b_tiled:
-        # the layer's layouts: A (NaN padding rows, never read) and the SwiGLU
-        # output in the tile layout, over whole 16-row tiles
+        # the layer's layouts: A (NaN in its padding rows and unused tiles, never
+        # read) and the SwiGLU output in the tile layout
         wt = np.ascontiguousarray(w.reshape(N // 16, 16, K // 32, 32).transpose(0, 2, 1, 3))
-        c_rows = -(-M // 16) * 16 if epi == 2 else M
-        buf16 = torch.full((lead + (c_rows + 2) * ncol,), CANARY, dtype=torch.int16, device="cuda")
-        C = buf16.view(torch.uint16)[lead:lead + c_rows * ncol].view(c_rows, ncol)
+        n_c = tile_elems(M, ncol) if epi == 2 else M * ncol
+        buf16 = torch.full((lead + n_c + 2 * ncol,), CANARY, dtype=torch.int16, device="cuda")
+        C = buf16.view(torch.uint16)[lead:lead + n_c]
+        if epi != 2:
+            C = C.view(M, ncol)
         mx.mx_debug_gemm(dev(to_tiles(a)), dev(wt.reshape(-1)), C, dev(r) if epi == 1 else None,
                          epi, ws, tile_cfg=tile_cfg, ksplit=ksplit, tiled=True, M=M, N=N, K=K)
     else:
-        c_rows = M
         mx.mx_debug_gemm(dev(a), dev(w), C, dev(r) if epi == 1 else None, epi, ws,
                          tile_cfg=tile_cfg, ksplit=ksplit)
     sync()
-    guard = torch.cat([buf16[:lead], buf16[lead + c_rows * ncol:]]).cpu().numpy()
+    guard = torch.cat([buf16[:lead], buf16[lead + n_c:]]).cpu().numpy()
     assert (guard == CANARY).all(), "GEMM wrote outside C"
     if b_tiled and epi == 2:
-        full = from_tiles(C, c_rows, ncol)
-        assert (full[M:].view(np.int16) == CANARY).all(), "GEMM wrote a padding row of C"
-        C = torch.from_numpy(np.ascontiguousarray(full[:M]))
+        assert (tiles_unwritten(C, M, ncol).view(np.int16) == CANARY).all(), \
+            "GEMM wrote a padding row or an unused tile of C"
+        C = torch.from_numpy(from_tiles(C, M, ncol))
     # every row at small shapes, sampled rows keep the fp64 reference cheap at large ones
     if M * N * K <= (1 << 31):
         rows = np.arange(M)
@@ -396,10 +398,11 @@ def run_layer(cfg, b, w, x, seed, reps=1, keep_before=False):
         o = off[name]
         return ws[o:o + T * cols * 2].view(torch.uint16).reshape(T, cols)
 
-    def view_tiled(name, cols):  # a projection input: [ceil(T/16)][cols/32][16][32]
+    def view_tiled(name, cols):  # a projection input: tile rows of [cols/32 + 1][16][32]
         o = off[name]
         T16 = -(-T // 16) * 16
-        t = ws[o:o + T16 * cols * 2].view(torch.int16).reshape(T16 // 16, cols // 32, 16, 32)
+        t = ws[o:o + tile_elems(T, cols) * 2].view(torch.int16)
+        t = t.reshape(T16 // 16, cols // 32 + 1, 16, 32)[:, :cols // 32]
         return t.permute(0, 2, 1, 3).reshape(T16, cols)[:T].contiguous().view(torch.uint16)
 
     return dict(y=y, k=k, v=v, q=view("q", nqd), o=view_tiled("o", nqd), x1=view("x1", H),
@@ -768,20 +771,22 @@ def test_gemm_row_split(M, N, K, epi, m_main, main_cfg, tail_cfg, tail_ks):
     r = wl.f32_to_bf16_bits(rng.standard_normal((M, N), dtype=np.float32))
     ncol = N // 2 if epi == 2 else N
     lead = -(-2 * ncol // 8) * 8
-    c_rows = -(-M // 16) * 16 if epi == 2 else M  # the SwiGLU output in the tile layout
-    buf16 = torch.full((lead + (c_rows + 2) * ncol,), CANARY, dtype=torch.int16, device="cuda")
-    C = buf16.view(torch.uint16)[lead:lead + c_rows * ncol].view(c_rows, ncol)
+    n_c = tile_elems(M, ncol) if epi == 2 else M * ncol  # the SwiGLU output in the tile layout
+    buf16 = torch.full((lead + n_c + 2 * ncol,), CANARY, dtype=torch.int16, device="cuda")
+    C = buf16.view(torch.uint16)[lead:lead + n_c]
+    if epi != 2:
+        C = C.view(M, ncol)
     ws = ws_tensor(max(tail_ks * (M - m_main) * N * 4 if tail_ks > 1 else 0, 256))
     wt = np.ascontiguousarray(w.reshape(N // 16, 16, K // 32, 32).transpose(0, 2, 1, 3))
     mx.mx_debug_gemm_rows(dev(to_tiles(a)), dev(wt.reshape(-1)), C, dev(r) if epi == 1 else None,
                           epi, M, N, K, m_main, main_cfg, tail_cfg, tail_ks, ws)
     sync()
-    guard = torch.cat([buf16[:lead], buf16[lead + c_rows * ncol:]]).cpu().numpy()
+    guard = torch.cat([buf16[:lead], buf16[lead + n_c:]]).cpu().numpy()
     assert (guard == CANARY).all(), "GEMM wrote outside C"
     if epi == 2:
-        full = from_tiles(C, c_rows, ncol)
-        assert (full[M:].view(np.int16) == CANARY).all(), "GEMM wrote a padding row of C"
-        C = torch.from_numpy(np.ascontiguousarray(full[:M]))
+        assert (tiles_unwritten(C, M, ncol).view(np.int16) == CANARY).all(), \
+            "GEMM wrote a padding row or an unused tile of C"
+        C = torch.from_numpy(from_tiles(C, M, ncol))
     acc = oracle.linear(wl.bf16_bits_to_f64(a), w)
     if epi == 1:
         exp = acc + wl.bf16_bits_to_f64(r)
@@ -826,7 +831,7 @@ def test_reduce_residual_rmsnorm(H, ks, split_row):
     x1_done = wl.f32_to_bf16_bits(rng.standard_normal((M, H), dtype=np.float32))
     g = wl.f32_to_bf16_bits(1 + 0.1 * rng.standard_normal(H, dtype=np.float32))
     x1 = dev(x1_done)
-    h = torch.empty((-(-M // 16) * 16 * H,), dtype=torch.uint16, device="cuda")  # tile layout
+    h = torch.empty((tile_elems(M, H),), dtype=torch.uint16, device="cuda")  # tile layout
     mx.mx_debug_reduce_residual_rmsnorm(torch.from_numpy(planes).cuda(), ks, dev(r), x1, dev(g), h,
                                         eps=1e-5, split_row=split_row)
     sync()
