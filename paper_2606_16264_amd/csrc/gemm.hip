@@ -273,50 +273,128 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MB][NB], int M,
   }
 }
 
-// Plain or residual epilogue of one wave's block (rows r0.., columns c0..),
-// per 32-row block in three phases like the QKV epilogue: every residual read
-// (unconditional, indices clamped into range), the sums rounded to bf16, then
-// the stores.  R must not overlap C.
+// Output staging of the plain, residual and SwiGLU epilogues.  The
+// matrix-core layout gives a lane one column of four rows per 32 x 32 block, so
+// writing it out directly takes one 2-byte store (and one 2-byte residual load)
+// per element: 64-128 store instructions per lane per tile, and a CU issues
+// about one vector memory instruction per 16 cycles, so the epilogue of a
+// 256 x 256 tile cost 5-15 us.  Instead each wave stages one 32-row block of
+// its fp32 results at a time in LDS (the operand ring, free once the main loop
+// is done) and reads it back as runs of 8 consecutive columns of one row: a
+// lane then moves 8 outputs, and 8 residuals, per 16-byte access.  The sums
+// and roundings are the same as unstaged.  Staged rows are padded by 4 floats
+// so that the rows 4 apart, which one write instruction covers, fall on other
+// banks.
+constexpr int kStageRow = 64 + 4;              // floats per staged row (64 columns)
+constexpr int kStageFloats = 32 * kStageRow;   // one wave's 32-row block
+constexpr int kStageRowSw = 32 + 4;            // SwiGLU: 32 output columns per wave
+
+// Plain or residual epilogue of one wave's block (rows r0.., columns c0..,
+// 64 columns).  Every residual read (indices clamped into range) is issued
+// first, then per 32-row block the staging, the sums rounded to bf16 and the
+// stores.  Rows whose stride is not a multiple of 8 elements, and the columns
+// at the N edge, take 2-byte accesses.  R must not overlap C.
 template <int MB, int NB, bool RESIDUAL>
 __device__ __forceinline__ void store_epilogue(const f32x16 (&acc)[MB][NB], int M, int N, int r0,
                                                int c0, int lane, const uint16_t* __restrict__ R,
-                                               int ldr, uint16_t* __restrict__ C, int ldc) {
+                                               int ldr, uint16_t* __restrict__ C, int ldc,
+                                               MX_LDS float* st) {
+  static_assert(NB == 2, "the staging holds 64 columns per wave");
   const int ccol = lane & 31, crow = 4 * (lane >> 5);
+  const int rq = lane >> 3, col = c0 + 8 * (lane & 7);  // read-back: rows rq + 8 q, 8 columns
+  const bool vec = ldc % 8 == 0 && (!RESIDUAL || ldr % 8 == 0) && col + 8 <= N;
+  u32x4 res[MB][4];
 #pragma unroll
-  for (int i = 0; i < MB; i++) {
-    float res[16][NB];
+  for (int i = 0; i < MB; i++)
 #pragma unroll
-    for (int r = 0; r < 16; r++)
+    for (int q = 0; q < 4; q++) {
+      res[i][q] = u32x4{0, 0, 0, 0};
+      if constexpr (RESIDUAL) {
+        const uint16_t* rp = R + (int64_t)min(r0 + i * 32 + rq + 8 * q, M - 1) * ldr;
+        if (vec) {
+          res[i][q] = *reinterpret_cast<const u32x4*>(rp + col);
+        } else {
 #pragma unroll
-      for (int j = 0; j < NB; j++) {
-        res[r][j] = 0.f;
-        if constexpr (RESIDUAL) {
-          const int row = min(r0 + i * 32 + 8 * (r >> 2) + crow + (r & 3), M - 1);
-          const int colg = min(c0 + j * 32 + ccol, N - 1);
-          res[r][j] = bf16_to_f32(R[(int64_t)row * ldr + colg]);
+          for (int e = 0; e < 8; e += 2) {
+            const uint32_t lo = rp[min(col + e, N - 1)], hi = rp[min(col + e + 1, N - 1)];
+            res[i][q][e / 2] = lo | (hi << 16);
+          }
         }
       }
-    __builtin_amdgcn_sched_barrier(0);
-    // (pinned: otherwise the sums sink into the bounds-checked store blocks,
-    // behind earlier stores)
-    uint32_t out[16][NB];
+    }
+#pragma unroll
+  for (int i = 0; i < MB; i++) {
 #pragma unroll
     for (int r = 0; r < 16; r++)
 #pragma unroll
-      for (int j = 0; j < NB; j++) {
-        out[r][j] = f32_to_bf16(acc[i][j][r] + res[r][j]);
-        asm volatile("" : "+v"(out[r][j]));
-      }
-    __builtin_amdgcn_sched_barrier(0);
+      for (int j = 0; j < NB; j++)
+        st[(8 * (r >> 2) + crow + (r & 3)) * kStageRow + j * 32 + ccol] = acc[i][j][r];
+    lgkm_wait<0>();  // (and no access below moves above the staging)
+    u32x4 out[4];
 #pragma unroll
-    for (int r = 0; r < 16; r++) {
-      const int row = r0 + i * 32 + 8 * (r >> 2) + crow + (r & 3);
+    for (int q = 0; q < 4; q++) {
+      const MX_LDS f32x4* sp =
+          reinterpret_cast<const MX_LDS f32x4*>(st + (rq + 8 * q) * kStageRow + 8 * (lane & 7));
+      const f32x4 lo = sp[0], hi = sp[1];
+#pragma unroll
+      for (int e = 0; e < 2; e++) {
+        out[q][e] = pack_bf16x2(lo[2 * e] + __uint_as_float(res[i][q][e] << 16),
+                                lo[2 * e + 1] + __uint_as_float(res[i][q][e] & 0xFFFF0000u));
+        out[q][2 + e] = pack_bf16x2(hi[2 * e] + __uint_as_float(res[i][q][2 + e] << 16),
+                                    hi[2 * e + 1] + __uint_as_float(res[i][q][2 + e] & 0xFFFF0000u));
+      }
+    }
+    lgkm_wait<0>();  // the block is read back before the next one is staged
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+      const int row = r0 + i * 32 + rq + 8 * q;
+      if (row >= M || col >= N) continue;
+      uint16_t* cp = C + (int64_t)row * ldc + col;
+      if (vec) {
+        *reinterpret_cast<u32x4*>(cp) = out[q];
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; e++)
+          if (col + e < N) cp[e] = (uint16_t)(out[q][e / 2] >> (16 * (e & 1)));
+      }
+    }
+  }
+}
+
+// SwiGLU epilogue of one wave's block: packed columns c0.. hold 32-column
+// blocks of gate and up of the same 32 features; the 32 outputs (columns
+// c0 / 2 ..) go to C row-major or, c_tiled, in the projection-input tile
+// layout, through the same staging as above (ldc a multiple of 32).
+template <int MB, int NB>
+__device__ __forceinline__ void swiglu_epilogue(const f32x16 (&acc)[MB][NB], int M, int N, int r0,
+                                                int c0, int lane, uint16_t* __restrict__ C,
+                                                int ldc, bool c_tiled, MX_LDS float* st) {
+  static_assert(NB == 2, "one gate/up pair per wave");
+  const int ccol = lane & 31, crow = 4 * (lane >> 5);
+  const int rq = lane >> 2, col = c0 / 2 + 8 * (lane & 3);  // read-back: rows rq + 16 q
+  if (c0 >= N) return;  // (wave-uniform)
+#pragma unroll
+  for (int i = 0; i < MB; i++) {
+#pragma unroll
+    for (int r = 0; r < 16; r++)
+      st[(8 * (r >> 2) + crow + (r & 3)) * kStageRowSw + ccol] = silu(acc[i][0][r]) * acc[i][1][r];
+    lgkm_wait<0>();
+    u32x4 out[2];
+#pragma unroll
+    for (int q = 0; q < 2; q++) {
+      const MX_LDS f32x4* sp =
+          reinterpret_cast<const MX_LDS f32x4*>(st + (rq + 16 * q) * kStageRowSw + 8 * (lane & 3));
+      const f32x4 lo = sp[0], hi = sp[1];
+      out[q] = u32x4{pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]), pack_bf16x2(hi[0], hi[1]),
+                     pack_bf16x2(hi[2], hi[3])};
+    }
+    lgkm_wait<0>();
+#pragma unroll
+    for (int q = 0; q < 2; q++) {
+      const int row = r0 + i * 32 + rq + 16 * q;
       if (row >= M) continue;
-#pragma unroll
-      for (int j = 0; j < NB; j++) {
-        const int colg = c0 + j * 32 + ccol;
-        if (colg < N) C[(int64_t)row * ldc + colg] = (uint16_t)out[r][j];
-      }
+      *reinterpret_cast<u32x4*>(C + (c_tiled ? tile_index(row, col, ldc) : (int64_t)row * ldc + col)) =
+          out[q];
     }
   }
 }
@@ -506,9 +584,17 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
                          e.tok_slot, e.q_out, e.k_pool, e.v_pool, e.nq, e.nkv, e.head_dim);
     return;
   }
-  if constexpr (!SPLIT && (EPI == EPI_STORE || EPI == EPI_RESIDUAL)) {
-    store_epilogue<MB, NB, EPI == EPI_RESIDUAL>(acc, a.M, a.N, m0 + wave_m * WM, n0 + wave_n * WN,
-                                                lane, a.R, a.ldr, a.C, a.ldc);
+  if constexpr (!SPLIT && (EPI == EPI_STORE || EPI == EPI_RESIDUAL || EPI == EPI_SWIGLU)) {
+    static_assert(NWAVES * kStageFloats * 4 <= NS * STAGE, "the staging does not fit the ring");
+    wg_barrier();  // every wave is done reading the ring
+    MX_LDS float* st = reinterpret_cast<MX_LDS float*>((MX_LDS char*)smem) + wave_s * kStageFloats;
+    if constexpr (EPI == EPI_SWIGLU)
+      swiglu_epilogue<MB, NB>(acc, a.M, a.N, m0 + wave_m * WM, n0 + wave_n * WN, lane, a.C, a.ldc,
+                              a.c_tiled != 0, st);
+    else
+      store_epilogue<MB, NB, EPI == EPI_RESIDUAL>(acc, a.M, a.N, m0 + wave_m * WM,
+                                                  n0 + wave_n * WN, lane, a.R, a.ldr, a.C, a.ldc,
+                                                  st);
     return;
   }
   const int ccol = lane & 31, crow = 4 * (lane >> 5);
@@ -523,16 +609,6 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
         for (int j = 0; j < NB; j++) {
           const int colg = n0 + wave_n * WN + j * 32 + ccol;
           if (colg < a.N) a.partial[((int64_t)kz * a.M + row) * a.N + colg] = acc[i][j][r];
-        }
-      } else if constexpr (EPI == EPI_SWIGLU) {
-#pragma unroll
-        for (int jp = 0; jp < NB / 2; jp++) {
-          const int colg = n0 + wave_n * WN + jp * 64;  // first packed column of the pair
-          if (colg >= a.N) continue;
-          const float gt = acc[i][2 * jp][r], up = acc[i][2 * jp + 1][r];
-          const int col = colg / 2 + ccol;
-          a.C[a.c_tiled ? tile_index(row, col, a.ldc) : (int64_t)row * a.ldc + col] =
-              f32_to_bf16(silu(gt) * up);
         }
       }
     }
