@@ -133,20 +133,29 @@ __device__ __forceinline__ int rope_index(int t, int c, int hd) {
   return t * (hd / 2) + 32 * (within / 64) + (within % 32);
 }
 
-// QKV epilogue of one wave's block (rows r0.., columns c0..).  q and k heads
-// are rotated and rounded once; q goes to q_out, k to its pool slot.  A v head
-// goes to the transposed value pages [page][kv head][dim][16 slots], where one
-// dim of consecutive slots is a contiguous run: when rows 8 jj .. 8 jj + 7 of a
-// 32-row block hold tokens in eight consecutive slots starting at a multiple
-// of 8, the lane pair (l, l ^ 32) trades halves so that each lane holds the
-// eight tokens of one dim and writes them with a single 16-byte store;
-// otherwise every value is stored on its own.
-// Per 32-row block, in three phases: every read (KV slots, rotary cos/sin;
-// unconditional, indices clamped into range), then all arithmetic (rotated
-// values, destination offsets, the traded value runs) in straight-line code,
-// then the stores, which use no register a load is still filling.  (A wait on
-// a load also waits for every store issued before it, so loads and stores
-// interleaved would cost one memory round trip per element.)
+// QKV epilogue of one wave's block (rows r0.., the 64 columns c0..: one
+// 64-column group of one head, i.e. the two 32-column halves of its rotary
+// pairs).  q and k heads are rotated and rounded once; q goes to q_out, k to
+// its pool slot ([d / 32][16 slots][32] pages), v to the transposed value
+// pages [page][kv head][dim][16 slots].  Per 32-row block the rounded values
+// are staged in LDS, like the outputs of the other epilogues, and written in
+// 16-byte runs: q and k read back token-major (8 consecutive dims of one
+// token per run), v dim-major, 8 consecutive tokens of one dim per run
+// wherever they fill 8 consecutive slots starting at a multiple of 8, in any
+// position in the block (a chunk's start need not line up with the rows); the
+// tokens left over are stored one value at a time.  Each block first issues
+// its reads (this lane's token slot, the rotary cos/sin), so that no wait on
+// them also waits for a store (one counter tracks both).
+constexpr int kQkRow = 64 + 8;  // bf16 per staged token row (q, k)
+constexpr int kVRow = 32 + 8;   // bf16 per staged dim row (v)
+constexpr int kQkvStageHalves = 64 * kVRow > 32 * kQkRow ? 64 * kVRow : 32 * kQkRow;
+
+__device__ __forceinline__ int64_t lane_slot(int64_t s, int l) {  // s of lane l (uniform l)
+  const int lo = __builtin_amdgcn_readlane((int)(uint32_t)s, l);
+  const int hi = __builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)s >> 32), l);
+  return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
 template <int MB, int NB>
 __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MB][NB], int M, int N, int r0,
                                              int c0, int lane, const float2* __restrict__ rope_cs,
@@ -154,121 +163,106 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MB][NB], int M,
                                              uint16_t* __restrict__ q_out,
                                              uint16_t* __restrict__ k_pool,
                                              uint16_t* __restrict__ v_pool, int nq, int nkv,
-                                             int hd) {
-  constexpr int NP = NB / 2;  // 64-column groups (rotary pairs) per lane
+                                             int hd, MX_LDS uint16_t* st) {
+  static_assert(NB == 2, "one 64-column group per wave");
+  if (c0 >= N) return;  // (wave-uniform)
   const int ccol = lane & 31, crow = 4 * (lane >> 5);
-  const bool upper = lane >= 32;
+  const int head = c0 / hd, within0 = c0 % hd;
+  const bool is_v = head >= nq + nkv, is_q = head < nq;
+  // dims of the low and high 32-column blocks (q / k: the packed rotary halves)
+  const int d_lo = is_v ? within0 : 32 * (within0 / 64);
+  const int d_hi = is_v ? within0 + 32 : d_lo + hd / 2;
 #pragma unroll
   for (int i = 0; i < MB; i++) {
-    // 1. reads: the KV slots of this lane's rows, the (cos, sin) of its pairs
-    int64_t slot[4][4];
-    float2 cs[4][NP][4];
+    const int rb = r0 + i * 32;
+    // 1. reads: the slot of token rb + lane % 32, the (cos, sin) of this lane's rows
+    const int64_t myslot = tok_slot[min(rb + (lane & 31), M - 1)];
+    float2 cs[16];
+    if (!is_v) {
 #pragma unroll
-    for (int jj = 0; jj < 4; jj++)
-#pragma unroll
-      for (int ii = 0; ii < 4; ii++) {
-        const int row = min(r0 + i * 32 + 8 * jj + crow + ii, M - 1);
-        slot[jj][ii] = tok_slot[row];
-#pragma unroll
-        for (int jp = 0; jp < NP; jp++)
-          cs[jj][jp][ii] = rope_cs[rope_index(row, c0 + jp * 64 + ccol, hd)];
-      }
-    __builtin_amdgcn_sched_barrier(0);
-    // 2. arithmetic: what goes where
-    uint32_t val[4][NP][4];  // bf16 pair (low: dim d_lo or c, high: d_lo + hd/2 or c + 32)
-    int64_t dst[4][NP][4];   // element offset of the low value in its buffer
-    u32x4 run[4][NP];        // the traded value run of a v head (when run8)
-    bool run8[4];
-    int64_t run_slot[4];     // slot of row 8 jj (where a run starts)
-#pragma unroll
-    for (int jj = 0; jj < 4; jj++) {
-      const int rbase = r0 + i * 32 + 8 * jj;
-      bool own = true;
-#pragma unroll
-      for (int ii = 1; ii < 4; ii++) own = own && slot[jj][ii] == slot[jj][0] + ii;
-      const int64_t other = __shfl_xor(slot[jj][0], 32);
-      const bool other_own = __shfl_xor((int)own, 32) != 0;
-      const int64_t s_lo = upper ? other : slot[jj][0], s_hi = upper ? slot[jj][0] : other;
-      run8[jj] = rbase + 7 < M && own && other_own && (s_lo & 7) == 0 && s_hi == s_lo + 4;
-      run_slot[jj] = s_lo;
-#pragma unroll
-      for (int jp = 0; jp < NP; jp++) {
-        const int colg = c0 + jp * 64 + ccol;
-        const int head = colg / hd, within = colg % hd;
-        const int d_lo = 32 * (within / 64) + (within % 32);
-        float lo[4], hi[4];
-#pragma unroll
-        for (int ii = 0; ii < 4; ii++) {
-          lo[ii] = acc[i][2 * jp][4 * jj + ii];
-          hi[ii] = acc[i][2 * jp + 1][4 * jj + ii];
-        }
-        // lower lane: dim c, tokens 0..3 (own) + 4..7 (partner);
-        // upper lane: dim c + 32, tokens 0..3 (partner) + 4..7 (own)
-        float tok[8];
-#pragma unroll
-        for (int ii = 0; ii < 4; ii++) {
-          const float got = __shfl_xor(upper ? lo[ii] : hi[ii], 32);
-          tok[ii] = upper ? got : lo[ii];
-          tok[4 + ii] = upper ? hi[ii] : got;
-        }
-#pragma unroll
-        for (int h = 0; h < 4; h++) run[jj][jp][h] = pack_bf16x2(tok[2 * h], tok[2 * h + 1]);
-        asm volatile("" : "+v"(run[jj][jp]));
-#pragma unroll
-        for (int ii = 0; ii < 4; ii++) {
-          const int t = rbase + crow + ii;
-          const int64_t sl = slot[jj][ii];
-          if (head < nq + nkv) {
-            const float2 c = cs[jj][jp][ii];
-            val[jj][jp][ii] = pack_bf16x2(lo[ii] * c.x - hi[ii] * c.y, hi[ii] * c.x + lo[ii] * c.y);
-            dst[jj][jp][ii] = head < nq ? ((int64_t)t * nq + head) * hd + d_lo
-                                        : ((sl >> 4) * nkv + (head - nq)) * 16 * hd +
-                                              (d_lo >> 5) * 512 + (sl & 15) * 32 + (d_lo & 31);
-          } else {
-            val[jj][jp][ii] = pack_bf16x2(lo[ii], hi[ii]);
-            dst[jj][jp][ii] = (((sl >> 4) * nkv + (head - nq - nkv)) * hd + within) * 16 + (sl & 15);
-          }
-          // (pinned: otherwise this sinks into the bounds-checked store blocks)
-          asm volatile("" : "+v"(val[jj][jp][ii]), "+v"(dst[jj][jp][ii]));
-        }
+      for (int r = 0; r < 16; r++) {
+        const int row = min(rb + 8 * (r >> 2) + crow + (r & 3), M - 1);
+        cs[r] = rope_cs[(int64_t)row * (hd / 2) + d_lo + ccol];
       }
     }
     __builtin_amdgcn_sched_barrier(0);
-    // 3. stores
+    if (!is_v) {
+      // 2. rotate, round, stage token-major: [token][low 32 dims, high 32 dims]
 #pragma unroll
-    for (int jj = 0; jj < 4; jj++) {
-      const int rbase = r0 + i * 32 + 8 * jj;
-      if (rbase >= M) continue;
-#pragma unroll
-      for (int jp = 0; jp < NP; jp++) {
-        const int cb = c0 + jp * 64;
-        if (cb >= N) continue;
-        const int head = (cb + ccol) / hd;
-        if (head >= nq + nkv && run8[jj]) {
-          // (every cross-lane exchange happens above, with all lanes active)
-          const int64_t s0 = run_slot[jj];
-          const int within = (cb + ccol) % hd + (upper ? 32 : 0);
-          *reinterpret_cast<u32x4*>(v_pool + (((s0 >> 4) * nkv + (head - nq - nkv)) * hd + within) * 16 +
-                                    (s0 & 15)) = run[jj][jp];
-          continue;
-        }
-#pragma unroll
-        for (int ii = 0; ii < 4; ii++) {
-          if (rbase + crow + ii >= M) continue;
-          const uint16_t vlo = (uint16_t)(val[jj][jp][ii] & 0xFFFFu);
-          const uint16_t vhi = (uint16_t)(val[jj][jp][ii] >> 16);
-          if (head < nq) {
-            q_out[dst[jj][jp][ii]] = vlo;
-            q_out[dst[jj][jp][ii] + hd / 2] = vhi;
-          } else if (head < nq + nkv) {
-            k_pool[dst[jj][jp][ii]] = vlo;
-            k_pool[dst[jj][jp][ii] + 8 * hd] = vhi;  // dim d_lo + hd/2: hd/64 blocks on
-          } else {
-            v_pool[dst[jj][jp][ii]] = vlo;
-            v_pool[dst[jj][jp][ii] + 32 * 16] = vhi;
-          }
-        }
+      for (int r = 0; r < 16; r++) {
+        const int t = 8 * (r >> 2) + crow + (r & 3);
+        const float lo = acc[i][0][r], hi = acc[i][1][r];
+        st[t * kQkRow + ccol] = f32_to_bf16(lo * cs[r].x - hi * cs[r].y);
+        st[t * kQkRow + 32 + ccol] = f32_to_bf16(hi * cs[r].x + lo * cs[r].y);
       }
+      lgkm_wait<0>();  // (and no access below moves above the staging)
+      // 3. read back token (lane / 8) + 8 q, dims 8 (lane % 8) .. + 7 of the 64
+      u32x4 out[4];
+#pragma unroll
+      for (int q = 0; q < 4; q++)
+        out[q] = *reinterpret_cast<const MX_LDS u32x4*>(st + ((lane >> 3) + 8 * q) * kQkRow +
+                                                        8 * (lane & 7));
+      lgkm_wait<0>();  // the block is read back before the next one is staged
+      const int p = lane & 7;
+      const int dim = (p < 4 ? d_lo : d_hi) + 8 * (p & 3);
+#pragma unroll
+      for (int q = 0; q < 4; q++) {
+        const int t = (lane >> 3) + 8 * q;
+        const int64_t slot = __shfl(myslot, t);  // (every lane takes part)
+        if (rb + t >= M) continue;
+        uint16_t* dst;
+        if (is_q) {
+          dst = q_out + ((int64_t)(rb + t) * nq + head) * hd + dim;
+        } else {
+          dst = k_pool + ((slot >> 4) * nkv + (head - nq)) * 16 * hd + (dim >> 5) * 512 +
+                (slot & 15) * 32 + (dim & 31);
+        }
+        *reinterpret_cast<u32x4*>(dst) = out[q];
+      }
+    } else {
+      // 2. stage dim-major: [dim (low 32, high 32)][token]; this lane's four
+      // consecutive tokens of a row group are one 8-byte write
+#pragma unroll
+      for (int k = 0; k < 4; k++)
+#pragma unroll
+        for (int j = 0; j < 2; j++) {
+          u32x2 w;
+          w[0] = pack_bf16x2(acc[i][j][4 * k], acc[i][j][4 * k + 1]);
+          w[1] = pack_bf16x2(acc[i][j][4 * k + 2], acc[i][j][4 * k + 3]);
+          *reinterpret_cast<MX_LDS u32x2*>(st + (32 * j + ccol) * kVRow + 8 * k + crow) = w;
+        }
+      lgkm_wait<0>();
+      // runs: token t starts one where its slot is a multiple of 8 and token
+      // t + 7 holds the slot 7 further (then the eight tokens are consecutive
+      // positions of one request: a page belongs to one request)
+      const int tl = lane & 31;
+      const int64_t s7 = __shfl(myslot, min(tl + 7, 31));
+      const bool start = tl + 7 < 32 && rb + tl + 7 < M && (myslot & 7) == 0 && s7 == myslot + 7;
+      uint32_t starts = (uint32_t)__ballot(start);
+      const int nrow = min(32, M - rb);
+      uint32_t single = nrow >= 32 ? ~0u : ((1u << nrow) - 1u);
+      for (uint32_t m = starts; m; m &= m - 1) single &= ~(0xFFu << __builtin_ctz(m));
+      const int vh = head - nq - nkv;
+      const int dim = within0 + lane;  // lane l writes dim row l of the staging
+      const MX_LDS uint16_t* srow = st + lane * kVRow;
+      for (; starts; starts &= starts - 1) {
+        const int t = __builtin_ctz(starts);
+        const int64_t slot = lane_slot(myslot, t);
+        u32x4 v;
+        if ((t & 7) == 0) {
+          v = *reinterpret_cast<const MX_LDS u32x4*>(srow + t);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; e++) v[e] = (uint32_t)srow[t + 2 * e] | ((uint32_t)srow[t + 2 * e + 1] << 16);
+        }
+        *reinterpret_cast<u32x4*>(v_pool + (((slot >> 4) * nkv + vh) * hd + dim) * 16 + (slot & 15)) = v;
+      }
+      for (; single; single &= single - 1) {
+        const int t = __builtin_ctz(single);
+        const int64_t slot = lane_slot(myslot, t);
+        v_pool[(((slot >> 4) * nkv + vh) * hd + dim) * 16 + (slot & 15)] = srow[t];
+      }
+      lgkm_wait<0>();
     }
   }
 }
@@ -579,9 +573,13 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
 
   // epilogue
   if constexpr (EPI == EPI_QKV && !SPLIT) {
+    static_assert(NWAVES * kQkvStageHalves * 2 <= NS * STAGE, "the staging does not fit the ring");
+    wg_barrier();  // every wave is done reading the ring
+    MX_LDS uint16_t* st =
+        reinterpret_cast<MX_LDS uint16_t*>((MX_LDS char*)smem) + wave_s * kQkvStageHalves;
     const QkvEpilogue& e = a.qkv;
     qkv_epilogue<MB, NB>(acc, a.M, a.N, m0 + wave_m * WM, n0 + wave_n * WN, lane, e.rope_cs,
-                         e.tok_slot, e.q_out, e.k_pool, e.v_pool, e.nq, e.nkv, e.head_dim);
+                         e.tok_slot, e.q_out, e.k_pool, e.v_pool, e.nq, e.nkv, e.head_dim, st);
     return;
   }
   if constexpr (!SPLIT && (EPI == EPI_STORE || EPI == EPI_RESIDUAL || EPI == EPI_SWIGLU)) {
