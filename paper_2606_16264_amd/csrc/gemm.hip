@@ -355,6 +355,51 @@ __device__ __forceinline__ void store_epilogue(const f32x16 (&acc)[MB][NB], int 
   }
 }
 
+// The fp32 partial sums of one K split, through the same staging: 8
+// consecutive columns of one row per lane and run, two 16-byte stores (rows
+// of N % 4 != 0 floats, and the columns at the N edge, take 4-byte stores).
+template <int MB, int NB>
+__device__ __forceinline__ void split_epilogue(const f32x16 (&acc)[MB][NB], int M, int N, int r0,
+                                               int c0, int lane, float* __restrict__ P,
+                                               MX_LDS float* st) {
+  static_assert(NB == 2, "the staging holds 64 columns per wave");
+  const int ccol = lane & 31, crow = 4 * (lane >> 5);
+  const int rq = lane >> 3, col = c0 + 8 * (lane & 7);
+  const bool vec = N % 4 == 0 && col + 8 <= N;
+#pragma unroll
+  for (int i = 0; i < MB; i++) {
+#pragma unroll
+    for (int r = 0; r < 16; r++)
+#pragma unroll
+      for (int j = 0; j < NB; j++)
+        st[(8 * (r >> 2) + crow + (r & 3)) * kStageRow + j * 32 + ccol] = acc[i][j][r];
+    lgkm_wait<0>();
+    f32x4 lo[4], hi[4];
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+      const MX_LDS f32x4* sp =
+          reinterpret_cast<const MX_LDS f32x4*>(st + (rq + 8 * q) * kStageRow + 8 * (lane & 7));
+      lo[q] = sp[0];
+      hi[q] = sp[1];
+    }
+    lgkm_wait<0>();
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+      const int row = r0 + i * 32 + rq + 8 * q;
+      if (row >= M || col >= N) continue;
+      float* pp = P + (int64_t)row * N + col;
+      if (vec) {
+        reinterpret_cast<f32x4*>(pp)[0] = lo[q];
+        reinterpret_cast<f32x4*>(pp)[1] = hi[q];
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; e++)
+          if (col + e < N) pp[e] = e < 4 ? lo[q][e] : hi[q][e - 4];
+      }
+    }
+  }
+}
+
 // SwiGLU epilogue of one wave's block: packed columns c0.. hold 32-column
 // blocks of gate and up of the same 32 features; the 32 outputs (columns
 // c0 / 2 ..) go to C row-major or, c_tiled, in the projection-input tile
@@ -595,21 +640,12 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
                                                   st);
     return;
   }
-  const int ccol = lane & 31, crow = 4 * (lane >> 5);
-#pragma unroll
-  for (int i = 0; i < MB; i++) {
-#pragma unroll
-    for (int r = 0; r < 16; r++) {
-      const int row = m0 + wave_m * WM + i * 32 + 8 * (r >> 2) + crow + (r & 3);
-      if (row >= a.M) continue;
-      if constexpr (SPLIT) {
-#pragma unroll
-        for (int j = 0; j < NB; j++) {
-          const int colg = n0 + wave_n * WN + j * 32 + ccol;
-          if (colg < a.N) a.partial[((int64_t)kz * a.M + row) * a.N + colg] = acc[i][j][r];
-        }
-      }
-    }
+  if constexpr (SPLIT) {  // this split's fp32 plane, [M][N]
+    static_assert(NWAVES * kStageFloats * 4 <= NS * STAGE, "the staging does not fit the ring");
+    wg_barrier();
+    MX_LDS float* st = reinterpret_cast<MX_LDS float*>((MX_LDS char*)smem) + wave_s * kStageFloats;
+    split_epilogue<MB, NB>(acc, a.M, a.N, m0 + wave_m * WM, n0 + wave_n * WN, lane,
+                           a.partial + (int64_t)kz * a.M * a.N, st);
   }
 }
 
