@@ -75,20 +75,6 @@ __device__ __forceinline__ void tile_coords(int bid, int tiles_m, int tiles_n, i
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
 
-// Pointers of the fused QKV epilogue, passed to the epilogue functions as
-// separate __restrict__ parameters: the table reads (rotary cos/sin, KV slots)
-// then cannot alias the stores, so the reads of a whole row block are issued
-// before its first store.  (A wait on a load also waits for every store issued
-// before it: interleaved, each store would put a full memory round trip in
-// front of the next load.)
-struct QkvPtrs {
-  const float2* rope_cs;
-  const int64_t* tok_slot;
-  uint16_t* q_out;
-  uint16_t* k_pool;
-  uint16_t* v_pool;
-};
-
 // Fused QKV epilogue for one rotary pair: packed columns c and c + 32 (c in the
 // low 32-column block of a 64-column group) of token row t, fp32 values lo,
 // hi, with the token's KV slot and the pair's (cos, sin) already read.  q and k
