@@ -4,9 +4,15 @@ times are taken as highly predictable there, which the fit's residuals test).
 
 A mixed iteration's latency is modelled as linear in the work its parts do:
 
-    t = c0 + c_tok * T + c_kv * KV + c_pair * PAIRS + c_req * R
+    t = c0 + c_tok * T + c_big * max(T - T_KNOT, 0) + c_kv * KV + c_pair * PAIRS + c_req * R
 
 T      tokens in the iteration (every projection streams them);
+max(T - T_KNOT, 0)
+       the tokens beyond one 256-row GEMM tile: up to about that many rows
+       the projections stream their weights from HBM once and cost little
+       more per token, beyond it they are bound by the matrix cores and cost
+       a fixed amount per token (a hinge at T_KNOT, so that one fit spans
+       decode-only and prefill-heavy batches);
 KV     cached keys read by the decode rows, sum over decodes of ctx + 1
        (decode attention streams the KV cache);
 PAIRS  query-key pairs of the prefill chunks, sum over chunks of
@@ -24,7 +30,8 @@ from typing import Dict, Iterable, List, Sequence
 
 import numpy as np
 
-FEATURES = ("one", "tokens", "decode_kv", "prefill_pairs", "requests")
+FEATURES = ("one", "tokens", "tokens_beyond_knot", "decode_kv", "prefill_pairs", "requests")
+T_KNOT = 256
 
 
 def batch_features(n_new: Sequence[int], ctx_len: Sequence[int], is_decode: Sequence[bool]) -> np.ndarray:
@@ -36,7 +43,7 @@ def batch_features(n_new: Sequence[int], ctx_len: Sequence[int], is_decode: Sequ
     kv = (ctx[dec] + 1.0).sum()
     t, p = n_new[~dec], ctx[~dec]
     pairs = (t * p + t * (t + 1.0) / 2.0).sum()
-    return np.array([1.0, T, kv, pairs, float(len(n_new))])
+    return np.array([1.0, T, max(T - T_KNOT, 0.0), kv, pairs, float(len(n_new))])
 
 
 @dataclass

@@ -15,20 +15,23 @@ def brute_features(n_new, ctx, dec):
         for i in range(t):            # new token i sits at position p + i ...
             for j in range(p + i + 1):  # ... and attends to keys 0 .. p + i
                 pairs += 1
-    return [1.0, T, kv, pairs, len(n_new)]
+    return [1.0, T, max(T - 256, 0), kv, pairs, len(n_new)]
 
 
 def test_features_hand_example():
     f = batch_features([1, 1, 4], [10, 20, 3], [True, True, False])
-    assert list(f) == [1.0, 6.0, 32.0, 22.0, 3.0]
-    assert FEATURES == ("one", "tokens", "decode_kv", "prefill_pairs", "requests")
+    assert list(f) == [1.0, 6.0, 0.0, 32.0, 22.0, 3.0]
+    f = batch_features([1, 300], [10, 0], [True, False])
+    assert list(f) == [1.0, 301.0, 45.0, 11.0, 300 * 301 / 2, 2.0]
+    assert FEATURES == ("one", "tokens", "tokens_beyond_knot", "decode_kv", "prefill_pairs",
+                        "requests")
 
 
 @pytest.mark.parametrize("seed", range(5))
 def test_features_match_brute_force(seed):
     rng = np.random.default_rng(seed)
     n_dec, n_pre = int(rng.integers(0, 6)), int(rng.integers(0, 4))
-    n_new = [1] * n_dec + [int(v) for v in rng.integers(1, 40, size=n_pre)]
+    n_new = [1] * n_dec + [int(v) for v in rng.integers(1, 400, size=n_pre)]
     ctx = [int(v) for v in rng.integers(0, 60, size=n_dec + n_pre)]
     ctx[:n_dec] = [max(1, c) for c in ctx[:n_dec]]
     dec = [True] * n_dec + [False] * n_pre
@@ -50,7 +53,7 @@ def synthetic(rng, n, coef, noise=0.0):
 
 def test_fit_recovers_exact_coefficients():
     rng = np.random.default_rng(7)
-    coef = np.array([150.0, 0.08, 1.9e-4, 3.0e-7, 0.4])
+    coef = np.array([150.0, 0.02, 0.08, 1.9e-4, 3.0e-7, 0.4])
     feats, lat = synthetic(rng, 40, coef)
     m = LatencyModel.fit(feats, lat)
     np.testing.assert_allclose(m.coef, coef, rtol=1e-6)
@@ -64,7 +67,7 @@ def test_fit_recovers_exact_coefficients():
 
 def test_fit_with_noise_has_small_residuals():
     rng = np.random.default_rng(8)
-    coef = np.array([150.0, 0.08, 1.9e-4, 3.0e-7, 0.4])
+    coef = np.array([150.0, 0.02, 0.08, 1.9e-4, 3.0e-7, 0.4])
     feats, lat = synthetic(rng, 60, coef, noise=0.01)
     m = LatencyModel.fit(feats[:30], lat[:30])
     assert m.residuals(feats[30:], lat[30:])["median_abs_rel"] < 0.02
@@ -72,7 +75,7 @@ def test_fit_with_noise_has_small_residuals():
 
 def test_fit_needs_enough_samples():
     with pytest.raises(ValueError):
-        LatencyModel.fit([np.ones(5)] * 3, [1.0, 2.0, 3.0])
+        LatencyModel.fit([np.ones(6)] * 3, [1.0, 2.0, 3.0])
 
 
 # ---------------------------------------------------------------- SLO and slack
@@ -137,7 +140,7 @@ def test_admission_gates():
 
 
 # ---------------------------------------------------------------- simulator
-TOY = LatencyModel(coef=np.array([50.0, 10.0, 0.0, 0.0, 0.0]))   # 50 + 10 per token, per layer
+TOY = LatencyModel(coef=np.array([50.0, 10.0, 0.0, 0.0, 0.0, 0.0]))   # 50 + 10 per token, per layer
 
 
 def test_simulator_fig7_scenario():
@@ -166,7 +169,7 @@ def test_simulator_fig7_scenario():
 def test_simulator_conserves_requests(policy):
     reqs = synthetic_requests(rate_per_s=20.0, n=120, seed=5, prompt_median=512, output_median=32)
     slo = SLO(ttft=2e6, tpot=4e4)
-    model = LatencyModel(coef=np.array([250.0, 0.5, 1.5e-3, 7e-5, 1.0]))
+    model = LatencyModel(coef=np.array([250.0, 0.5, 0.0, 1.5e-3, 7e-5, 1.0]))
     sim = Simulator(model, Cluster(policy, workers=4, prefill_workers=2, chunk=512), slo, seed=1)
     res = sim.run(reqs)
     assert res["requests"] == len(reqs)
@@ -176,7 +179,7 @@ def test_simulator_conserves_requests(policy):
 
 
 def test_light_load_meets_every_slo():
-    model = LatencyModel(coef=np.array([250.0, 0.5, 1.5e-3, 7e-5, 1.0]))
+    model = LatencyModel(coef=np.array([250.0, 0.5, 0.0, 1.5e-3, 7e-5, 1.0]))
     from paper_2606_16264_amd.sched import light_load_slo
     slo = light_load_slo(model, 32, 512, 512)
     reqs = synthetic_requests(rate_per_s=0.2, n=30, seed=6, prompt_median=512, output_median=16,
