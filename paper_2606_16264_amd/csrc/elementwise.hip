@@ -71,22 +71,13 @@ __global__ __launch_bounds__(256) void token_map_kernel(TokenMapArgs a) {
 }
 
 // ---------------------------------------------------------------- RMSNorm
-__device__ __forceinline__ float block_sum_256(float v, float* red) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-  const int wave = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) red[wave] = v;
-  __syncthreads();
-  return red[0] + red[1] + red[2] + red[3];
-}
-
 // Two rows per block of 256 threads, written in the tile layout.  Thread t
 // works on row 2j + (t / 4) % 2 and on its chunks (8 columns each)
 // i = 4 (t / 8) + t % 4 + 128 k: the eight threads 8 s .. 8 s + 7 hold the same
 // 32 columns of both rows, which are one 128-byte line of a 16 x 32 tile
 // (rows 2j and 2j + 1 are adjacent in it), so every store instruction writes
-// whole lines; with one row per block each store covered half a line, and the
-// 70B-shaped norms took 70-77 us instead of 52-58 us.  Rows of up to 8192
+// whole lines (70B-shaped norms: 59-65 us; 70-77 us with one row per block,
+// whose stores covered half a line each).  Rows of up to 8192
 // elements are held in registers between the sum of squares and the scaling
 // (with the gains, read in the same first pass), so a row is read from memory
 // once; longer rows are read twice.
