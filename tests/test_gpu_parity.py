@@ -592,6 +592,32 @@ def test_layer_step_aligned_value_runs(cfg):
     assert changed_slots(got["v0"], got["v"], True) <= written
 
 
+def test_layer_step_value_runs_any_alignment():
+    """Chunks whose first row falls at different offsets in the 32-row blocks
+    of the QKV epilogue and whose cached lengths put their first slot at every
+    offset 0 .. 7 within a group of 8: the value runs are found from the slots
+    themselves (a run may start at any row of a block and cross into the next
+    page's group), the tokens left over go one at a time.  Every row and every
+    new slot is checked, and no pool entry outside the new slots may change."""
+    say("case: layer step value runs at every alignment")
+    cfg = SMALL_GQA
+    rng = np.random.default_rng(93)
+    # first rows 5, 42, 87, 116, 182, 223, 284, 311; first slots 3, 5, 6, 7, 2, 1, 4, 0 mod 8
+    b = wl.custom_batch(rng, [9, 30, 100, 250, 17],
+                        [(37, 3), (45, 21), (29, 14), (66, 7), (41, 26), (61, 9), (27, 12), (50, 32)])
+    w = small_weights(rng, cfg)
+    x = wl.f32_to_bf16_bits(rng.standard_normal((b.T, cfg.hidden), dtype=np.float32))
+    got = run_layer(cfg, b, w, x, 4545, keep_before=True)
+    kp, vp = wl.prior_kv_concat(cfg, b, 4545)
+    exp = oracle.layer_step(cfg.as_dict(), b.n_new, b.ctx_len, x, w, kp, vp)
+    rows = np.arange(b.T)
+    check_layer(cfg, b, got, exp, rows, "any-alignment", staged_attention(cfg, b, x, w, kp, vp, rows), x=x)
+    check_pool_rows(cfg, b, got, exp.k_new, exp.v_new, rows)
+    written = set(oracle.token_map(b.n_new, b.ctx_len, b.page_tables, 16).tok_slot.tolist())
+    assert changed_slots(got["k0"], got["k"], False) <= written
+    assert changed_slots(got["v0"], got["v"], True) <= written
+
+
 MEDIUM_MHA = wl.LayerConfig("medium-mha", 1536, 2816, 12, 12, 128)
 
 
