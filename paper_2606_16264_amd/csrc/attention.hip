@@ -293,13 +293,17 @@ __device__ __forceinline__ bool chunk_interior(int pi0, int page_end, int first_
 // (waves 0 and 1 the keys of the chunk's two pages, waves 2 and 3 their
 // values), and every wave reads its matrix-core fragments from there.  Keys
 // are stored [32][HD] with the 16-byte chunk c of key row j at c ^ ksw(j);
-// values [HD][32 keys] with the 16-byte chunk c of dim row d at
-// c ^ ((d >> 2) & 3).  Both make the fragment reads (16 key rows, or 16 dim
-// rows, at one logical chunk) hit distinct bank groups.  A DMA instruction
-// writes 1 KB of LDS in lane order, so each lane fetches the 16 bytes that
-// belong at its position: a permutation within the page's rows (and, for
-// keys, within its 32-dim blocks), which keeps every copy a run of whole
-// 128-byte lines.
+// values page by page, [2 pages][HD][2 halves of 8 keys], with half h of dim
+// row d at h ^ ((d >> 3) & 1).  Both make the fragment reads (16 key rows, or
+// 16 dim rows, at one logical chunk) hit distinct bank groups.  A DMA
+// instruction writes 1 KB of LDS in lane order, so each lane fetches the 16
+// bytes that belong at its position: a permutation within the page's rows
+// (and, for keys, within its 32-dim blocks), which keeps every copy a run of
+// whole 128-byte lines.  Each copy instruction reads from one page only, so
+// its page address is the same for every lane (scalar arithmetic; with the
+// values' two pages side by side in every dim row, as first laid out, the
+// lanes of one copy read from both, and choosing and forming a 64-bit address
+// per lane cost 14 of the loop's 81 vector instructions per chunk).
 template <int HD>
 __device__ __forceinline__ int ksw(int key) {
   if constexpr (HD == 128) return (key & 3) | ((key >> 3) << 2);
@@ -405,7 +409,7 @@ __device__ __forceinline__ void prefill_item(const AttnParams& p, const AttnItem
   // kb = NLD * wave + i of the slot (keys first, then values) with the 16 bytes
   // at element offset off[i] of the chunk's first (sel[i] false) or second page.
   int off[NLD];
-  bool sel[NLD];
+  bool sel[NLD];  // (the same for every lane: each copy reads one page)
 #pragma unroll
   for (int i = 0; i < NLD; i++) {
     const int kb = NLD * wave + i;
@@ -413,13 +417,16 @@ __device__ __forceinline__ void prefill_item(const AttnParams& p, const AttnItem
       constexpr int lanes_per_row = HD / 8;  // 16-byte pieces of a key row
       const int j = kb * (64 / lanes_per_row) + lane / lanes_per_row;
       const int lc = (lane % lanes_per_row) ^ ksw<HD>(j);
-      sel[i] = j >= 16;
+      sel[i] = kb * (64 / lanes_per_row) >= 16;
       off[i] = (lc >> 2) * 512 + (j & 15) * 32 + (lc & 3) * 8;
     } else {
-      const int d = (kb - KB / 1024) * 16 + (lane >> 2);
-      const int c = (lane & 3) ^ ((d >> 2) & 3);  // logical 8-key piece: page c / 2
-      sel[i] = c >= 2;
-      off[i] = d * 16 + (c & 1) * 8;
+      // values: [page][dim][2 halves of 8 keys], half h of dim row d stored
+      // at h ^ ((d >> 3) & 1)
+      const int vb = (kb - KB / 1024) * 1024 + lane * 16;  // byte in the value half
+      const int d = (vb % (HD * 32)) / 32;
+      const int h = ((vb / 16) & 1) ^ ((d >> 3) & 1);
+      sel[i] = (kb - KB / 1024) * 1024 >= HD * 32;
+      off[i] = d * 16 + h * 8;
     }
   }
   const uint16_t* pool = wave < 2 ? p.k_pool : p.v_pool;
@@ -431,7 +438,9 @@ __device__ __forceinline__ void prefill_item(const AttnParams& p, const AttnItem
     const uint16_t* bb = pool + ((int64_t)pb * p.nkv + kvh) * (16 * HD);
     const unsigned dst = lds0 + (unsigned)((c & 3) * CB + NLD * wave * 1024);
 #pragma unroll
-    for (int i = 0; i < NLD; i++) dma16((sel[i] ? bb : ba) + off[i], dst + i * 1024);
+    for (int i = 0; i < NLD; i++) {
+      dma16((sel[i] ? bb : ba) + off[i], dst + i * 1024);
+    }
   };
   auto page_of = [&](int pi) { return ptab[min(pi, last_page)]; };
 
@@ -442,7 +451,8 @@ __device__ __forceinline__ void prefill_item(const AttnParams& p, const AttnItem
 #pragma unroll
   for (int ds = 0; ds < ND; ds++)
     kaddr[ds] = (unsigned)(key0 * (HD * 2) + (((4 * ds + g4) ^ ksw<HD>(key0)) << 4));
-  const unsigned vaddr = (unsigned)(KB + col * 64 + ((g4 ^ ((col >> 2) & 3)) << 4));
+  const unsigned vaddr = (unsigned)(KB + (g4 >> 1) * (HD * 32) + col * 32 +
+                                    (((g4 & 1) ^ ((col >> 3) & 1)) << 4));
 
   // scores of chunk c from its keys in LDS: this lane's masked raw scores, their
   // max, and whether some lane of the wave is above its row's threshold
@@ -475,8 +485,8 @@ __device__ __forceinline__ void prefill_item(const AttnParams& p, const AttnItem
     constexpr bool MASK = decltype(mask)::value;
     const unsigned va = lds0 + (unsigned)((c & 3) * CB) + vaddr;
     u32x4 v0[ND], v1[ND];
-    lds_read_run<0, ND, 0, 1024>(va, v0);
-    lds_read_run<0, ND, ND * 1024, 1024>(va, v1);
+    lds_read_run<0, ND, 0, 512>(va, v0);
+    lds_read_run<0, ND, ND * 512, 512>(va, v1);
     uint32_t keep[4] = {~0u, ~0u, ~0u, ~0u};
     if constexpr (MASK) value_keep(2 * c, page_end, rq.kv_len, g4, keep);
     lgkm_wait<ND>();
