@@ -73,7 +73,13 @@ __device__ __forceinline__ void tile_coords(int bid, int tiles_m, int tiles_n, i
   tn = in_group / gm;
 }
 
-__device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
+// silu(g) = g / (1 + e^-g), the quotient through the reciprocal instruction
+// (1 ulp) rather than the IEEE division sequence (about ten instructions per
+// element in the epilogue): the result is rounded to bf16 anyway.  g -> -inf:
+// 1 / inf = 0, so silu -> -0; g -> +inf: g.
+__device__ __forceinline__ float silu(float g) {
+  return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g));
+}
 
 // Fused QKV epilogue for one rotary pair: packed columns c and c + 32 (c in the
 // low 32-column block of a 64-column group) of token row t, fp32 values lo,
