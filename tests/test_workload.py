@@ -83,3 +83,19 @@ def test_bf16_half_ulp_bounds_rounding():
     # tight: at 1.0 the bf16 spacing is 2^-7, so half an ulp is 2^-8
     assert bf16_half_ulp(np.array([1.0, 1.5, 2.0]))[0] == 2.0 ** -8
     assert bf16_half_ulp(np.array([2.0]))[0] == 2.0 ** -7
+
+
+def test_key_page_layout_conversions():
+    """The device's blocked key pages [page][head][d/32][16][32] and the
+    canonical [page][head][16][d] order: element (slot s, dim e) of a page sits
+    at (e / 32) * 512 + s * 32 + e % 32, and the two conversions are inverses."""
+    import workload.device as wdev
+    rng = np.random.default_rng(3)
+    for d in (64, 128):
+        canon = rng.integers(0, 65536, (3, 2, 16, d), dtype=np.uint16)
+        blocked = wdev.k_pool_blocked(canon)
+        assert blocked.shape == (3, 2, d // 32, 16, 32)
+        flat = blocked.reshape(3, 2, -1)
+        for s, e in ((0, 0), (5, 33), (15, d - 1), (7, 31)):
+            assert flat[1, 1, (e // 32) * 512 + s * 32 + e % 32] == canon[1, 1, s, e]
+        np.testing.assert_array_equal(wdev.k_pool_canonical(blocked), canon)
