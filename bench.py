@@ -54,8 +54,8 @@ def parse():
                          "latency model on the even-numbered ones and report its residuals "
                          "on the odd-numbered ones; prints one JSON line")
     ap.add_argument("--simulate", metavar="MODEL_JSON",
-                    help="CPU only: SLO attainment of colocated, disaggregated and SLO-aware "
-                         "multiplexing serving over a sweep of arrival rates, simulated with the "
+                    help="CPU only: SLO attainment of SLO-aware multiplexed serving over a sweep "
+                         "of arrival rates, simulated with the "
                          "latency model that `--predictor` printed (MODEL_JSON); prints one JSON line")
     ap.add_argument("--rates", type=float, nargs="+", default=[4, 8, 16, 24, 32, 48])
     ap.add_argument("--requests", type=int, default=800)
@@ -491,15 +491,16 @@ def main():
         summarize_traffic(*a)
         return
     if args.simulate:
-        from paper_2606_16264_amd.sched import LatencyModel, compare
+        from paper_2606_16264_amd.sched import LatencyModel, attainment_sweep
         import workload as wl
         rec = json.load(open(args.simulate))["latency_model"]
         cfg = wl.CONFIGS[args.config]
         noise = rec["held_out_residuals"]["median_abs_rel"]
-        res = compare(LatencyModel.from_dict(rec["coef_us"]), args.rates, n=args.requests,
-                      kv_bytes_per_token=32.0 * cfg.kv_bytes_per_token, noise=noise)
+        res = attainment_sweep(LatencyModel.from_dict(rec["coef_us"]), args.rates,
+                               n=args.requests, kv_bytes_per_token=32.0 * cfg.kv_bytes_per_token,
+                               noise=noise)
         res.update(latency_model=rec["workload"], noise=noise, layers=32,
-                   workers="4 (2 prefill + 2 decode/multiplexing; colocated: 4 mixed)",
+                   workers="4 (2 prefill + 2 multiplexing)",
                    requests=args.requests,
                    arrivals="Poisson; prompts lognormal(median 2048, sigma 1) in [32, 16384]; "
                             "outputs lognormal(median 128, sigma 0.8) in [1, 1024]")

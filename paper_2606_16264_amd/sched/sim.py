@@ -1,24 +1,16 @@
-"""Discrete-event simulator of prefill/decode scheduling on a group of workers,
-driven by the iteration-latency model (per layer, times the model's layers).
+"""Discrete-event simulator of SLO-aware prefill/decode multiplexing on a group
+of workers, driven by the iteration-latency model (per layer, times the model's
+layers).
 
-Policies (Section 4 and the baselines of Section 5.1):
-  colocated      every worker mixes its running decodes with one prefill chunk
-                 per iteration (non-disaggregated serving with chunked prefill);
-                 new requests go to the worker with the fewest unfinished tokens.
-  disaggregated  prefill workers run whole prompts first-come first-served;
-                 the KV cache then migrates over the link to the decode worker
-                 with the fewest unfinished tokens.
-  multiplexing   prefill workers plus multiplexing workers (SLO-aware
-                 multiplexing).  A multiplexing worker piggybacks a prefill
-                 chunk onto its next decode iteration only when the TPOT-slack
-                 test and the decode-batch and HBM gates pass (slo.admits_chunk);
-                 a prefill worker takes a queued request only when the predicted
-                 queueing plus execution time fits the request's remaining TTFT
-                 budget; a request no worker can serve within its SLO any more
-                 goes to the least-loaded prefill worker.  Requests prefilled on
-                 a prefill worker migrate to the multiplexing worker with the
-                 fewest unfinished tokens; requests prefilled on a multiplexing
-                 worker decode where they are.
+Workers (Section 4.2): prefill workers and multiplexing workers.  A
+multiplexing worker runs its decodes and piggybacks a prefill chunk onto its
+next decode iteration only when the TPOT-slack test and the decode-batch and HBM
+gates pass (slo.admits_chunk); a prefill worker takes a queued request only
+when the predicted queueing plus execution time fits the request's remaining
+TTFT budget; a request no worker can serve within its SLO any more goes to the
+least-loaded prefill worker.  Requests prefilled on a prefill worker migrate to
+the multiplexing worker with the fewest unfinished tokens; requests prefilled on
+a multiplexing worker decode where they are.
 
 Every decode iteration's time (including the piggybacked chunk) is added to
 the decode time of each request in it, so interference shows up in TPOT.
@@ -41,9 +33,8 @@ from .slo import SLO, Request, admits_chunk, attainment
 
 @dataclass
 class Cluster:
-    policy: str                    # "colocated" | "disaggregated" | "multiplexing"
     workers: int = 4               # total workers
-    prefill_workers: int = 2       # disaggregated / multiplexing: how many are prefill workers
+    prefill_workers: int = 2       # how many of them are prefill workers
     chunk: int = 2048              # chunk size of chunked prefill
     max_batch: int = 256           # running decodes per worker
     layers: int = 32
@@ -57,7 +48,7 @@ class Cluster:
 @dataclass
 class _Worker:
     wid: int
-    role: str                      # "prefill" | "decode" | "mixed" | "mux"
+    role: str                      # "prefill" | "mux"
     queue: deque = field(default_factory=deque)     # prefill requests assigned to it
     running: List[Request] = field(default_factory=list)
     pending: deque = field(default_factory=deque)   # waiting for KV room / migration
@@ -75,17 +66,11 @@ class Simulator:
         self.c = cluster
         self.slo = slo
         self.rng = np.random.default_rng(seed)
-        roles: List[str]
-        if cluster.policy == "colocated":
-            roles = ["mixed"] * cluster.workers
-        elif cluster.policy == "disaggregated":
-            roles = ["prefill"] * cluster.prefill_workers + ["decode"] * (cluster.workers - cluster.prefill_workers)
-        elif cluster.policy == "multiplexing":
-            roles = ["prefill"] * cluster.prefill_workers + ["mux"] * (cluster.workers - cluster.prefill_workers)
-        else:
-            raise ValueError(f"unknown policy {cluster.policy}")
+        if not 1 <= cluster.prefill_workers < cluster.workers:
+            raise ValueError("need at least one prefill and one multiplexing worker")
+        roles = ["prefill"] * cluster.prefill_workers + ["mux"] * (cluster.workers - cluster.prefill_workers)
         self.w = [_Worker(i, r) for i, r in enumerate(roles)]
-        self.toggle: deque = deque()   # multiplexing: requests not yet placed
+        self.toggle: deque = deque()   # requests not yet placed
         self.done: List[Request] = []
         self.events: list = []
         self.seq = 0
@@ -131,10 +116,11 @@ class Simulator:
         start = max(now, w.busy_until) if w.busy else now
         return start - now + sum(self._prefill_time(r) for r in w.queue)
 
-    def _place_decode(self, r: Request, now: float, migrate: bool, roles):
-        ws = [w for w in self.w if w.role in roles]
-        w = min(ws, key=self._unfinished)
-        r.ready = now + (r.prompt * self.c.kv_bytes_per_token / self.c.link_bytes_per_us if migrate else 0.0)
+    def _place_decode(self, r: Request, now: float):
+        """A request prefilled on a prefill worker: its KV cache migrates to the
+        multiplexing worker with the fewest unfinished tokens."""
+        w = min((w for w in self.w if w.role == "mux"), key=self._unfinished)
+        r.ready = now + r.prompt * self.c.kv_bytes_per_token / self.c.link_bytes_per_us
         r.worker = w.wid
         w.pending.append(r)
         self._kick(w, now)
@@ -161,16 +147,7 @@ class Simulator:
 
     # ------------------------------------------------------------ dispatch
     def _dispatch(self, now: float):
-        pol = self.c.policy
-        if pol in ("colocated", "disaggregated"):
-            roles = ("mixed",) if pol == "colocated" else ("prefill",)
-            while self.toggle:
-                r = self.toggle.popleft()
-                w = min((w for w in self.w if w.role in roles), key=self._unfinished)
-                w.queue.append(r)
-                self._kick(w, now)
-            return
-        # multiplexing: prefill workers take a request when it fits its TTFT budget
+        # prefill workers take a request when it fits its TTFT budget
         keep = deque()
         while self.toggle:
             r = self.toggle.popleft()
@@ -203,22 +180,7 @@ class Simulator:
             prefill_req = w.queue.popleft()
             chunk = (prefill_req.prompt - prefill_req.prefilled, prefill_req.prefilled)
             decodes = []
-        elif w.role == "decode":
-            if not decodes:
-                if w.pending:
-                    self._push(min(r.ready for r in w.pending), "wake", w.wid)
-                return
-        elif w.role == "mixed":
-            if w.prefill is None and w.queue:
-                w.prefill = w.queue.popleft()
-            if w.prefill is not None:
-                prefill_req = w.prefill
-                chunk = (min(self.c.chunk, prefill_req.prompt - prefill_req.prefilled), prefill_req.prefilled)
-            if not decodes and chunk is None:
-                if w.pending:
-                    self._push(min(r.ready for r in w.pending), "wake", w.wid)
-                return
-        elif w.role == "mux":
+        else:
             t_base = self.predict(decodes) if decodes else 0.0
             cand = []
             if w.prefill is not None:
@@ -261,19 +223,18 @@ class Simulator:
             if preq.prefilled >= preq.prompt:
                 preq.first_token = now
                 preq.generated = 1
-                if w.role in ("mixed", "mux"):
+                if w.role == "mux":
                     w.prefill = None
                 if preq.output <= 1:
                     preq.finish = now
                     self.done.append(preq)
                 elif w.role == "prefill":
-                    roles = ("decode",) if self.c.policy == "disaggregated" else ("mux",)
-                    self._place_decode(preq, now, True, roles)
+                    self._place_decode(preq, now)
                 else:
                     preq.worker = w.wid
                     preq.ready = now
                     w.pending.append(preq)
-        if self.c.policy == "multiplexing" and w.role == "prefill":
+        if w.role == "prefill":
             self._dispatch(now)
         self._kick(w, now)
 
@@ -290,7 +251,7 @@ class Simulator:
                 self._iteration_done(now, payload)
             elif kind == "wake":
                 self._kick(self.w[payload], now)
-            if self.c.policy == "multiplexing" and self.toggle:
+            if self.toggle:
                 self._dispatch(now)
         if len(self.done) != len(requests):
             raise RuntimeError(f"{len(requests) - len(self.done)} requests never finished")
@@ -327,25 +288,21 @@ def per_request_ttft(model: LatencyModel, layers: int, reqs: Sequence[Request], 
         r.ttft_slo = factor * model.predict_batch([r.prompt], [0], [False]) * layers
 
 
-def compare(model: LatencyModel, rates: Sequence[float], n: int = 1500, seed: int = 11,
-            workers: int = 4, prefill_workers: int = 2, layers: int = 32, chunk: int = 2048,
-            kv_bytes_per_token: float = 131072.0, kv_capacity: float = 250e9, noise: float = 0.0,
-            prompt_median: int = 2048, output_median: int = 128, slo_factor: float = 5.0) -> Dict:
-    """SLO attainment of the three policies over a sweep of arrival rates on
-    the same synthetic request stream per rate."""
+def attainment_sweep(model: LatencyModel, rates: Sequence[float], n: int = 1500, seed: int = 11,
+                     workers: int = 4, prefill_workers: int = 2, layers: int = 32, chunk: int = 2048,
+                     kv_bytes_per_token: float = 131072.0, kv_capacity: float = 250e9,
+                     noise: float = 0.0, prompt_median: int = 2048, output_median: int = 128,
+                     slo_factor: float = 5.0) -> Dict:
+    """SLO attainment of multiplexed serving over a sweep of arrival rates, one
+    synthetic request stream per rate."""
     slo = light_load_slo(model, layers, prompt_median, prompt_median, slo_factor)
-    out = {"slo_us": {"ttft_of_median_prompt": slo.ttft, "tpot": slo.tpot,
-                      "ttft_rule": f"{slo_factor} x each request's own prefill time alone"},
-           "rates": list(rates), "policies": {}}
-    for pol in ("colocated", "disaggregated", "multiplexing"):
-        rows = []
-        for rate in rates:
-            reqs = synthetic_requests(rate, n, seed, prompt_median, output_median)
-            per_request_ttft(model, layers, reqs, slo_factor)
-            cl = Cluster(pol, workers=workers, prefill_workers=prefill_workers, chunk=chunk,
-                         layers=layers, kv_bytes_per_token=kv_bytes_per_token, kv_capacity=kv_capacity,
-                         noise=noise)
-            rows.append(Simulator(model, cl, slo, seed=seed).run(reqs))
-        out["policies"][pol] = rows
-    return out
-
+    rows = []
+    for rate in rates:
+        reqs = synthetic_requests(rate, n, seed, prompt_median, output_median)
+        per_request_ttft(model, layers, reqs, slo_factor)
+        cl = Cluster(workers=workers, prefill_workers=prefill_workers, chunk=chunk, layers=layers,
+                     kv_bytes_per_token=kv_bytes_per_token, kv_capacity=kv_capacity, noise=noise)
+        rows.append(Simulator(model, cl, slo, seed=seed).run(reqs))
+    return {"slo_us": {"ttft_of_median_prompt": slo.ttft, "tpot": slo.tpot,
+                       "ttft_rule": f"{slo_factor} x each request's own prefill time alone"},
+            "rates": list(rates), "attainment": rows}

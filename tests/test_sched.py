@@ -151,7 +151,7 @@ def test_simulator_fig7_scenario():
     slack for it, and is then prefilled on the multiplexing worker without
     pushing R0 over its TPOT SLO."""
     slo = SLO(ttft=1000.0, tpot=100.0)
-    cl = Cluster("multiplexing", workers=2, prefill_workers=1, chunk=64, layers=1,
+    cl = Cluster(workers=2, prefill_workers=1, chunk=64, layers=1,
                  kv_bytes_per_token=1.0, link_bytes_per_us=1e12, kv_capacity=1e12)
     reqs = [Request(0, 0.0, 5, 10), Request(1, 1.0, 1000, 2), Request(2, 150.0, 10, 2)]
     sim = Simulator(TOY, cl, slo, trace=True)
@@ -165,12 +165,13 @@ def test_simulator_fig7_scenario():
     assert res["requests"] == 3
 
 
-@pytest.mark.parametrize("policy", ["colocated", "disaggregated", "multiplexing"])
-def test_simulator_conserves_requests(policy):
+@pytest.mark.parametrize("prefill_workers", [1, 2, 3])
+def test_simulator_conserves_requests(prefill_workers):
     reqs = synthetic_requests(rate_per_s=20.0, n=120, seed=5, prompt_median=512, output_median=32)
     slo = SLO(ttft=2e6, tpot=4e4)
     model = LatencyModel(coef=np.array([250.0, 0.5, 0.0, 1.5e-3, 7e-5, 1.0]))
-    sim = Simulator(model, Cluster(policy, workers=4, prefill_workers=2, chunk=512), slo, seed=1)
+    sim = Simulator(model, Cluster(workers=4, prefill_workers=prefill_workers, chunk=512), slo,
+                    seed=1)
     res = sim.run(reqs)
     assert res["requests"] == len(reqs)
     for r in sim.done:
@@ -184,6 +185,6 @@ def test_light_load_meets_every_slo():
     slo = light_load_slo(model, 32, 512, 512)
     reqs = synthetic_requests(rate_per_s=0.2, n=30, seed=6, prompt_median=512, output_median=16,
                               max_prompt=2048)
-    for policy in ("colocated", "disaggregated", "multiplexing"):
-        res = Simulator(model, Cluster(policy, workers=4, prefill_workers=2), slo).run(reqs)
-        assert res["attainment"] == 1.0, (policy, res)
+    for prefill_workers in (1, 2, 3):
+        res = Simulator(model, Cluster(workers=4, prefill_workers=prefill_workers), slo).run(reqs)
+        assert res["attainment"] == 1.0, (prefill_workers, res)
