@@ -785,6 +785,15 @@ static __device__ __align__(256) char scratch[kStaticScratchBytes];
 std::mutex g_scratch_mu;
 std::map<int, void*> g_scratch_ptr;
 
+// Host side of the same calls: the metadata block is packed into this
+// file-scope buffer (no allocation per call) and copied from it with
+// hipMemcpyAsync.  From pageable memory HIP performs that copy synchronously
+// (the source has been read when the call returns), so the buffer is free
+// again on return; the lock keeps the calls of different threads apart while
+// they pack and copy.
+std::mutex g_static_host_mu;
+alignas(64) char g_static_host[kStaticScratchBytes];
+
 mx_status static_scratch(void** out) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -830,10 +839,12 @@ MX_EXPORT mx_status mx_paged_attn_static(const mx_batch* batch, const mx_attn_sh
   // the metadata block, packed on the host and copied into the scratch in
   // stream order (nothing in the scratch needs to start at zero: every split
   // partial is written by its item before the merge reads it)
-  thread_local std::vector<char> host;
-  if (host.size() < L.meta_end) host.resize(L.meta_end);
-  pack_meta(p, L, shape, 1e4f, host.data());
-  hipError_t e = hipMemcpyAsync(ws, host.data(), L.meta_end, hipMemcpyHostToDevice, stream);
+  hipError_t e;
+  {
+    std::lock_guard<std::mutex> g(g_static_host_mu);
+    pack_meta(p, L, shape, 1e4f, g_static_host);  // L.meta_end <= L.total, checked above
+    e = hipMemcpyAsync(ws, g_static_host, L.meta_end, hipMemcpyHostToDevice, stream);
+  }
   if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (metadata)");
   AttnParams a = attn_params(p, L, shape, ws, q, (int64_t)shape->n_q_heads * shape->head_dim,
                              k_pool, v_pool, out);
