@@ -364,6 +364,18 @@ def test_gemm_uneven_split(tile_cfg, b_tiled, M, N, K, epi, ksplit):
     gemm_case(M, N, K, epi, tile_cfg=tile_cfg, ksplit=ksplit, b_tiled=b_tiled)
 
 
+# More 256 x 256 tiles than the chip holds workgroups at once (several rounds
+# of the XCD-grouped tile order over a ragged tile grid): ragged M and N edges,
+# every epilogue, row-major and tiled operands, short K (8 to 16 slices of the
+# four-stage ring, one of them not a multiple of four).
+@pytest.mark.parametrize("M,N,K,epi,b_tiled", [
+    (4112, 4160, 256, 0, False), (4100, 4352, 384, 1, False), (4112, 4160, 512, 1, True),
+    (4097, 8320, 256, 2, True), (4112, 4160, 320, 0, True),
+])
+def test_gemm_many_tiles_per_workgroup(M, N, K, epi, b_tiled):
+    gemm_case(M, N, K, epi, tile_cfg=0, ksplit=1, b_tiled=b_tiled)
+
+
 # ----------------------------------------------------------------------- layer step
 def pack_layer(cfg, b, w):
     c = mx_cfg(mx, cfg, b.pool_pages)
