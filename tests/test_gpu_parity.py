@@ -990,3 +990,28 @@ def test_layer_step_random_batches(batch, heads):
     rows = np.arange(b.T)
     check_layer(cfg, b, got, exp, rows, "random", staged_attention(cfg, b, x, w, kp, vp, rows), x=x)
     check_pool_rows(cfg, b, got, exp.k_new, exp.v_new, rows)
+
+
+@st.composite
+def gemm_problem(draw):
+    """A random GEMM of the debug entry points: ragged M, N a multiple of 16
+    (64 for SwiGLU), K a multiple of 64, any epilogue, row-major operands or
+    the layer's layouts, the library's plan or a forced tile shape and K split."""
+    epi = draw(st.sampled_from([0, 1, 2]))
+    M = draw(st.integers(1, 640))
+    unit = 64 if epi == 2 else 16
+    N = unit * draw(st.integers(1, 2048 // unit))
+    K = 64 * draw(st.integers(1, 32))
+    tiled = draw(st.booleans())
+    cfg = draw(st.sampled_from([-1, 0, 1, 2, 3, 4]))
+    ks = draw(st.integers(1, min(8, K // 64))) if cfg >= 0 else 0
+    return M, N, K, epi, tiled, cfg, ks
+
+
+@settings(max_examples=30, **RANDOM_SETTINGS)
+@given(p=gemm_problem())
+def test_gemm_random_problems(p):
+    """The GEMM against the oracle, with canaries around C, on random shapes,
+    epilogues, layouts, tile shapes and K splits."""
+    M, N, K, epi, tiled, cfg, ks = p
+    gemm_case(M, N, K, epi, tile_cfg=cfg, ksplit=ks, b_tiled=tiled)
