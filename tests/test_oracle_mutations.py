@@ -72,6 +72,14 @@ MUTATIONS = {
     "layer-drops-residual": ("for (int64_t e = 0; e < H; e++) x1[i * H + e] += xd[row_idx[i] * H + e];", ";"),
     "layer-rope-on-v": ("orc_rope(T, (int32_t)nkv, (int32_t)d, pos, c->rope_theta, k_new);",
                         "orc_rope(T, (int32_t)nkv, (int32_t)d, pos, c->rope_theta, k_new);\n  orc_rope(T, (int32_t)nkv, (int32_t)d, pos, c->rope_theta, v_new);"),
+    "layer-norm2-gain-g1": ("orc_rmsnorm(nr, H, x1, g2d, c->rms_eps, h2);",
+                            "orc_rmsnorm(nr, H, x1, g1d, c->rms_eps, h2);"),
+    "layer-k-from-v-rows": ("orc_linear(T, H, nkv * d, h, w_qkv + nq * d * H, k_new);",
+                            "orc_linear(T, H, nkv * d, h, w_qkv + (nq + nkv) * d * H, k_new);"),
+    "layer-q-no-rope": ("  orc_rope(nr, (int32_t)nq, (int32_t)d, pos_r, c->rope_theta, q);\n", "\n"),
+    "layer-row-misses-own-key": ("row_ctx[i] = pos_r[i];", "row_ctx[i] = pos_r[i] > 0 ? pos_r[i] - 1 : 0;"),
+    "layer-down-residual-x": ("for (int64_t i = 0; i < nr * H; i++) y[i] += x1[i];",
+                              "for (int64_t i = 0; i < nr; i++)\n    for (int64_t e = 0; e < H; e++) y[i * H + e] += xd[row_idx[i] * H + e];"),
     "layer-gu-no-down": ("for (int64_t i = 0; i < nr * H; i++) y[i] += x1[i];", ""),
 }
 
