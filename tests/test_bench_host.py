@@ -1,0 +1,87 @@
+"""Host logic of bench.py on the CPU: the one-GPU guard, the simulator leg's
+JSON line, and the algorithmic byte and flop counts behind the roofline
+fractions, checked against per-row brute force."""
+import json
+import os
+import subprocess
+import sys
+
+import numpy as np
+
+import bench
+import workload as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def run_bench(*args):
+    return subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *args],
+                          capture_output=True, text=True, timeout=300, cwd=ROOT)
+
+
+def test_more_than_one_gpu_is_refused():
+    r = run_bench("--gpus", "2")
+    assert r.returncode == 2
+    line = json.loads(r.stdout.strip().splitlines()[-1])
+    assert "one GPU" in line["error"]
+
+
+def test_simulate_prints_one_attainment_line():
+    r = run_bench("--config", "c4", "--simulate",
+                  os.path.join(ROOT, "profiles", "latency_model_layer_step_c4.json"),
+                  "--rates", "4", "16", "--requests", "60")
+    assert r.returncode == 0, r.stderr[-2000:]
+    line = json.loads(r.stdout.strip().splitlines()[-1])
+    assert line["rates"] == [4.0, 16.0]
+    assert len(line["attainment"]) == 2
+    for row in line["attainment"]:
+        assert row["requests"] == 60
+        assert 0.0 <= row["attainment"] <= 1.0
+        assert row["ttft_p50_us"] <= row["ttft_p90_us"]
+        assert row["tpot_p50_us"] <= row["tpot_p90_us"]
+
+
+def brute_attention(cfg, b):
+    """Flops and bytes of the attention, one query row at a time: a row at
+    position p scores and weighs keys 0 .. p (4 nq d flops per key: q.k and
+    p v, two flops per multiply-add); a decode row reads its request's keys
+    and values and page table once; a prefill request reads each of its keys
+    and values once (the chunk's own new keys included); every row reads its
+    q and writes its o in bf16."""
+    nq, d = cfg.n_q_heads, cfg.head_dim
+    flops = 0.0
+    dec_bytes = 0.0
+    pre_bytes = 0.0
+    for r in range(b.R):
+        ctx, n = int(b.ctx_len[r]), int(b.n_new[r])
+        for i in range(n):
+            flops += 4.0 * nq * d * (ctx + i + 1)
+        keys = ctx + n
+        if b.phase[r] == wl.DECODE:
+            dec_bytes += keys * cfg.kv_bytes_per_token + 2 * 2 * nq * d + 4 * -(-keys // 16)
+        else:
+            pre_bytes += keys * cfg.kv_bytes_per_token + n * 2 * 2 * nq * d
+    return flops, dec_bytes, pre_bytes
+
+
+def test_algorithmic_counts_match_brute_force():
+    rng = np.random.default_rng(7)
+    for key in ("c1", "c4"):
+        cfg = wl.CONFIGS[key]
+        b = wl.custom_batch(rng, [1, 15, 16, 17, 300], [(37, 0), (5, 40), (64, 1000)])
+        parts = bench.algorithmic(cfg, b)
+        flops, dec_bytes, pre_bytes = brute_attention(cfg, b)
+        a = parts["attention"]
+        assert a["flops"] == flops
+        assert a["decode_bytes"] == dec_bytes
+        assert a["bytes"] == dec_bytes + pre_bytes
+        T, H, F = b.T, cfg.hidden, cfg.ffn
+        nqd = cfg.n_q_heads * cfg.head_dim
+        qkv = nqd + 2 * cfg.n_kv_heads * cfg.head_dim
+        # each projection: 2 M N K flops; weights, input rows and output rows
+        # once (bf16), plus the residual rows of the O and down projections
+        for name, (N, K, n_out, res) in {"qkv": (qkv, H, qkv, 0), "o": (H, nqd, H, 1),
+                                         "gate_up": (2 * F, H, F, 0),
+                                         "down": (H, F, H, 1)}.items():
+            assert parts[name]["flops"] == 2.0 * T * N * K
+            assert parts[name]["bytes"] == 2.0 * (N * K + T * K + T * n_out) + res * 2.0 * T * N
