@@ -202,10 +202,11 @@ mx_status mx_paged_attn(const mx_batch* batch, const mx_attn_shape* shape, const
  * kernels and the same results, bit for bit, with the call's metadata and
  * split partials in a static device array of mx_paged_attn_static_max_bytes()
  * bytes (32 MiB) that the library holds on every GPU it runs on until the
- * process ends.  Allocates no device, pinned or host memory per call: the
- * metadata is packed into a static host buffer of the library and copied into
- * the array with hipMemcpyAsync on the stream, which HIP performs synchronously
- * from pageable memory (the call returns once the copy has run).  The copy
+ * process ends.  Allocates no device or pinned memory (the host-side plan
+ * uses ordinary heap memory): the metadata is packed into a static host buffer
+ * of the library and copied into the array with hipMemcpyAsync on the stream,
+ * which HIP performs synchronously from pageable memory (the call returns once
+ * the copy has run).  The copy
  * reads that host buffer when it runs, so the call is not meant for HIP graph
  * capture (a captured copy would read whatever a later call packed there).
  * A batch whose metadata and partials
