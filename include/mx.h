@@ -206,10 +206,9 @@ mx_status mx_paged_attn(const mx_batch* batch, const mx_attn_shape* shape, const
  * uses ordinary heap memory): the metadata is packed into a static host buffer
  * of the library and copied into the array with hipMemcpyAsync on the stream,
  * which HIP performs synchronously from pageable memory (the call returns once
- * the copy has run).  The copy
- * reads that host buffer when it runs, so the call is not meant for HIP graph
- * capture (a captured copy would read whatever a later call packed there).
- * A batch whose metadata and partials
+ * the copy has run).  The copy reads that host buffer when it runs, so the
+ * call is not meant for HIP graph capture (a captured copy would read
+ * whatever a later call packed there).  A batch whose metadata and partials
  * need more than the array holds returns MX_ERR_TOO_LARGE before any device
  * work.  All calls on one GPU share that GPU's array: calls that overlap on one
  * GPU (different streams, or threads without ordering) race; calls ordered on
