@@ -442,28 +442,38 @@ def chunk_sweep(args, key, cfg, packed):
                                       "fit_attention_us_per_chunk_index": fit_attn}}))
 
 
-def predictor_fit(args, key, cfg, packed):
-    """Fit of the iteration-latency model to measured steps of random batches
-    (held-out residuals test how predictable the mixed iteration is)."""
+def predictor_batches(key, n):
+    """The random batches the latency model is fitted on, in order (seeded):
+    (record, batch) with 8-256 decodes at contexts U[64, 4096] and a chunk of
+    0-4096 tokens after 0-4096 cached ones."""
     import numpy as np
     import workload as wl
-    from paper_2606_16264_amd.sched import LatencyModel, batch_features
     rng = np.random.default_rng(2024)
     max_dec = 256
-    feats, lat, recs = [], [], []
-    for i in range(args.predictor):
+    for _ in range(n):
         n_dec = int(rng.integers(8, max_dec + 1))
         dec_ctx = [int(c) for c in rng.integers(64, 4097, size=n_dec)]
         P = int(rng.choice([0, 0, 128, 512, 1024, 2048, 4096]))
         pctx = int(rng.choice([0, 0, 1024, 4096])) if P else 0
         b = wl.make_batch(key, P, decode_ctx=dec_ctx, prefill_lens=[P] if P else [],
                           prefill_ctx=[pctx] if P else [])
+        yield dict(n_decode=n_dec, P=P, prefill_ctx=pctx, T=int(b.T)), b
+
+
+def predictor_fit(args, key, cfg, packed):
+    """Fit of the iteration-latency model to measured steps of random batches
+    (held-out residuals test how predictable the mixed iteration is)."""
+    import workload as wl
+    from paper_2606_16264_amd.sched import LatencyModel, batch_features
+    feats, lat, recs = [], [], []
+    for i, (rec, b) in enumerate(predictor_batches(key, args.predictor)):
+        P = rec["P"]
         pt = Point(key, P, None, packed, cfg, batch=b)
         ms, _ = time_fn(pt.step, args.steps, args.warmup)
         f = batch_features(b.n_new, b.ctx_len, b.phase == wl.DECODE)
         feats.append(f)
         lat.append(ms * 1e3)
-        recs.append(dict(n_decode=n_dec, P=P, prefill_ctx=pctx, T=int(b.T), us=round(ms * 1e3, 2)))
+        recs.append(dict(rec, us=round(ms * 1e3, 2)))
         print(f"# sample {i}: {recs[-1]}", file=sys.stderr, flush=True)
         pt.release()
     train = list(range(0, len(lat), 2))

@@ -188,3 +188,35 @@ def test_light_load_meets_every_slo():
     for prefill_workers in (1, 2, 3):
         res = Simulator(model, Cluster(workers=4, prefill_workers=prefill_workers), slo).run(reqs)
         assert res["attainment"] == 1.0, (prefill_workers, res)
+
+
+# ---------------------------------------------------------------- committed fits
+@pytest.mark.parametrize("key", ["c2", "c4"])
+def test_committed_latency_model_refits_from_its_samples(key):
+    """The fitted latency model in profiles/ follows from its own recorded
+    samples: the seeded batches regenerate with the recorded sizes, and a refit
+    on their features and the recorded latencies (even samples; odd ones held
+    out) predicts what the committed coefficients predict, with the committed
+    held-out error."""
+    import json
+    import os
+
+    import bench
+    import workload as wl
+    path = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "profiles",
+                        f"latency_model_layer_step_{key}.json")
+    rec = json.load(open(path))["latency_model"]
+    samples = rec["samples"]
+    feats = []
+    for s, (r, b) in zip(samples, bench.predictor_batches(key, len(samples))):
+        assert {k: s[k] for k in r} == r
+        feats.append(batch_features(b.n_new, b.ctx_len, b.phase == wl.DECODE))
+    lat = [s["us"] for s in samples]
+    train, test = list(range(0, len(lat), 2)), list(range(1, len(lat), 2))
+    m = LatencyModel.fit([feats[i] for i in train], [lat[i] for i in train])
+    committed = LatencyModel.from_dict(rec["coef_us"])
+    got, want = m.predict(np.array(feats)), committed.predict(np.array(feats))
+    assert np.max(np.abs(got - want) / np.array(lat)) < 1e-3
+    held = m.residuals([feats[i] for i in test], [lat[i] for i in test])
+    assert held["median_abs_rel"] == pytest.approx(rec["held_out_residuals"]["median_abs_rel"],
+                                                   abs=1e-3)
