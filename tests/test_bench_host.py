@@ -1,12 +1,14 @@
 """Host logic of bench.py on the CPU: the one-GPU guard, the simulator leg's
 JSON line, and the algorithmic byte and flop counts behind the roofline
-fractions, checked against per-row brute force."""
+fractions, checked against per-row brute force; the committed chunk sweep
+against its own points."""
 import json
 import os
 import subprocess
 import sys
 
 import numpy as np
+import pytest
 
 import bench
 import workload as wl
@@ -85,3 +87,28 @@ def test_algorithmic_counts_match_brute_force():
                                          "down": (H, F, H, 1)}.items():
             assert parts[name]["flops"] == 2.0 * T * N * K
             assert parts[name]["bytes"] == 2.0 * (N * K + T * K + T * n_out) + res * 2.0 * T * N
+
+
+def test_committed_chunk_sweep_follows_from_its_points():
+    """profiles/chunk_sweep_layer_step_c4.json: chunk k continues a prompt with
+    k chunks cached; its prefill attention flops are the per-row sum over the
+    chunk's rows, and both recorded line fits refit from the recorded points."""
+    rec = json.load(open(os.path.join(ROOT, "profiles", "chunk_sweep_layer_step_c4.json")))
+    sw = rec["chunk_sweep"]
+    cfg = wl.CONFIGS["c4"]
+    C = sw["chunk"]
+    pts = sw["points"]
+    for p in pts:
+        assert p["ctx"] == p["k"] * C and p["T"] == 256 + C
+        rows = p["ctx"] + np.arange(C, dtype=np.float64)  # positions of the chunk's rows
+        assert p["prefill_attn_flops"] == float((4.0 * cfg.n_q_heads * cfg.head_dim * (rows + 1)).sum())
+    k = np.array([p["k"] for p in pts], dtype=np.float64)
+    for field, fit in (("us", sw["fit_us_per_chunk_index"]),
+                       ("attn_us", sw["fit_attention_us_per_chunk_index"])):
+        y = np.array([p[field] for p in pts])
+        slope, icpt = np.polyfit(k, y, 1)
+        r2 = 1.0 - ((y - (slope * k + icpt)) ** 2).sum() / ((y - y.mean()) ** 2).sum()
+        assert fit["points"] == len(pts)
+        assert slope == pytest.approx(fit["slope_us_per_chunk_index"], abs=1e-3)
+        assert icpt == pytest.approx(fit["intercept_us"], abs=1e-2)
+        assert r2 == pytest.approx(fit["r2"], abs=1e-4)
