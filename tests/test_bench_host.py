@@ -112,3 +112,31 @@ def test_committed_chunk_sweep_follows_from_its_points():
         assert slope == pytest.approx(fit["slope_us_per_chunk_index"], abs=1e-3)
         assert icpt == pytest.approx(fit["intercept_us"], abs=1e-2)
         assert r2 == pytest.approx(fit["r2"], abs=1e-4)
+
+
+def test_committed_traffic_summaries_are_consistent():
+    """Every profiles/traffic_*.json: the copy calibration scales the counters
+    (bytes of the 1 GiB copy over what each counter read for it), the per-launch
+    bytes are the scaled counter means, and the algorithmic bytes beside them
+    are the kernel's part of the workload it names."""
+    paths = sorted(p for p in os.listdir(os.path.join(ROOT, "profiles"))
+                   if p.startswith("traffic_") and p.endswith(".json"))
+    assert paths
+    for name in paths:
+        rec = json.load(open(os.path.join(ROOT, "profiles", name)))
+        cal = rec["copy_calibration"]
+        fs = cal["bytes"] / (cal["FETCH_SIZE_KiB"] * 1024.0)
+        ws = cal["bytes"] / (cal["WRITE_SIZE_KiB"] * 1024.0)
+        assert cal["fetch_scale"] == pytest.approx(fs, abs=1e-4)
+        assert cal["write_scale"] == pytest.approx(ws, abs=1e-4)
+        # the recorded means are rounded to 0.1 KiB
+        fetch = rec["FETCH_SIZE_KiB_mean"] * 1024.0 * fs
+        write = rec["WRITE_SIZE_KiB_mean"] * 1024.0 * ws
+        assert rec["fetch_bytes_per_launch"] == pytest.approx(fetch, abs=0.05 * 1024 * fs + 1)
+        assert rec["write_bytes_per_launch"] == pytest.approx(write, abs=0.05 * 1024 * ws + 1)
+        assert rec["hbm_bytes_per_launch"] == pytest.approx(
+            rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"], abs=1)
+        key, P = rec["workload"].split("_P")
+        part, _ = bench.TRAFFIC_TAGS[rec["tag"]]
+        parts = bench.algorithmic(wl.CONFIGS[key], wl.make_batch(key, int(P)))
+        assert rec["algorithmic_bytes_per_launch"] == int(parts[part]["bytes"])
