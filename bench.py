@@ -516,6 +516,9 @@ def main():
                             "outputs lognormal(median 128, sigma 0.8) in [1, 1024]")
         print(json.dumps(res))
         return
+    if args.predictor and args.predictor < 12:
+        sys.exit("--predictor needs at least 12 batches: the model's six coefficients are fitted "
+                 "on the even-numbered half")
     if args.gpus != 1:
         print(json.dumps({"error": "the layer step runs on one GPU; --gpus must be 1 "
                                    "(there is no multi-GPU path)"}))

@@ -140,3 +140,9 @@ def test_committed_traffic_summaries_are_consistent():
         part, _ = bench.TRAFFIC_TAGS[rec["tag"]]
         parts = bench.algorithmic(wl.CONFIGS[key], wl.make_batch(key, int(P)))
         assert rec["algorithmic_bytes_per_launch"] == int(parts[part]["bytes"])
+
+
+def test_too_few_predictor_batches_are_refused_before_any_gpu_work():
+    r = run_bench("--predictor", "4")
+    assert r.returncode != 0
+    assert "at least 12" in r.stderr
