@@ -148,44 +148,50 @@ __device__ __forceinline__ int64_t lane_slot(int64_t s, int l) {  // s of lane l
   return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
 }
 
-template <int MB, int NB>
-__device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MB][NB], int M, int N, int r0,
+template <int MA, int NQ>
+__device__ __forceinline__ void qkv_epilogue(const f32x4 (&acc)[MA][NQ], int M, int N, int r0,
                                              int c0, int lane, const float2* __restrict__ rope_cs,
                                              const int64_t* __restrict__ tok_slot,
                                              uint16_t* __restrict__ q_out,
                                              uint16_t* __restrict__ k_pool,
                                              uint16_t* __restrict__ v_pool, int nq, int nkv,
                                              int hd, MX_LDS uint16_t* st) {
-  static_assert(NB == 2, "one 64-column group per wave");
+  static_assert(NQ == 4, "one 64-column group per wave");
   if (c0 >= N) return;  // (wave-uniform)
-  const int ccol = lane & 31, crow = 4 * (lane >> 5);
+  // accumulator layout: block (a, j) holds rows 16 a + crow .. + 3 of column
+  // 16 j + ccol in this lane
+  const int ccol = lane & 15, crow = 4 * (lane >> 4);
   const int head = c0 / hd, within0 = c0 % hd;
   const bool is_v = head >= nq + nkv, is_q = head < nq;
   // dims of the low and high 32-column blocks (q / k: the packed rotary halves)
   const int d_lo = is_v ? within0 : 32 * (within0 / 64);
   const int d_hi = is_v ? within0 + 32 : d_lo + hd / 2;
 #pragma unroll
-  for (int i = 0; i < MB; i++) {
+  for (int i = 0; i < MA / 2; i++) {  // 32-row blocks: accumulator rows 2 i, 2 i + 1
     const int rb = r0 + i * 32;
-    // 1. reads: the slot of token rb + lane % 32, the (cos, sin) of this lane's rows
+    // 1. reads: the slot of token rb + lane % 32, the (cos, sin) of this lane's
+    // elements (rows 16 h + crow + v, low columns 16 j + ccol, h, j < 2)
     const int64_t myslot = tok_slot[min(rb + (lane & 31), M - 1)];
     float2 cs[16];
     if (!is_v) {
 #pragma unroll
-      for (int r = 0; r < 16; r++) {
-        const int row = min(rb + 8 * (r >> 2) + crow + (r & 3), M - 1);
-        cs[r] = rope_cs[(int64_t)row * (hd / 2) + d_lo + ccol];
+      for (int e = 0; e < 16; e++) {
+        const int h = e >> 3, j = (e >> 2) & 1, v = e & 3;
+        const int row = min(rb + 16 * h + crow + v, M - 1);
+        cs[e] = rope_cs[(int64_t)row * (hd / 2) + d_lo + 16 * j + ccol];
       }
     }
     __builtin_amdgcn_sched_barrier(0);
     if (!is_v) {
       // 2. rotate, round, stage token-major: [token][low 32 dims, high 32 dims]
+      // (a pair's halves are columns c and c + 32: blocks j and j + 2, same lane)
 #pragma unroll
-      for (int r = 0; r < 16; r++) {
-        const int t = 8 * (r >> 2) + crow + (r & 3);
-        const float lo = acc[i][0][r], hi = acc[i][1][r];
-        st[t * kQkRow + ccol] = f32_to_bf16(lo * cs[r].x - hi * cs[r].y);
-        st[t * kQkRow + 32 + ccol] = f32_to_bf16(hi * cs[r].x + lo * cs[r].y);
+      for (int e = 0; e < 16; e++) {
+        const int h = e >> 3, j = (e >> 2) & 1, v = e & 3;
+        const int t = 16 * h + crow + v, c = 16 * j + ccol;
+        const float lo = acc[2 * i + h][j][v], hi = acc[2 * i + h][j + 2][v];
+        st[t * kQkRow + c] = f32_to_bf16(lo * cs[e].x - hi * cs[e].y);
+        st[t * kQkRow + 32 + c] = f32_to_bf16(hi * cs[e].x + lo * cs[e].y);
       }
       lgkm_wait<0>();  // (and no access below moves above the staging)
       // 3. read back token (lane / 8) + 8 q, dims 8 (lane % 8) .. + 7 of the 64
@@ -213,15 +219,16 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MB][NB], int M,
       }
     } else {
       // 2. stage dim-major: [dim (low 32, high 32)][token]; this lane's four
-      // consecutive tokens of a row group are one 8-byte write
+      // consecutive tokens of a block are one 8-byte write
 #pragma unroll
-      for (int k = 0; k < 4; k++)
+      for (int h = 0; h < 2; h++)
 #pragma unroll
-        for (int j = 0; j < 2; j++) {
+        for (int j = 0; j < 4; j++) {
+          const f32x4 a = acc[2 * i + h][j];
           u32x2 w;
-          w[0] = pack_bf16x2(acc[i][j][4 * k], acc[i][j][4 * k + 1]);
-          w[1] = pack_bf16x2(acc[i][j][4 * k + 2], acc[i][j][4 * k + 3]);
-          *reinterpret_cast<MX_LDS u32x2*>(st + (32 * j + ccol) * kVRow + 8 * k + crow) = w;
+          w[0] = pack_bf16x2(a[0], a[1]);
+          w[1] = pack_bf16x2(a[2], a[3]);
+          *reinterpret_cast<MX_LDS u32x2*>(st + (16 * j + ccol) * kVRow + 16 * h + crow) = w;
         }
       lgkm_wait<0>();
       // runs: token t starts one where its slot is a multiple of 8 and token
@@ -280,13 +287,14 @@ constexpr int kStageRowSw = 32 + 4;            // SwiGLU: 32 output columns per 
 // first, then per 32-row block the staging, the sums rounded to bf16 and the
 // stores.  Rows whose stride is not a multiple of 8 elements, and the columns
 // at the N edge, take 2-byte accesses.  R must not overlap C.
-template <int MB, int NB, bool RESIDUAL>
-__device__ __forceinline__ void store_epilogue(const f32x16 (&acc)[MB][NB], int M, int N, int r0,
+template <int MA, int NQ, bool RESIDUAL>
+__device__ __forceinline__ void store_epilogue(const f32x4 (&acc)[MA][NQ], int M, int N, int r0,
                                                int c0, int lane, const uint16_t* __restrict__ R,
                                                int ldr, uint16_t* __restrict__ C, int ldc,
                                                MX_LDS float* st) {
-  static_assert(NB == 2, "the staging holds 64 columns per wave");
-  const int ccol = lane & 31, crow = 4 * (lane >> 5);
+  static_assert(NQ == 4, "the staging holds 64 columns per wave");
+  constexpr int MB = MA / 2;  // 32-row blocks
+  const int ccol = lane & 15, crow = 4 * (lane >> 4);  // accumulator layout
   const int rq = lane >> 3, col = c0 + 8 * (lane & 7);  // read-back: rows rq + 8 q, 8 columns
   const bool vec = ldc % 8 == 0 && (!RESIDUAL || ldr % 8 == 0) && col + 8 <= N;
   u32x4 res[MB][4];
@@ -311,10 +319,12 @@ __device__ __forceinline__ void store_epilogue(const f32x16 (&acc)[MB][NB], int 
 #pragma unroll
   for (int i = 0; i < MB; i++) {
 #pragma unroll
-    for (int r = 0; r < 16; r++)
+    for (int h = 0; h < 2; h++)
 #pragma unroll
-      for (int j = 0; j < NB; j++)
-        st[(8 * (r >> 2) + crow + (r & 3)) * kStageRow + j * 32 + ccol] = acc[i][j][r];
+      for (int v = 0; v < 4; v++)
+#pragma unroll
+        for (int j = 0; j < NQ; j++)
+          st[(16 * h + crow + v) * kStageRow + 16 * j + ccol] = acc[2 * i + h][j][v];
     lgkm_wait<0>();  // (and no access below moves above the staging)
     u32x4 out[4];
 #pragma unroll
@@ -350,21 +360,23 @@ __device__ __forceinline__ void store_epilogue(const f32x16 (&acc)[MB][NB], int 
 // The fp32 partial sums of one K split, through the same staging: 8
 // consecutive columns of one row per lane and run, two 16-byte stores (rows
 // of N % 4 != 0 floats, and the columns at the N edge, take 4-byte stores).
-template <int MB, int NB>
-__device__ __forceinline__ void split_epilogue(const f32x16 (&acc)[MB][NB], int M, int N, int r0,
+template <int MA, int NQ>
+__device__ __forceinline__ void split_epilogue(const f32x4 (&acc)[MA][NQ], int M, int N, int r0,
                                                int c0, int lane, float* __restrict__ P,
                                                MX_LDS float* st) {
-  static_assert(NB == 2, "the staging holds 64 columns per wave");
-  const int ccol = lane & 31, crow = 4 * (lane >> 5);
+  static_assert(NQ == 4, "the staging holds 64 columns per wave");
+  const int ccol = lane & 15, crow = 4 * (lane >> 4);  // accumulator layout
   const int rq = lane >> 3, col = c0 + 8 * (lane & 7);
   const bool vec = N % 4 == 0 && col + 8 <= N;
 #pragma unroll
-  for (int i = 0; i < MB; i++) {
+  for (int i = 0; i < MA / 2; i++) {
 #pragma unroll
-    for (int r = 0; r < 16; r++)
+    for (int h = 0; h < 2; h++)
 #pragma unroll
-      for (int j = 0; j < NB; j++)
-        st[(8 * (r >> 2) + crow + (r & 3)) * kStageRow + j * 32 + ccol] = acc[i][j][r];
+      for (int v = 0; v < 4; v++)
+#pragma unroll
+        for (int j = 0; j < NQ; j++)
+          st[(16 * h + crow + v) * kStageRow + 16 * j + ccol] = acc[2 * i + h][j][v];
     lgkm_wait<0>();
     f32x4 lo[4], hi[4];
 #pragma unroll
@@ -396,19 +408,25 @@ __device__ __forceinline__ void split_epilogue(const f32x16 (&acc)[MB][NB], int 
 // blocks of gate and up of the same 32 features; the 32 outputs (columns
 // c0 / 2 ..) go to C row-major or, c_tiled, in the projection-input tile
 // layout, through the same staging as above (ldc a multiple of 32).
-template <int MB, int NB>
-__device__ __forceinline__ void swiglu_epilogue(const f32x16 (&acc)[MB][NB], int M, int N, int r0,
+template <int MA, int NQ>
+__device__ __forceinline__ void swiglu_epilogue(const f32x4 (&acc)[MA][NQ], int M, int N, int r0,
                                                 int c0, int lane, uint16_t* __restrict__ C,
                                                 int ldc, bool c_tiled, MX_LDS float* st) {
-  static_assert(NB == 2, "one gate/up pair per wave");
-  const int ccol = lane & 31, crow = 4 * (lane >> 5);
+  static_assert(NQ == 4, "one gate/up pair per wave");
+  // accumulator layout; gate column c pairs with up column c + 32 (blocks j, j + 2)
+  const int ccol = lane & 15, crow = 4 * (lane >> 4);
   const int rq = lane >> 2, col = c0 / 2 + 8 * (lane & 3);  // read-back: rows rq + 16 q
   if (c0 >= N) return;  // (wave-uniform)
 #pragma unroll
-  for (int i = 0; i < MB; i++) {
+  for (int i = 0; i < MA / 2; i++) {
 #pragma unroll
-    for (int r = 0; r < 16; r++)
-      st[(8 * (r >> 2) + crow + (r & 3)) * kStageRowSw + ccol] = silu(acc[i][0][r]) * acc[i][1][r];
+    for (int h = 0; h < 2; h++)
+#pragma unroll
+      for (int v = 0; v < 4; v++)
+#pragma unroll
+        for (int j = 0; j < 2; j++)
+          st[(16 * h + crow + v) * kStageRowSw + 16 * j + ccol] =
+              silu(acc[2 * i + h][j][v]) * acc[2 * i + h][j + 2][v];
     lgkm_wait<0>();
     u32x4 out[2];
 #pragma unroll
@@ -436,15 +454,18 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
                                                                            int k_chunks) {
   constexpr int WAVES_N = BN / WN;
   constexpr int NWAVES = (BM / WM) * WAVES_N;
-  constexpr int MB = WM / 32, NB = WN / 32;
+  // 16 x 16 output blocks of v_mfma_f32_16x16x32_bf16: MA rows of them per
+  // wave, NQ columns; a slice (32 of K) is one product per block
+  constexpr int MA = WM / 16, NQ = WN / 16, MH = MA / 2;
   constexpr int ROWB = BKS * 2;                // bytes of one tile row in a stage (64)
   constexpr int STAGE = (BM + BN) * ROWB;      // bytes per LDS stage
   constexpr int L = STAGE / 1024 / NWAVES;     // DMA instructions per wave per stage
   static_assert(L * NWAVES * 1024 == STAGE, "stage does not split into whole DMA rows");
   constexpr int VM_KEEP = (NS - 2) * L;        // in flight after the oldest stage landed
-  constexpr int NREAD = MB + NB;               // fragment reads per k-step
-  static_assert((EPI != EPI_SWIGLU && EPI != EPI_QKV) || NB % 2 == 0,
-                "SwiGLU and the QKV epilogue need pairs of 32-column blocks");
+  constexpr int NR0 = NQ + MH;                 // fragment reads of phase 0 (B, first A half)
+  constexpr int NR1 = MH;                      // fragment reads of phase 1 (second A half)
+  static_assert(MA % 2 == 0 && NQ == 4, "two A halves; 64 columns per wave");
+  static_assert(NR0 + NR1 <= 15, "lgkmcnt range");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const unsigned sbase = (unsigned)(size_t)(MX_LDS char*)smem;
 
@@ -502,97 +523,111 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
     if (st < nk - 1) dsrc[i] += dstep[i];
   };
 
-  f32x16 acc[MB][NB];
+  f32x4 acc[MA][NQ];
 #pragma unroll
-  for (int i = 0; i < MB; i++)
+  for (int i = 0; i < MA; i++)
 #pragma unroll
-    for (int j = 0; j < NB; j++)
-#pragma unroll
-      for (int r = 0; r < 16; r++) acc[i][j][r] = 0.f;
+    for (int j = 0; j < NQ; j++) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int frow = lane & 31, fk = lane >> 5;
-  unsigned aoff[MB], boff[NB];
+  // A fragment of 16-row block a: lane l holds row 16 a + l % 16, logical
+  // chunk l / 16 (8 of the slice's 32 K values); B likewise for its columns
+  const int frow = lane & 15, fk = lane >> 4;
+  unsigned aoff[MA], boff[NQ];
 #pragma unroll
-  for (int i = 0; i < MB; i++) {
-    const int r = wave_m * WM + i * 32 + frow;
+  for (int i = 0; i < MA; i++) {
+    const int r = wave_m * WM + i * 16 + frow;
     aoff[i] = r * ROWB + (((unsigned)fk ^ swz(r)) << 4);
   }
 #pragma unroll
-  for (int j = 0; j < NB; j++) {
-    const int r = wave_n * WN + j * 32 + frow;
+  for (int j = 0; j < NQ; j++) {
+    const int r = wave_n * WN + j * 16 + frow;
     boff[j] = (BM + r) * ROWB + (((unsigned)fk ^ swz(r)) << 4);
   }
-  // k-step ks of a stage reads logical chunk 2 ks + fk; the XOR with the row
-  // term commutes with the +2 (bit 1 only), so ks = 1 is the base ^ 32 bytes
-  u32x4 fa[2][MB], fb[2][NB];
-  // fragment read r (A rows first, then B) of k-step ks of stage st into buffer buf
-  auto read_one = [&](int buf, int st, int ks, int r) {
+  // A slice runs in two phases, the first and second half of the wave's A
+  // blocks against all its B blocks: fa0 and fa1 hold the two halves, fb[p]
+  // the B fragments of slices of parity p (the next slice's arrive while the
+  // second phase still uses this one's).
+  u32x4 fa0[MH], fa1[MH], fb[2][NQ];
+  // phase-0 fragment r of slice st (B first, then the first A half), into fb[p]
+  auto read0 = [&](int p, int st, int r) {
     const unsigned slot = sbase + (unsigned)((st % NS) * STAGE);
-    const unsigned kx = ks ? 32u : 0u;
-    if (r < MB)
-      fa[buf][r] = lds_read16(slot + (aoff[r] ^ kx));
+    if (r < NQ)
+      fb[p][r] = lds_read16(slot + boff[r]);
     else
-      fb[buf][r - MB] = lds_read16(slot + (boff[r - MB] ^ kx));
+      fa0[r - NQ] = lds_read16(slot + aoff[r - NQ]);
   };
-  constexpr int NM = MB * NB;  // MFMAs per k-step
-  auto mfma_one = [&](int buf, int idx) {
-    const int i = idx / NB, j = idx % NB;
-    acc[i][j] = mfma32(as_bf16x8(fa[buf][i]), as_bf16x8(fb[buf][j]), acc[i][j]);
+  // phase-1 fragment r of slice st (the second A half)
+  auto read1 = [&](int st, int r) {
+    const unsigned slot = sbase + (unsigned)((st % NS) * STAGE);
+    fa1[r] = lds_read16(slot + aoff[MH + r]);
+  };
+  constexpr int NM = MH * NQ;  // MFMAs per phase
+  auto mfma0 = [&](int p, int idx) {
+    const int i = idx / NQ, j = idx % NQ;
+    acc[i][j] = mfma16(as_bf16x8(fa0[i]), as_bf16x8(fb[p][j]), acc[i][j]);
+  };
+  auto mfma1 = [&](int p, int idx) {
+    const int i = idx / NQ, j = idx % NQ;
+    acc[MH + i][j] = mfma16(as_bf16x8(fa1[i]), as_bf16x8(fb[p][j]), acc[MH + i][j]);
   };
 
-  // One slice: its two k-steps.  The MFMAs of each k-step go out one at a
-  // time, with the slice's memory instructions spread between them (the DMA
-  // of slice kt + NS - 1 among the first k-step's, the next slice's first
-  // fragment reads among the second's), so that a wave keeps the matrix core
-  // fed while it issues them: with the instructions in bursts, the two waves
-  // of a SIMD, lined up by the barrier, issued theirs at the same time and
-  // the matrix core idled meanwhile.  `more` issues the fragment reads of the
-  // next slice's first k-step.  The last slice must not: the compiler sees the
-  // result of a read that is never consumed as dead and may hand its registers
-  // to the epilogue while the read is still in flight, and the landing data
-  // would then overwrite them.
-  auto slice = [&](int kt, bool more) {
+  // One slice (p = kt % 2, a constant at every call): its two phases.  The
+  // MFMAs of each phase go out one at a time, with the slice's memory
+  // instructions spread between them (the DMA of slice kt + NS - 1 among the
+  // first phase's, the next slice's phase-0 fragment reads among the
+  // second's), so that a wave keeps the matrix core fed while it issues them:
+  // with the instructions in bursts, the two waves of a SIMD, lined up by the
+  // barrier, issued theirs at the same time and the matrix core idled
+  // meanwhile.  `more` issues the fragment reads of the next slice's first
+  // phase.  The last slice must not: the compiler sees the result of a read
+  // that is never consumed as dead and may hand its registers to the epilogue
+  // while the read is still in flight, and the landing data would then
+  // overwrite them.
+  auto slice = [&](int kt, bool more, auto parity) {
+    constexpr int p = decltype(parity)::value;
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int r = 0; r < NREAD; r++) read_one(1, kt, 1, r);
-    lgkm_wait<NREAD>();  // the k-step 0 fragments (older reads) have landed
-    pin(fa[0]);
-    pin(fb[0]);
+    for (int r = 0; r < NR1; r++) read1(kt, r);
+    lgkm_wait<NR1>();  // the phase-0 fragments (older reads) have landed
+    pin(fa0);
+    pin(fb[p]);
     // slot (kt + NS - 1) % NS was last read in slice kt - 1, before its barrier
 #pragma unroll
     for (int idx = 0; idx < NM; idx++) {
-      mfma_one(0, idx);
+      mfma0(p, idx);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < L; i++)
         if (i * NM / L == idx) dma_one(i, kt + NS - 1);
       __builtin_amdgcn_sched_barrier(0);
     }
-    // (both fragment buffers stay live across each k-step, so that no read's
-    // destination is a register an MFMA of the k-step took as a source)
-    pin(fa[0]);
-    pin(fb[0]);
+    // (every fragment buffer of a phase stays live across it, so that no
+    // read's destination is a register an MFMA of the phase took as a source)
+    pin(fa0);
+    pin(fb[p]);
     // own DMA of stage kt + 1 landed, own reads of stage kt done; after the
     // barrier everyone's are, so stage kt + 1 is readable and slot kt % NS free
     vm_wait<VM_KEEP>();
     lgkm_wait<0>();
-    pin(fa[1]);
-    pin(fb[1]);
+    pin(fa1);
+    pin(fb[p]);
     wg_barrier();
 #pragma unroll
     for (int idx = 0; idx < NM; idx++) {
-      mfma_one(1, idx);
+      mfma1(p, idx);
       __builtin_amdgcn_sched_barrier(0);
       if (more) {
 #pragma unroll
-        for (int r = 0; r < NREAD; r++)
-          if (r * NM / NREAD == idx) read_one(0, kt + 1, 0, r);
+        for (int r = 0; r < NR0; r++)
+          if (r * NM / NR0 == idx) read0(p ^ 1, kt + 1, r);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
-    pin(fa[1]);
-    pin(fb[1]);
+    pin(fa1);
+    pin(fb[p]);
   };
+  using P0 = std::integral_constant<int, 0>;
+  using P1 = std::integral_constant<int, 1>;
 
 #pragma unroll
   for (int st = 0; st < NS - 1; st++)
@@ -601,9 +636,14 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   vm_wait<VM_KEEP>();
   wg_barrier();
 #pragma unroll
-  for (int r = 0; r < NREAD; r++) read_one(0, 0, 0, r);
-  for (int kt = 0; kt < nk - 1; kt++) slice(kt, true);
-  slice(nk - 1, false);
+  for (int r = 0; r < NR0; r++) read0(0, 0, r);
+  // nk is even (K is a multiple of 64), so slices pair up by parity
+  for (int kt = 0; kt < nk - 2; kt += 2) {
+    slice(kt, true, P0{});
+    slice(kt + 1, true, P1{});
+  }
+  slice(nk - 2, true, P0{});
+  slice(nk - 1, false, P1{});
   // drain: no DMA may still target this workgroup's LDS when it exits (no
   // fragment read is outstanding: the last slice waited for all of them)
   vm_wait<0>();
@@ -615,7 +655,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
     MX_LDS uint16_t* st =
         reinterpret_cast<MX_LDS uint16_t*>((MX_LDS char*)smem) + wave_s * kQkvStageHalves;
     const QkvEpilogue& e = a.qkv;
-    qkv_epilogue<MB, NB>(acc, a.M, a.N, m0 + wave_m * WM, n0 + wave_n * WN, lane, e.rope_cs,
+    qkv_epilogue<MA, NQ>(acc, a.M, a.N, m0 + wave_m * WM, n0 + wave_n * WN, lane, e.rope_cs,
                          e.tok_slot, e.q_out, e.k_pool, e.v_pool, e.nq, e.nkv, e.head_dim, st);
     return;
   }
@@ -624,10 +664,10 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
     wg_barrier();  // every wave is done reading the ring
     MX_LDS float* st = reinterpret_cast<MX_LDS float*>((MX_LDS char*)smem) + wave_s * kStageFloats;
     if constexpr (EPI == EPI_SWIGLU)
-      swiglu_epilogue<MB, NB>(acc, a.M, a.N, m0 + wave_m * WM, n0 + wave_n * WN, lane, a.C, a.ldc,
+      swiglu_epilogue<MA, NQ>(acc, a.M, a.N, m0 + wave_m * WM, n0 + wave_n * WN, lane, a.C, a.ldc,
                               a.c_tiled != 0, st);
     else
-      store_epilogue<MB, NB, EPI == EPI_RESIDUAL>(acc, a.M, a.N, m0 + wave_m * WM,
+      store_epilogue<MA, NQ, EPI == EPI_RESIDUAL>(acc, a.M, a.N, m0 + wave_m * WM,
                                                   n0 + wave_n * WN, lane, a.R, a.ldr, a.C, a.ldc,
                                                   st);
     return;
@@ -636,7 +676,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
     static_assert(NWAVES * kStageFloats * 4 <= NS * STAGE, "the staging does not fit the ring");
     wg_barrier();
     MX_LDS float* st = reinterpret_cast<MX_LDS float*>((MX_LDS char*)smem) + wave_s * kStageFloats;
-    split_epilogue<MB, NB>(acc, a.M, a.N, m0 + wave_m * WM, n0 + wave_n * WN, lane,
+    split_epilogue<MA, NQ>(acc, a.M, a.N, m0 + wave_m * WM, n0 + wave_n * WN, lane,
                            a.partial + (int64_t)kz * a.M * a.N, st);
   }
 }
