@@ -4,7 +4,9 @@
 //
 // Design:
 //  - workgroup tile BM x BN, K step 64; waves of 64 lanes each own a WM x WN
-//    sub-tile computed with v_mfma_f32_32x32x16_bf16;
+//    sub-tile computed with v_mfma_f32_16x16x32_bf16 (one product per 16 x 16
+//    block and 32-wide K slice: under the chip's power limit it sustains a
+//    higher rate than the 32 x 32 x 16 form, for the same LDS reads);
 //  - K is consumed in 32-wide slices through an LDS ring (4 stages; 3 for the
 //    shape that puts two workgroups on a CU) filled by the DMA path
 //    (global_load_lds): the other slices are in flight while the matrix cores
@@ -12,10 +14,11 @@
 //  - B is addressed through block, row and K-slice strides: row-major, or the
 //    packed weights' 16 x 32 tiles of 1 KB, where each DMA instruction reads
 //    one contiguous kilobyte;
-//  - each k-step's MFMAs are issued one at a time, with the slice's DMA issues
-//    (first k-step) and the next slice's fragment reads (second k-step) spread
-//    between them, so that a wave keeps the matrix core fed while it issues
-//    its memory instructions; one barrier per slice;
+//  - a slice runs in two phases (the two halves of the wave's A blocks against
+//    all its B blocks); each phase's MFMAs are issued one at a time, with the
+//    slice's DMA issues (first phase) and the next slice's fragment reads
+//    (second phase) spread between them, so that a wave keeps the matrix core
+//    fed while it issues its memory instructions; one barrier per slice;
 //  - LDS rows are 64 bytes (32 bf16 of K); the 16-byte chunk c of row r is
 //    stored at c ^ swz(r), which makes the fragment reads of 16 consecutive
 //    rows hit 16 distinct bank groups (the LDS serves a 16-byte read for 16

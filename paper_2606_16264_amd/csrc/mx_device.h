@@ -62,14 +62,6 @@ __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-// 32x32x16 bf16 matrix-core product, fp32 accumulate.
-// A: lane l holds row (l % 32), k = 8 * (l / 32) .. +7
-// B: lane l holds col (l % 32), k = 8 * (l / 32) .. +7
-// C: lane l, register 4j + i holds col (l % 32), row 8j + 4 (l / 32) + i
-__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-}
-
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 // Hand-placed waits and LDS traffic for kernels that copy global -> LDS with
