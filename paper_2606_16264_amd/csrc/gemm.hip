@@ -765,15 +765,16 @@ struct Shape {
   double feed_gbs;  // bytes a CU streams per microsecond (x1e3) with cold weights
 };
 // 256x256 and 128x256 run eight waves (2 per SIMD), the smaller shapes four.
-// The last shape is 128x256 with a three-stage ring (72 KB of LDS), so that
-// two workgroups share a CU: problems of more than 256 such tiles then run in
-// one round instead of two.  A round holds two tiles per CU, each running
-// 1.86 times as long as alone (measured in the layer step), hence b.
+// The last shape is 128x256 with a three-stage ring (72 KB of LDS), meant for
+// two workgroups per CU; with the 16 x 16 x 32 main loop a 128x256 wave needs
+// more than the 128 registers that four waves per SIMD leave, so it runs one
+// per CU, and its figures (a fourth stage missing against the 128x256 shape)
+// keep the model from choosing it.
 constexpr Shape kShapes[] = {{256, 256, 3.471, 0.02443, 1, 33.8},
                              {128, 256, 0.978, 0.01544, 1, 42.1},
                              {128, 128, 0.615, 0.0115, 1, 43.3},
                              {64, 128, 0.0, 0.00729, 1, 49.6},
-                             {128, 256, 0.978, 0.0287, 2, 42.1}};
+                             {128, 256, 0.978, 0.0287, 1, 42.1}};
 constexpr int kNumShapes = 5;
 constexpr int kFeedMaxM = 256;  // rows up to which the feed estimate is used
 constexpr double kCUs = 256.0;
